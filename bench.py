@@ -1,0 +1,343 @@
+"""Benchmark of the fused LogbQuant dequantize-and-multiply on one MI355X.
+
+Default workload: the 8192 x 28672 layer (weights 0.015 * t3, 4-bit LogbQuant per tensor,
+float16 N(0,1) activations) at batch M = 1. One step is one logbq_linear call on packed codes
+already resident in HBM. The codes are held in several copies (>= 1 GiB together) and the
+steps cycle through them, so every step streams its weights from HBM and not from the 256 MB
+last-level cache. value = packed weight bytes (N * K / 2) per step / time per step.
+
+The same run also measures, each in its own timed region:
+  * decode weight passes: 16 layers x 7 linears (1B-shaped) and 32 x 7 (8B-shaped) at M = 1,
+    and the 8B-shaped pass at M = 4, each captured once in a HIP graph and replayed per
+    token (tokens/s = M / time per pass);
+  * the same layer at M = 8, 32, 128 (GEMV and MFMA paths);
+  * logbq_encode of the layer's float32 weights;
+  * the 2048 x 8192 up-projection and the 2048 x 2048 linear at M = 1.
+And, on the host, the CPU oracle (dequantize + float64 matmul) on a row sample of the layer.
+
+Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--quick]
+"""
+import argparse
+import concurrent.futures as cf
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "fused LogbQuant GEMV effective weight GB/s (% HBM peak) + decode tokens/s, M=1"
+HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0
+ROTATE_BYTES = 1 << 30
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class Calls:
+    """Pre-marshalled logbq_linear argument tuples, so the timed loop only calls the library."""
+
+    def __init__(self, L, stream):
+        self.fn = L.lib().logbq_linear
+        self.stream = ctypes.c_void_p(stream)
+        self.args = []
+        self.keep = []
+
+    def add(self, x, codes, cb, y):
+        cbarr = np.ascontiguousarray(cb, dtype=np.float32)
+        self.keep.append(cbarr)
+        self.args.append((ctypes.c_void_p(x.data_ptr()), x.shape[0], x.shape[1],
+                          ctypes.c_void_p(codes.data_ptr()), codes.shape[0],
+                          cbarr.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                          ctypes.c_void_p(y.data_ptr()), self.stream))
+
+    def run(self, idx):
+        st = self.fn(*self.args[idx])
+        if st != 0:
+            raise RuntimeError(f"logbq_linear failed with status {st}")
+
+
+def time_region(torch, stream, fn, steps, warmup):
+    """Events around `steps` calls of fn on `stream`; returns ms per call."""
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(steps):
+        fn(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def _capture(torch, L, launches, count, offset=0):
+    graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=cap):
+        calls = Calls(L, torch.cuda.current_stream().cuda_stream)
+        for a in launches:
+            calls.add(*a)
+        for i in range(count):
+            calls.run((offset + i) % len(launches))
+    return graph
+
+
+def time_launches(torch, L, stream, launches, steps, warmup):
+    """Time exactly `steps` logbq_linear launches back to back after `warmup` untimed ones.
+    `launches` is a list of (x, codes, cb, y); launch i uses entry i % len(launches). Each
+    sequence is captured in one HIP graph so that host launch cost cannot starve the GPU; the
+    timed graph is replayed once between two events. Returns ms per launch."""
+    if warmup > 0:
+        _capture(torch, L, launches, warmup).replay()
+    timed = _capture(torch, L, launches, steps, offset=warmup)
+    return time_region(torch, stream, lambda i: timed.replay(), 1, 0) / steps
+
+
+def make_tensor(torch, L, inputs, lin, wl, seed, dev):
+    """Generate one weight tensor on the GPU, fit it on the host, encode it on the GPU."""
+    wd = inputs.student_t_weights(lin.n, lin.k, wl["nu"], wl["scale"], seed=seed, device=dev,
+                                  outlier_frac=wl.get("outlier_frac", 0.0))
+    p = L.fit(wd.cpu().numpy())
+    codes, cb = L.encode(wd, p)
+    return codes, cb
+
+
+def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup):
+    """The 8192 x 28672 layer: rotation copies, M sweep, encode timing."""
+    wl = inputs.WORKLOADS["layer_8192x28672"]
+    lin = wl["layers"][0]
+    n, k = lin.n, lin.k
+    log("layer 8192x28672: generate / fit / encode")
+    wd = inputs.student_t_weights(n, k, wl["nu"], wl["scale"], seed=[wl["cfg"], 0, 0, 0],
+                                  device=dev)
+    w = wd.cpu().numpy()
+    t0 = time.perf_counter()
+    p = L.fit(w)
+    fit_s = time.perf_counter() - t0
+    del w
+    codes, cb = L.encode(wd, p)
+    torch.cuda.synchronize()
+    packed = n * k // 2
+    copies = max(2, -(-ROTATE_BYTES // packed))
+    code_list = [codes] + [codes.clone() for _ in range(copies - 1)]
+    results = {}
+    # encode: 1 float32 tensor of 0.94 GB is read per call (larger than the last-level cache)
+    enc_out = torch.empty_like(codes)
+    def enc(i):
+        L.encode(wd, p, out=enc_out, stream=stream)
+    enc_ms = time_region(torch, stream, enc, max(5, steps // 20), 2)
+    assert torch.equal(enc_out, codes)
+    enc_bytes = n * k * 4 + packed
+    results["encode_8192x28672"] = {"ms": enc_ms, "GB_s": enc_bytes / enc_ms / 1e6,
+                                    "hbm_frac": enc_bytes / enc_ms / 1e6 / HBM_PEAK_GBS,
+                                    "bytes": enc_bytes}
+    del wd
+    for m in ms:
+        x = inputs.activations(m, k, seed=[wl["cfg"], 0, 0, 1], device=dev)
+        launches = [(x, c, cb, torch.empty((m, n), dtype=torch.float32, device=dev))
+                    for c in code_list]
+        timed = steps if m == ms[0] else max(64, steps // 4)
+        t = time_launches(torch, L, stream, launches, timed, warmup)
+        algo = packed + 2 * m * k + 4 * m * n + 64
+        flops = 2.0 * m * n * k
+        results[f"linear_8192x28672_m{m}"] = {
+            "ms": t, "us": t * 1e3, "launches_timed": timed, "weight_GB_s": packed / t / 1e6,
+            "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
+            "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
+            "algo_bytes": algo, "path": "gemv" if m <= 8 else "mfma"}
+    return results, {"n": n, "k": k, "packed": packed, "copies": copies, "fit_s": fit_s,
+                     "params": {"base": p.base, "shift": p.shift, "wmin": p.wmin,
+                                "wmax": p.wmax}}, codes, cb
+
+
+def bench_small(torch, L, inputs, dev, stream, name, steps, warmup):
+    wl = inputs.WORKLOADS[name]
+    lin = wl["layers"][0]
+    codes, cb = make_tensor(torch, L, inputs, lin, wl, [wl["cfg"], 0, 0, 0], dev)
+    packed = lin.n * lin.k // 2
+    copies = max(2, -(-ROTATE_BYTES // packed))
+    code_list = [codes] + [codes.clone() for _ in range(copies - 1)]
+    x = inputs.activations(1, lin.k, seed=[wl["cfg"], 0, 0, 1], device=dev)
+    y = torch.empty((1, lin.n), dtype=torch.float32, device=dev)
+    timed = steps
+    t = time_launches(torch, L, stream, [(x, c, cb, y) for c in code_list], steps, warmup)
+    return {"ms": t, "us": t * 1e3, "launches_timed": timed, "weight_GB_s": packed / t / 1e6,
+            "hbm_frac": packed / t / 1e6 / HBM_PEAK_GBS, "copies": copies}
+
+
+def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):
+    """A full decode weight pass in dependency order, captured in a HIP graph."""
+    wl = inputs.WORKLOADS[name]
+    layers = wl["n_layers"]
+    log(f"{name}: generating {layers} x {len(wl['layers'])} tensors")
+    tensors = []
+    t0 = time.perf_counter()
+    with cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 4)) as pool:
+        for li in range(layers):
+            hosts, devs = [], []
+            for lin in wl["layers"]:
+                wd = inputs.student_t_weights(lin.n, lin.k, wl["nu"], wl["scale"],
+                                              seed=[wl["cfg"], li, inputs.PROJ[lin.name], 0],
+                                              device=dev)
+                devs.append(wd)
+                hosts.append(wd.cpu().numpy())
+            params = list(pool.map(L.fit, hosts))
+            for lin, wd, p in zip(wl["layers"], devs, params):
+                codes, cb = L.encode(wd, p)
+                tensors.append((lin, codes, cb))
+            torch.cuda.synchronize()
+            del hosts, devs
+    setup_s = time.perf_counter() - t0
+    bytes_pass = sum(lin.n * lin.k // 2 for lin, _, _ in tensors)
+    out = {}
+    for m in batches:
+        xs = {}
+        ys = []
+        g = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        for lin, codes, cb in tensors:
+            key = (lin.k, lin.name)
+            if key not in xs:
+                xs[key] = inputs.activations(m, lin.k, seed=[wl["cfg"], 0, inputs.PROJ[lin.name], 1],
+                                             device=dev)
+            ys.append(torch.empty((m, lin.n), dtype=torch.float32, device=dev))
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=cap):
+            calls = Calls(L, torch.cuda.current_stream().cuda_stream)
+            for (lin, codes, cb), y in zip(tensors, ys):
+                calls.add(xs[(lin.k, lin.name)], codes, cb, y)
+            for i in range(len(tensors)):
+                calls.run(i)
+        # check the replay against eager launches
+        g.replay()
+        torch.cuda.synchronize()
+        ref = [y.clone() for y in ys]
+        for (lin, codes, cb), y in zip(tensors, ys):
+            L.linear(xs[(lin.k, lin.name)], codes, cb, out=y)
+        torch.cuda.synchronize()
+        assert all(torch.equal(a, b) for a, b in zip(ref, ys)), "graph replay differs"
+        t = time_region(torch, stream, lambda i: g.replay(), steps, warmup)
+        out[f"m{m}"] = {"ms_per_token_pass": t, "tokens_per_s": m / (t * 1e-3),
+                        "weight_GB_s": bytes_pass / t / 1e6,
+                        "hbm_frac": bytes_pass / t / 1e6 / HBM_PEAK_GBS,
+                        "launches": len(tensors)}
+        del g
+    return {"bytes_per_pass": bytes_pass, "setup_s": setup_s, **out}
+
+
+def cpu_baseline(L_unused, inputs, target_s=12.0):
+    """The oracle (unpack + dequantize + float64 matmul) on a row sample of the layer."""
+    from oracle import logbq_oracle as O
+    wl = inputs.WORKLOADS["layer_8192x28672"]
+    lin = wl["layers"][0]
+    rows = 1024
+    w = inputs.student_t_weights(rows, lin.k, wl["nu"], wl["scale"], seed=[wl["cfg"], 99, 0, 0])
+    r = O.fit(w)
+    codes = O.pack(O.encode(w, r.base, r.shift))
+    lut = O.codebook(r.base, r.shift)
+    x = inputs.activations(1, lin.k, seed=[wl["cfg"], 0, 0, 1])
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        y = O.linear(x, O.dequantize(O.unpack(codes), lut))
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= target_s or reps >= 200:
+            break
+    del y
+    per = el / reps
+    threads = 1
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([1] + [int(i.get("num_threads", 1)) for i in threadpool_info()])
+    except Exception:
+        pass
+    packed = rows * lin.k // 2
+    return {"value": packed / per / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{rows} of 28672 rows of the 8192x28672 layer at M=1, {reps} reps, "
+                      f"{el:.1f} s; unpack + dequantize + float64 matmul (numpy; BLAS threads "
+                      f"{threads}, table lookup single-threaded)",
+            "s_per_rep": per}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--quick", action="store_true", help="main layer only, no extra rows")
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_01127_amd import inputs
+    from paper_2607_01127_amd import logbq as L
+    L.lib()
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+
+    ms = [1] if args.quick else [1, 8, 32, 128]
+    res, info, codes, cb = bench_layer(torch, L, inputs, dev, stream, ms, args.steps, args.warmup)
+    main_row = res["linear_8192x28672_m1"]
+    t_ms = main_row["ms"]
+    packed = info["packed"]
+    algo = main_row["algo_bytes"]
+    value = packed / t_ms / 1e6
+
+    rows = dict(res)
+    if not args.quick:
+        for name in ("up_2048x8192_outliers", "linear_2048x2048"):
+            log(name)
+            rows[name + "_m1"] = bench_small(torch, L, inputs, dev, stream, name, 2000, 100)
+        del codes
+        torch.cuda.empty_cache()
+        rows["decode_1b_16x7"] = bench_decode(torch, L, inputs, dev, stream, "decode_1b_16x7",
+                                              [1], 200, 20)
+        torch.cuda.empty_cache()
+        rows["decode_8b_32x7"] = bench_decode(torch, L, inputs, dev, stream, "decode_8b_32x7",
+                                              [1, 4], 100, 10)
+        torch.cuda.empty_cache()
+
+    cpu = None
+    if not args.no_cpu:
+        log("cpu baseline (oracle)")
+        cpu = cpu_baseline(None, inputs)
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": t_ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": "layer_8192x28672", "m": 1, "n_out": info["n"], "k_in": info["k"],
+                   "weights": "0.015*StudentT(3) float32 -> 4-bit LogbQuant per tensor",
+                   "activations": "float16 N(0,1)", "accumulate": "f32",
+                   "rotation_copies": info["copies"], "params": info["params"],
+                   "host_fit_s": info["fit_s"]},
+        "roofline": {"bound": "hbm", "achieved": round(algo / t_ms / 1e6, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(algo / t_ms / 1e6 / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "k_gemv<1,4>", "algo_bytes_per_launch": algo,
+                     "avg_launch_us": t_ms * 1e3},
+        "cpu_baseline": cpu,
+        "rows": rows,
+    }
+    if "decode_8b_32x7" in rows:
+        out["decode_tokens_per_s_m1"] = rows["decode_8b_32x7"]["m1"]["tokens_per_s"]
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,134 @@
+/*
+ * logbq.h -- C ABI of liblogbq, 4-bit LogbQuant weight-only inference on AMD MI355X (gfx950).
+ *
+ * LogbQuant (Bohn et al., arXiv 2607.01127) quantizes each weight matrix with its own
+ * logarithmic codebook of base b and shift s (Sec. 3.1): a weight x maps to the integer
+ * q = sign(x) * round(log_b|x| + s) with |q| <= q_max = 2^(n-1) - 1 (Eq. 1), and q decodes to
+ * sign(q) * b^(|q| - s), or 0 for q = 0 (Eq. 2). b and s come from the effective weight range
+ * [w_min, w_max] (Eq. 3, Eq. 4); w_min discards a fraction eps of the signal energy (Eq. 5).
+ * Inference dequantizes through a lookup table instead of evaluating b^x (Sec. 3.3).
+ *
+ * Conventions shared by every call
+ *   - Every call validates all of its arguments before it touches the GPU, and returns a
+ *     logbq_status. Nothing is allocated and nothing is synchronised inside a call; device
+ *     calls are enqueued on the given stream and return at once, so they can be captured in a
+ *     HIP graph. Faults of an enqueued kernel surface at the caller's next synchronisation.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the default stream.
+ *   - The caller owns every buffer. "device" pointers are HIP device memory of the current
+ *     device; "host" pointers are ordinary host memory.
+ *   - Weights are row-major [N][K] (N out features, K in features, as a PyTorch Linear).
+ *   - Packed codes: row-major [N][K/2] bytes; element (n, k) is the nibble at byte
+ *     n*K/2 + k/2, the low nibble when k is even. A nibble is sign<<3 | magnitude: bit 3 set
+ *     means negative, magnitude 0..7 is |q|. Code 8 ("-0") is never written and decodes to +0.
+ *   - Shapes: K must be a multiple of 32 (every packed row is then 16-byte aligned);
+ *     device pointers must be 16-byte aligned. N = 0 or M = 0 is a valid empty call.
+ */
+#ifndef LOGBQ_H
+#define LOGBQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LOGBQ_ABI_VERSION 1
+
+typedef enum logbq_status {
+  LOGBQ_OK = 0,
+  LOGBQ_ERR_INVALID_ARG = 1,   /* null pointer, negative size, eps outside (0,1), ... */
+  LOGBQ_ERR_NONFINITE = 2,     /* fit: a weight is NaN or Inf                           */
+  LOGBQ_ERR_DEGENERATE = 3,    /* fit: all weights zero, or w_min == w_max (b = 1)      */
+  LOGBQ_ERR_UNSUPPORTED = 4,   /* bits != 4, K % 32 != 0, misaligned pointer, too large */
+  LOGBQ_ERR_HIP = 5            /* a HIP call failed (no device, launch failure, ...)    */
+} logbq_status;
+
+/* Per-tensor codebook parameters (Sec. 3.1, Sec. 3.2). Plain data; copy freely. */
+typedef struct logbq_params {
+  int32_t bits;            /* codebook bit width n; 4 is supported                        */
+  int32_t qmax;            /* q_max = 2^(n-1) - 1                                          */
+  double eps;              /* pruned energy fraction of Eq. 5                               */
+  double wmin;             /* w_min of Eq. 5                                                */
+  double wmax;             /* w_max = max |w| (Sec. 3.2)                                    */
+  double base;             /* b of Eq. 3                                                    */
+  int32_t shift;           /* s of Eq. 4 (an integer)                                       */
+  int32_t reserved;
+  int64_t wmin_index;      /* position of w_min in |w| sorted ascending                     */
+  float codebook[16];      /* Dequant (Eq. 2) of every 4-bit code, float32                  */
+  float thresholds[8];     /* [k] = smallest float32 whose magnitude index exceeds k,
+                              k = 0..qmax-1; [7] = +inf (unused)                            */
+} logbq_params;
+
+/* ABI version of the loaded library (LOGBQ_ABI_VERSION it was built with). */
+int32_t logbq_abi_version(void);
+
+/* Static English name of a status code; never NULL. */
+const char* logbq_status_str(int32_t status);
+
+/*
+ * logbq_fit -- per-tensor codebook parameters (Sec. 3.1 Eq. 3-4, Sec. 3.2 Eq. 5). Host only.
+ *   w_host : host, numel float32 weights, read only.
+ *   bits   : codebook width n; must be 4.
+ *   eps    : pruned energy fraction, 0 < eps < 1 (the paper uses 4e-3 at 4 bits).
+ *   out    : host, filled on success; untouched on error.
+ * w_max = max|w|. w_min is the smallest |w_i| at which the ascending float64 prefix sum of
+ * w^2, divided by the total, reaches eps (sequential summation in ascending |w| order).
+ * b = (w_max / w_min)^(1/q_max); s = q_max - J with J the largest integer such that
+ * b^J <= w_max. codebook[k] = float32(b^(k-s)), codebook[8+k] = -codebook[k] (k = 1..7),
+ * codebook[0] = codebook[8] = +0. thresholds[k] is exact: the smallest float32 t with
+ * t >= b^(k + 1/2 - s).
+ * Errors: INVALID_ARG (null, numel < 2, eps outside (0,1)), UNSUPPORTED (bits != 4),
+ * NONFINITE (NaN/Inf weight), DEGENERATE (w_max == 0, or w_min == w_max).
+ * Reentrant; allocates host scratch of 4*numel bytes internally for the sort.
+ */
+int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
+                  logbq_params* out);
+
+/*
+ * logbq_encode -- Quant (Eq. 1) of a weight matrix into packed 4-bit codes (Sec. 3.3 packing).
+ *   w_dev        : device, [n][k] float32 weights.
+ *   n, k         : shape; k % 32 == 0.
+ *   p            : host, parameters from logbq_fit (bits must be 4).
+ *   codes_dev    : device, [n][k/2] bytes, written.
+ *   codebook_out : host, 16 floats, receives p->codebook (may be NULL).
+ *   stream       : hipStream_t or NULL.
+ * The magnitude index of x is the number of thresholds t with |x| >= t, which equals
+ * clamp(round-half-up(log_b|x| + s), 0, q_max); the sign bit is set for negative x with a
+ * nonzero magnitude. NaN and +-0 encode to 0, +-Inf to the largest magnitude with its sign.
+ * Errors: INVALID_ARG (null, negative size), UNSUPPORTED (bits, k % 32, alignment),
+ * HIP (launch failure).
+ */
+int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_params* p,
+                     uint8_t* codes_dev, float* codebook_out, void* stream);
+
+/*
+ * logbq_linear -- y = x . W_hat^T on packed codes: weight-only inference with the codebook
+ * lookup fused into the product (Sec. 3.3).
+ *   x_dev     : device, [m][k] IEEE float16 activations (bit patterns as uint16).
+ *   m, k      : batch rows and in features; k % 32 == 0.
+ *   codes_dev : device, [n][k/2] packed codes.
+ *   n         : out features.
+ *   codebook  : host, 16 floats (logbq_params.codebook); copied into the kernel arguments,
+ *               so the call is capturable in a HIP graph. Entries are rounded to float16 after
+ *               a common power-of-two scaling, exact in the result up to float16 rounding.
+ *   y_dev     : device, [m][n] float32, written.
+ * Accumulation is float32. m <= 8 runs the wavefront-reduced GEMV; larger m (or shapes whose
+ * activations do not fit the GEMV's registers) runs the dequantize-into-MFMA skinny GEMM.
+ * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment), HIP.
+ */
+int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
+                     int64_t n, const float* codebook, float* y_dev, void* stream);
+
+/*
+ * logbq_dequantize -- Dequant (Eq. 2) of packed codes into float32 weights, by lookup.
+ *   codes_dev : device, [n][k/2]; codebook: host, 16 floats; w_dev: device, [n][k] float32.
+ * Bit-exact: w[n][k] = codebook[code(n, k)]. Errors: INVALID_ARG, UNSUPPORTED, HIP.
+ */
+int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const float* codebook,
+                         float* w_dev, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LOGBQ_H */

@@ -1,0 +1,231 @@
+// Host side of liblogbq: the per-tensor fit (Sec. 3.1 Eq. 3-4, Sec. 3.2 Eq. 5), the exact
+// encoding thresholds, status strings.
+//
+// Built with g++ -O2 -ffp-contract=off and without -ffast-math: every float64 operation
+// below must round exactly as written (no fused multiply-add, no reassociation), because
+// the fitted parameters are compared bit for bit with an independent implementation.
+
+#include <algorithm>
+#include <cfloat>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <limits>
+#include <vector>
+
+#include "logbq.h"
+
+namespace {
+
+inline uint32_t f2u(float f) { uint32_t u; std::memcpy(&u, &f, 4); return u; }
+inline float u2f(uint32_t u) { float f; std::memcpy(&f, &u, 4); return f; }
+
+// LSD radix sort of non-negative float32 bit patterns (their integer order is their value
+// order). Three 11-bit passes; passes whose digit is constant over the input are skipped.
+void radix_sort_u32(std::vector<uint32_t>& a) {
+  const size_t n = a.size();
+  std::vector<uint32_t> tmp(n);
+  uint32_t* src = a.data();
+  uint32_t* dst = tmp.data();
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = pass * 11;
+    std::vector<size_t> count(2049, 0);
+    for (size_t i = 0; i < n; ++i) count[((src[i] >> shift) & 2047u) + 1]++;
+    bool constant = false;
+    for (int d = 1; d <= 2048; ++d) if (count[d] == n) { constant = true; break; }
+    if (constant) continue;
+    for (int d = 1; d <= 2048; ++d) count[d] += count[d - 1];
+    for (size_t i = 0; i < n; ++i) dst[count[(src[i] >> shift) & 2047u]++] = src[i];
+    std::swap(src, dst);
+  }
+  if (src != a.data()) std::memcpy(a.data(), src, n * sizeof(uint32_t));
+}
+
+// ---- small unsigned big integer, enough for exact threshold tests -----------------------
+struct Big {
+  std::vector<uint32_t> d;  // little-endian 32-bit limbs
+  explicit Big(uint64_t v = 0) { while (v) { d.push_back(uint32_t(v)); v >>= 32; } }
+  void mul_small(uint64_t m) {  // m < 2^64
+    const uint32_t mlo = uint32_t(m), mhi = uint32_t(m >> 32);
+    std::vector<uint32_t> r(d.size() + 3, 0);
+    for (size_t i = 0; i < d.size(); ++i) {
+      unsigned __int128 carry = 0;
+      unsigned __int128 t = (unsigned __int128)d[i] * mlo + r[i] + carry;
+      r[i] = uint32_t(t);
+      carry = t >> 32;
+      t = (unsigned __int128)d[i] * mhi + r[i + 1] + carry;
+      r[i + 1] = uint32_t(t);
+      carry = t >> 32;
+      size_t j = i + 2;
+      while (carry) { t = (unsigned __int128)r[j] + carry; r[j] = uint32_t(t); carry = t >> 32; ++j; }
+    }
+    d.swap(r);
+    trim();
+  }
+  void shl(int64_t bits) {
+    if (d.empty() || bits <= 0) return;
+    const size_t limbs = size_t(bits / 32);
+    const int rem = int(bits % 32);
+    std::vector<uint32_t> r(d.size() + limbs + 1, 0);
+    for (size_t i = 0; i < d.size(); ++i) {
+      uint64_t v = uint64_t(d[i]) << rem;
+      r[i + limbs] |= uint32_t(v);
+      r[i + limbs + 1] |= uint32_t(v >> 32);
+    }
+    d.swap(r);
+    trim();
+  }
+  void trim() { while (!d.empty() && d.back() == 0) d.pop_back(); }
+  static int cmp(const Big& a, const Big& b) {
+    if (a.d.size() != b.d.size()) return a.d.size() < b.d.size() ? -1 : 1;
+    for (size_t i = a.d.size(); i-- > 0;)
+      if (a.d[i] != b.d[i]) return a.d[i] < b.d[i] ? -1 : 1;
+    return 0;
+  }
+};
+
+// f = F * 2^ef for a finite non-negative float32.
+void split_f32(float f, uint64_t& F, int64_t& ef) {
+  const uint32_t u = f2u(f);
+  const uint32_t e = (u >> 23) & 0xFFu, m = u & 0x7FFFFFu;
+  if (e == 0) { F = m; ef = -149; }
+  else { F = m | 0x800000u; ef = int64_t(e) - 150; }
+}
+
+// b = B * 2^eb for a finite positive double.
+void split_f64(double b, uint64_t& B, int64_t& eb) {
+  uint64_t u; std::memcpy(&u, &b, 8);
+  const uint64_t e = (u >> 52) & 0x7FFu, m = u & ((uint64_t(1) << 52) - 1);
+  if (e == 0) { B = m; eb = -1074; }
+  else { B = m | (uint64_t(1) << 52); eb = int64_t(e) - 1075; }
+}
+
+// Exact test f >= b^(n/2) for odd n, i.e. f^2 >= b^n (f >= 0 finite, b > 1 finite).
+bool ge_half_power(float f, double b, int64_t n) {
+  uint64_t F, B; int64_t ef, eb;
+  split_f32(f, F, ef);
+  if (F == 0) return false;
+  split_f64(b, B, eb);
+  if (n >= 0) {
+    // F^2 2^(2ef) >= B^n 2^(n eb)
+    Big lhs(F); lhs.mul_small(F);
+    Big rhs(1); for (int64_t i = 0; i < n; ++i) rhs.mul_small(B);
+    const int64_t d = 2 * ef - n * eb;
+    if (d >= 0) lhs.shl(d); else rhs.shl(-d);
+    return Big::cmp(lhs, rhs) >= 0;
+  }
+  // F^2 2^(2ef) B^m 2^(m eb) >= 1  with m = -n
+  const int64_t m = -n;
+  Big lhs(F); lhs.mul_small(F);
+  for (int64_t i = 0; i < m; ++i) lhs.mul_small(B);
+  const int64_t e = -2 * ef - m * eb;   // need lhs >= 2^e
+  if (e <= 0) return true;              // lhs >= 1
+  Big rhs(1); rhs.shl(e);
+  return Big::cmp(lhs, rhs) >= 0;
+}
+
+// Smallest float32 t with t >= b^(k + 1/2 - s); +inf beyond the float32 range.
+float exact_threshold(double b, int32_t s, int k) {
+  const int64_t n = 2 * int64_t(k) + 1 - 2 * int64_t(s);
+  const long double approx = powl((long double)b, (long double)k + 0.5L - (long double)s);
+  if (!(approx <= (long double)FLT_MAX * 2)) return std::numeric_limits<float>::infinity();
+  float f = approx > (long double)FLT_MAX ? FLT_MAX : (float)approx;
+  const float inf = std::numeric_limits<float>::infinity();
+  while (!ge_half_power(f, b, n)) {
+    f = std::nextafter(f, inf);
+    if (std::isinf(f)) return f;
+  }
+  while (f > 0.0f) {
+    const float g = std::nextafter(f, 0.0f);
+    if (ge_half_power(g, b, n)) f = g; else break;
+  }
+  return f;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t logbq_abi_version(void) { return LOGBQ_ABI_VERSION; }
+
+const char* logbq_status_str(int32_t status) {
+  switch (status) {
+    case LOGBQ_OK: return "ok";
+    case LOGBQ_ERR_INVALID_ARG: return "invalid argument";
+    case LOGBQ_ERR_NONFINITE: return "non-finite weight";
+    case LOGBQ_ERR_DEGENERATE: return "degenerate weight range";
+    case LOGBQ_ERR_UNSUPPORTED: return "unsupported shape, alignment or bit width";
+    case LOGBQ_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
+                  logbq_params* out) {
+  if (!w_host || !out || numel < 2) return LOGBQ_ERR_INVALID_ARG;
+  if (!(eps > 0.0 && eps < 1.0)) return LOGBQ_ERR_INVALID_ARG;
+  if (bits != 4) return LOGBQ_ERR_UNSUPPORTED;
+  const int32_t qmax = (1 << (bits - 1)) - 1;
+
+  // |w| as float32 bit patterns (sign cleared); reject NaN / Inf.
+  std::vector<uint32_t> a((size_t)numel);
+  for (int64_t i = 0; i < numel; ++i) {
+    const uint32_t u = f2u(w_host[i]) & 0x7FFFFFFFu;
+    if (u >= 0x7F800000u) return LOGBQ_ERR_NONFINITE;
+    a[(size_t)i] = u;
+  }
+  radix_sort_u32(a);
+  const double wmax = (double)u2f(a.back());
+  if (wmax == 0.0) return LOGBQ_ERR_DEGENERATE;
+
+  // Eq. 5 with sequential float64 prefix sums in ascending |w| order; squares of float32
+  // values are exact in float64.
+  double total = 0.0;
+  for (size_t i = 0; i < a.size(); ++i) {
+    const double v = (double)u2f(a[i]);
+    total += v * v;
+  }
+  double prefix = 0.0;
+  size_t istar = a.size() - 1;
+  for (size_t i = 0; i < a.size(); ++i) {
+    const double v = (double)u2f(a[i]);
+    prefix += v * v;
+    if (prefix / total >= eps) { istar = i; break; }
+  }
+  const double wmin = (double)u2f(a[istar]);
+  if (!(wmin < wmax)) return LOGBQ_ERR_DEGENERATE;
+
+  // Eq. 3 and Eq. 4 (floor taken exactly: largest J with b^J <= w_max).
+  const double b = std::pow(wmax / wmin, 1.0 / (double)qmax);
+  if (!(b > 1.0)) return LOGBQ_ERR_DEGENERATE;
+  int64_t J = (int64_t)std::floor(std::log(wmax) / std::log(b));
+  while (std::pow(b, (double)(J + 1)) <= wmax) ++J;
+  while (std::pow(b, (double)J) > wmax) --J;
+  const int64_t s = qmax - J;
+  if (s > INT32_MAX / 4 || s < INT32_MIN / 4) return LOGBQ_ERR_DEGENERATE;
+
+  logbq_params p;
+  std::memset(&p, 0, sizeof(p));
+  p.bits = bits;
+  p.qmax = qmax;
+  p.eps = eps;
+  p.wmin = wmin;
+  p.wmax = wmax;
+  p.base = b;
+  p.shift = (int32_t)s;
+  p.wmin_index = (int64_t)istar;
+  const int half = 1 << (bits - 1);
+  for (int k = 1; k <= qmax; ++k) {
+    const float v = (float)std::pow(b, (double)(k - p.shift));
+    p.codebook[k] = v;
+    p.codebook[half + k] = -v;
+  }
+  p.codebook[0] = 0.0f;
+  p.codebook[half] = 0.0f;
+  for (int k = 0; k < qmax; ++k) p.thresholds[k] = exact_threshold(b, p.shift, k);
+  p.thresholds[7] = std::numeric_limits<float>::infinity();
+  *out = p;
+  return LOGBQ_OK;
+}
+
+}  // extern "C"

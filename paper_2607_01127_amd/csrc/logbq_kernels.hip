@@ -1,0 +1,581 @@
+// gfx950 kernels of liblogbq and the device entry points of the C ABI.
+//
+//   k_encode   Quant (Eq. 1): float32 weights -> packed sign+magnitude nibbles, by comparing
+//              |x| with the exact per-tensor thresholds (7 compares per weight).
+//   k_dequant  Dequant (Eq. 2) by codebook lookup: nibbles -> float32 (bit-exact).
+//   k_gemv     y = x . W_hat^T for m <= 8 batch rows: packed codes stream from HBM with 128-bit
+//              non-temporal loads; each code byte (two weights) indexes a 256-entry table of
+//              float16 pairs held in LDS (one private copy per lane, so lookups never conflict on
+//              a bank); v_dot2_f32_f16 accumulates in float32; DPP row reductions plus lane reads
+//              finish the wavefront sum.
+//   k_mfma     y = x . W_hat^T for larger m: the same byte -> float16-pair lookup builds the B
+//              operand of v_mfma_f32_32x32x16_f16 straight from a code dword; activations are
+//              staged through LDS as the A operand; float32 accumulation in the MFMA.
+//
+// The float16 tables hold codebook / 2^e with 2^e chosen so that the largest entry lies in
+// [2^14, 2^15); the result is multiplied back by 2^e (exact). Lookup replaces evaluating
+// b^(|q| - s) per weight, as in Sec. 3.3 of the paper.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+
+#include "logbq.h"
+
+namespace {
+
+typedef _Float16 half_t;
+typedef half_t half2v __attribute__((ext_vector_type(2)));
+typedef half_t half8v __attribute__((ext_vector_type(8)));
+typedef float float16v __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+struct Thresholds { float t[7]; };
+struct Codebook32 { float v[16]; };
+struct Lut16 { uint32_t h[8]; };   // h[i] = f16(lut[2i]) | f16(lut[2i+1]) << 16
+
+constexpr int kLutEntries = 256;   // one entry per code byte (two nibbles)
+constexpr int kLutCopies = 64;     // one copy per lane of a wavefront
+constexpr int kLutWords = kLutEntries * kLutCopies;
+
+// ------------------------------------------------------------------ encode
+__global__ __launch_bounds__(256) void k_encode(const f32x4* __restrict__ w,
+                                                uint32_t* __restrict__ codes, int64_t nwords,
+                                                Thresholds th) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nwords; i += stride) {
+    const f32x4 a = __builtin_nontemporal_load(w + 2 * i);
+    const f32x4 b = __builtin_nontemporal_load(w + 2 * i + 1);
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    uint32_t out = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float x = v[j];
+      const float ax = __builtin_fabsf(x);
+      uint32_t mag = 0;
+#pragma unroll
+      for (int t = 0; t < 7; ++t) mag += (ax >= th.t[t]) ? 1u : 0u;
+      const uint32_t sgn = (x < 0.0f && mag != 0u) ? 8u : 0u;
+      out |= (mag | sgn) << (4 * j);
+    }
+    codes[i] = out;
+  }
+}
+
+// ------------------------------------------------------------------ dequantize
+__global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ codes,
+                                                 f32x4* __restrict__ w, int64_t nwords,
+                                                 Codebook32 cb) {
+  __shared__ float s_cb[16];
+  if (threadIdx.x < 16) s_cb[threadIdx.x] = cb.v[threadIdx.x];
+  __syncthreads();
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nwords; i += stride) {
+    const uint32_t c = codes[i];
+    f32x4 a, b;
+    a.x = s_cb[c & 15u];         a.y = s_cb[(c >> 4) & 15u];
+    a.z = s_cb[(c >> 8) & 15u];  a.w = s_cb[(c >> 12) & 15u];
+    b.x = s_cb[(c >> 16) & 15u]; b.y = s_cb[(c >> 20) & 15u];
+    b.z = s_cb[(c >> 24) & 15u]; b.w = s_cb[c >> 28];
+    __builtin_nontemporal_store(a, w + 2 * i);
+    __builtin_nontemporal_store(b, w + 2 * i + 1);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_fill_zero(float* __restrict__ y, int64_t count) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
+    y[i] = 0.0f;
+}
+
+// ------------------------------------------------------------------ shared device helpers
+
+// float16 bits of table entry c (0..15).
+__device__ __forceinline__ uint32_t lut16_entry(const Lut16& lut, uint32_t c) {
+  const uint32_t i = c >> 1;
+  uint32_t w = lut.h[0];
+  w = (i == 1) ? lut.h[1] : w; w = (i == 2) ? lut.h[2] : w; w = (i == 3) ? lut.h[3] : w;
+  w = (i == 4) ? lut.h[4] : w; w = (i == 5) ? lut.h[5] : w; w = (i == 6) ? lut.h[6] : w;
+  w = (i == 7) ? lut.h[7] : w;
+  return (c & 1u) ? (w >> 16) : (w & 0xFFFFu);
+}
+
+// Fill the LDS pair table: word (e * 64 + lane) = f16(lut[e & 15]) | f16(lut[e >> 4]) << 16,
+// i.e. the two weights of code byte e in k order (low nibble = even k).
+template <int THREADS>
+__device__ __forceinline__ void fill_pair_lut(uint32_t* s_lut, const Lut16& lut) {
+  constexpr int kThreadsPerEntry = THREADS / kLutEntries;
+  constexpr int kWordsPerThread = kLutCopies / kThreadsPerEntry;
+  const int t = threadIdx.x;
+  const uint32_t e = (uint32_t)(t / kThreadsPerEntry);
+  const uint32_t v = lut16_entry(lut, e & 15u) | (lut16_entry(lut, e >> 4) << 16);
+  const u32x4 vv = v;
+  u32x4* dst = reinterpret_cast<u32x4*>(s_lut + e * kLutCopies + (t % kThreadsPerEntry) * kWordsPerThread);
+#pragma unroll
+  for (int i = 0; i < kWordsPerThread / 4; ++i) dst[i] = vv;
+}
+
+// The float16 pair for byte `i` (0..3) of code dword `d`, read from this lane's private copy.
+// v_perm_b32 builds the byte address (byte << 8) | (lane << 2) in one instruction.
+__device__ __forceinline__ uint32_t pair_lookup(const uint32_t* s_lut, uint32_t d,
+                                                uint32_t laneoff, int i) {
+  const uint32_t sel = 0x0C0C0000u | ((uint32_t)(4 + i) << 8);
+  const uint32_t addr = __builtin_amdgcn_perm(d, laneoff, sel);
+  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(s_lut) + addr);
+}
+
+__device__ __forceinline__ half2v as_half2(uint32_t u) { return __builtin_bit_cast(half2v, u); }
+
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+      0, __builtin_bit_cast(int, v), CTRL, ROW_MASK, 0xF, false));
+}
+
+// Sum over the 64 lanes of a wavefront; the result is valid in every lane.
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_f<0xB1>(v);    // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);    // quad_perm [2,3,0,1]
+  v += dpp_f<0x124>(v);   // row_ror:4
+  v += dpp_f<0x128>(v);   // row_ror:8   -> every lane holds its 16-lane row sum
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
+// ------------------------------------------------------------------ GEMV, m <= 8
+//
+// Work split: a workgroup of 8 wavefronts holds one LDS pair table. WK wavefronts share a row
+// (each takes an interleaved slice of the row's 16-byte chunks); the 8 / WK groups of a
+// workgroup take rows round-robin with every other group of the grid. Lane `l` of wavefront `kw`
+// in a group handles chunks c = s * 64 * WK + kw * 64 + l for s < CPL; its activations for those
+// chunks (M rows x 32 values each) stay in registers for the whole kernel. The next row's codes
+// are loaded before the current row is reduced.
+template <int M, int CPL>
+__global__ __launch_bounds__(512) void k_gemv(const uint8_t* __restrict__ codes,
+                                              const uint16_t* __restrict__ x,
+                                              float* __restrict__ y, int n_rows, int k_cols,
+                                              int wk, int iters, Lut16 lut, float scale) {
+  __shared__ __attribute__((aligned(16))) uint32_t s_lut[kLutWords];
+  __shared__ float s_red[8][M];
+
+  fill_pair_lut<512>(s_lut, lut);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int kw = wave % wk;
+  const int grp = wave / wk;
+  const int groups = 8 / wk;
+  const int nchunks = k_cols >> 5;
+  const int64_t row_bytes = (int64_t)(k_cols >> 1);
+
+  int chunk[CPL];
+  bool cval[CPL];
+#pragma unroll
+  for (int s = 0; s < CPL; ++s) {
+    chunk[s] = s * 64 * wk + kw * 64 + lane;
+    cval[s] = chunk[s] < nchunks;
+  }
+
+  uint32_t xr[M][CPL][16];
+#pragma unroll
+  for (int m = 0; m < M; ++m)
+#pragma unroll
+    for (int s = 0; s < CPL; ++s) {
+      u32x4 q0 = 0, q1 = 0, q2 = 0, q3 = 0;
+      if (cval[s]) {
+        const u32x4* px = reinterpret_cast<const u32x4*>(x + (int64_t)m * k_cols + (int64_t)chunk[s] * 32);
+        q0 = px[0]; q1 = px[1]; q2 = px[2]; q3 = px[3];
+      }
+      xr[m][s][0] = q0.x;  xr[m][s][1] = q0.y;  xr[m][s][2] = q0.z;  xr[m][s][3] = q0.w;
+      xr[m][s][4] = q1.x;  xr[m][s][5] = q1.y;  xr[m][s][6] = q1.z;  xr[m][s][7] = q1.w;
+      xr[m][s][8] = q2.x;  xr[m][s][9] = q2.y;  xr[m][s][10] = q2.z; xr[m][s][11] = q2.w;
+      xr[m][s][12] = q3.x; xr[m][s][13] = q3.y; xr[m][s][14] = q3.z; xr[m][s][15] = q3.w;
+    }
+
+  const int total_groups = gridDim.x * groups;
+  const int gid = blockIdx.x * groups + grp;
+  const uint32_t laneoff = (uint32_t)lane << 2;
+
+  auto load_row = [&](int r, u32x4 (&q)[CPL]) {
+#pragma unroll
+    for (int s = 0; s < CPL; ++s) {
+      q[s] = 0;
+      if (r < n_rows && cval[s])
+        q[s] = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>(codes + (int64_t)r * row_bytes + (int64_t)chunk[s] * 16));
+    }
+  };
+
+  u32x4 cur[CPL], nxt[CPL];
+  load_row(gid, cur);
+  __syncthreads();  // pair table ready
+
+  for (int it = 0; it < iters; ++it) {
+    const int r = gid + it * total_groups;
+    if (it + 1 < iters) load_row(r + total_groups, nxt);
+
+    float acc[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) acc[m] = 0.0f;
+#pragma unroll
+    for (int s = 0; s < CPL; ++s) {
+      if (!cval[s]) continue;
+      const uint32_t dw[4] = {cur[s].x, cur[s].y, cur[s].z, cur[s].w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const half2v wp = as_half2(pair_lookup(s_lut, dw[j], laneoff, i));
+#pragma unroll
+          for (int m = 0; m < M; ++m)
+            acc[m] = __builtin_amdgcn_fdot2(wp, as_half2(xr[m][s][4 * j + i]), acc[m], false);
+        }
+    }
+
+    if (wk == 1) {
+#pragma unroll
+      for (int m = 0; m < M; ++m) {
+        const float t = wave_sum(acc[m]);
+        if (lane == 0 && r < n_rows) y[(int64_t)m * n_rows + r] = t * scale;
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < M; ++m) {
+        const float t = wave_sum(acc[m]);
+        if (lane == 0) s_red[wave][m] = t;
+      }
+      __syncthreads();
+      if (kw == 0 && lane < M && r < n_rows) {
+        float t = 0.0f;
+        for (int w2 = 0; w2 < wk; ++w2) t += s_red[grp * wk + w2][lane];
+        y[(int64_t)lane * n_rows + r] = t * scale;
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int s = 0; s < CPL; ++s) cur[s] = nxt[s];
+  }
+}
+
+// ------------------------------------------------------------------ MFMA skinny GEMM
+//
+// Workgroup = 4 wavefronts = 128 weight rows (32 per wavefront) x MT * 32 batch rows.
+// K advances 64 per step: lane (j = l % 32, h = l / 32) loads 16 code bytes of row n0 + j at
+// byte 32 * step + 16 h, i.e. k in [64 step + 32 h, +32). Dword d of that load is the B operand
+// of the d-th v_mfma_f32_32x32x16_f16 (8 weights of column j); the A operand of lane (i, h) is
+// x[i][64 step + 32 h + 8 d .. +8], read from the LDS activation tile. Both operands use the
+// same k order, so every MFMA contracts 16 matching (x, w) pairs.
+constexpr int kXPad = 72;   // halves per staged activation row (64 + 8 padding)
+
+template <int MT>
+__global__ __launch_bounds__(256) void k_mfma(const uint8_t* __restrict__ codes,
+                                              const uint16_t* __restrict__ x,
+                                              float* __restrict__ y, int n_rows, int k_cols,
+                                              int m_rows, Lut16 lut, float scale) {
+  __shared__ __attribute__((aligned(16))) uint32_t s_lut[kLutWords];
+  __shared__ __attribute__((aligned(16))) uint16_t s_x[2][MT * 32][kXPad];
+
+  fill_pair_lut<256>(s_lut, lut);
+
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int wave = t >> 6;
+  const int j = lane & 31;
+  const int h = lane >> 5;
+  const int n0 = blockIdx.x * 128 + wave * 32;
+  const int mb = blockIdx.y * (MT * 32);
+  const int nsteps = (k_cols + 63) >> 6;
+  const int64_t row_bytes = (int64_t)(k_cols >> 1);
+  const uint32_t laneoff = (uint32_t)lane << 2;
+  const int row = n0 + j;
+
+  auto stage_x = [&](int step, int buf) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int idx = t + 256 * i;
+      const int m = idx >> 3;
+      const int sg = idx & 7;
+      const int kk = step * 64 + sg * 8;
+      u32x4 v = 0;
+      if (mb + m < m_rows && kk < k_cols)
+        v = *reinterpret_cast<const u32x4*>(x + (int64_t)(mb + m) * k_cols + kk);
+      *reinterpret_cast<u32x4*>(&s_x[buf][m][sg * 8]) = v;
+    }
+  };
+  auto load_codes = [&](int step) {
+    u32x4 q = 0;
+    if (row < n_rows && step * 64 + 32 * h < k_cols)
+      q = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4*>(codes + (int64_t)row * row_bytes + step * 32 + 16 * h));
+    return q;
+  };
+
+  float16v acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
+
+  u32x4 q = load_codes(0);
+  stage_x(0, 0);
+  __syncthreads();
+
+  for (int step = 0; step < nsteps; ++step) {
+    const int buf = step & 1;
+    u32x4 qn = 0;
+    if (step + 1 < nsteps) {
+      qn = load_codes(step + 1);
+      stage_x(step + 1, buf ^ 1);
+    }
+    const uint32_t dw[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      half8v b;
+      {
+        const half2v p0 = as_half2(pair_lookup(s_lut, dw[d], laneoff, 0));
+        const half2v p1 = as_half2(pair_lookup(s_lut, dw[d], laneoff, 1));
+        const half2v p2 = as_half2(pair_lookup(s_lut, dw[d], laneoff, 2));
+        const half2v p3 = as_half2(pair_lookup(s_lut, dw[d], laneoff, 3));
+        b[0] = p0[0]; b[1] = p0[1]; b[2] = p1[0]; b[3] = p1[1];
+        b[4] = p2[0]; b[5] = p2[1]; b[6] = p3[0]; b[7] = p3[1];
+      }
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const half8v a = *reinterpret_cast<const half8v*>(&s_x[buf][mt * 32 + j][32 * h + 8 * d]);
+        acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc[mt], 0, 0, 0);
+      }
+    }
+    q = qn;
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = mb + mt * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+      if (m < m_rows && row < n_rows) y[(int64_t)m * n_rows + row] = acc[mt][r] * scale;
+    }
+}
+
+// ------------------------------------------------------------------ host helpers
+
+// IEEE binary32 -> binary16, round to nearest even.
+uint16_t f32_to_f16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  const uint32_t sign = (u >> 16) & 0x8000u;
+  const uint32_t e = (u >> 23) & 0xFFu;
+  uint32_t m = u & 0x7FFFFFu;
+  if (e == 0xFF) return (uint16_t)(sign | 0x7C00u | (m ? 0x200u : 0u));
+  const int32_t ee = (int32_t)e - 127 + 15;
+  if (ee >= 31) return (uint16_t)(sign | 0x7C00u);
+  if (ee <= 0) {
+    if (ee < -10) return (uint16_t)sign;
+    m |= 0x800000u;
+    const int shift = 14 - ee;
+    uint32_t hm = m >> shift;
+    const uint32_t rem = m & ((1u << shift) - 1u);
+    const uint32_t halfway = 1u << (shift - 1);
+    if (rem > halfway || (rem == halfway && (hm & 1u))) ++hm;
+    return (uint16_t)(sign | hm);
+  }
+  uint32_t hm = m >> 13;
+  const uint32_t rem = m & 0x1FFFu;
+  uint32_t out = sign | ((uint32_t)ee << 10) | hm;
+  if (rem > 0x1000u || (rem == 0x1000u && (hm & 1u))) ++out;
+  return (uint16_t)out;
+}
+
+// float16 image of a codebook: lut16 = f16(cb / 2^e), scale = 2^e.
+void make_lut16(const float* cb, Lut16* lut, float* scale) {
+  float mx = 0.0f;
+  for (int i = 0; i < 16; ++i) mx = std::fmax(mx, std::fabs(cb[i]));
+  int e = 0;
+  if (mx > 0.0f) {
+    int E;
+    std::frexp(mx, &E);          // mx = f * 2^E, f in [0.5, 1)
+    e = E - 15;                  // mx / 2^e in [2^14, 2^15)
+  }
+  uint16_t h[16];
+  for (int i = 0; i < 16; ++i) h[i] = f32_to_f16(std::ldexp(cb[i], -e));
+  for (int i = 0; i < 8; ++i) lut->h[i] = (uint32_t)h[2 * i] | ((uint32_t)h[2 * i + 1] << 16);
+  *scale = std::ldexp(1.0f, e);
+}
+
+struct DeviceInfo { int cus = 0; };
+
+int device_cus() {
+  static std::mutex mu;
+  static DeviceInfo info[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  std::lock_guard<std::mutex> lock(mu);
+  if (info[dev].cus == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    info[dev].cus = cus;
+  }
+  return info[dev].cus;
+}
+
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int32_t launch_status() {
+  return hipGetLastError() == hipSuccess ? LOGBQ_OK : LOGBQ_ERR_HIP;
+}
+
+int64_t grid_for(int64_t items, int64_t per_block, int64_t cap) {
+  int64_t g = (items + per_block - 1) / per_block;
+  if (g > cap) g = cap;
+  if (g < 1) g = 1;
+  return g;
+}
+
+template <int M, int CPL>
+void launch_gemv(dim3 grid, hipStream_t st, const uint8_t* codes, const uint16_t* x, float* y,
+                 int n, int k, int wk, int iters, const Lut16& lut, float scale) {
+  hipLaunchKernelGGL((k_gemv<M, CPL>), grid, dim3(512), 0, st, codes, x, y, n, k, wk, iters, lut,
+                     scale);
+}
+
+bool dispatch_gemv(int m, int cpl, dim3 grid, hipStream_t st, const uint8_t* codes,
+                   const uint16_t* x, float* y, int n, int k, int wk, int iters, const Lut16& lut,
+                   float scale) {
+#define LOGBQ_G(MM, CC) \
+  if (m == MM && cpl == CC) { launch_gemv<MM, CC>(grid, st, codes, x, y, n, k, wk, iters, lut, scale); return true; }
+  LOGBQ_G(1, 1) LOGBQ_G(1, 2) LOGBQ_G(1, 4) LOGBQ_G(1, 8)
+  LOGBQ_G(2, 1) LOGBQ_G(2, 2) LOGBQ_G(2, 4)
+  LOGBQ_G(3, 1) LOGBQ_G(3, 2)
+  LOGBQ_G(4, 1) LOGBQ_G(4, 2)
+  LOGBQ_G(5, 1) LOGBQ_G(6, 1) LOGBQ_G(7, 1) LOGBQ_G(8, 1)
+#undef LOGBQ_G
+  return false;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_params* p,
+                     uint8_t* codes_dev, float* codebook_out, void* stream) {
+  if (!p || n < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
+  if (p->bits != 4) return LOGBQ_ERR_UNSUPPORTED;
+  if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
+  const int64_t numel = n * k;
+  if (n != 0 && numel / n != k) return LOGBQ_ERR_UNSUPPORTED;
+  if (numel > 0) {
+    if (!w_dev || !codes_dev) return LOGBQ_ERR_INVALID_ARG;
+    if (!aligned16(w_dev) || !aligned16(codes_dev)) return LOGBQ_ERR_UNSUPPORTED;
+  }
+  Thresholds th;
+  for (int i = 0; i < 7; ++i) {
+    th.t[i] = p->thresholds[i];
+    if (std::isnan(th.t[i]) || !(th.t[i] > 0.0f)) return LOGBQ_ERR_INVALID_ARG;
+    if (i > 0 && th.t[i] < th.t[i - 1]) return LOGBQ_ERR_INVALID_ARG;
+  }
+  if (codebook_out) std::memcpy(codebook_out, p->codebook, sizeof(p->codebook));
+  if (numel == 0) return LOGBQ_OK;
+  const int cus = device_cus();
+  if (cus <= 0) return LOGBQ_ERR_HIP;
+  const int64_t nwords = numel / 8;
+  const int64_t grid = grid_for(nwords, 256, (int64_t)cus * 16);
+  hipLaunchKernelGGL(k_encode, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream,
+                     reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint32_t*>(codes_dev),
+                     nwords, th);
+  return launch_status();
+}
+
+int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const float* codebook,
+                         float* w_dev, void* stream) {
+  if (!codebook || n < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
+  if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
+  const int64_t numel = n * k;
+  if (n != 0 && numel / n != k) return LOGBQ_ERR_UNSUPPORTED;
+  if (numel == 0) return LOGBQ_OK;
+  if (!codes_dev || !w_dev) return LOGBQ_ERR_INVALID_ARG;
+  if (!aligned16(codes_dev) || !aligned16(w_dev)) return LOGBQ_ERR_UNSUPPORTED;
+  Codebook32 cb;
+  std::memcpy(cb.v, codebook, sizeof(cb.v));
+  const int cus = device_cus();
+  if (cus <= 0) return LOGBQ_ERR_HIP;
+  const int64_t nwords = numel / 8;
+  const int64_t grid = grid_for(nwords, 256, (int64_t)cus * 16);
+  hipLaunchKernelGGL(k_dequant, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream,
+                     reinterpret_cast<const uint32_t*>(codes_dev), reinterpret_cast<f32x4*>(w_dev),
+                     nwords, cb);
+  return launch_status();
+}
+
+int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
+                     int64_t n, const float* codebook, float* y_dev, void* stream) {
+  if (!codebook || m < 0 || k < 0 || n < 0) return LOGBQ_ERR_INVALID_ARG;
+  if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
+  if (m > INT32_MAX || n > INT32_MAX || k > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
+  for (int i = 0; i < 16; ++i)
+    if (!std::isfinite(codebook[i])) return LOGBQ_ERR_INVALID_ARG;
+  if (m == 0 || n == 0) return LOGBQ_OK;
+  if (!y_dev) return LOGBQ_ERR_INVALID_ARG;
+  if (!aligned16(y_dev)) return LOGBQ_ERR_UNSUPPORTED;
+  hipStream_t st = (hipStream_t)stream;
+  const int cus = device_cus();
+  if (k == 0) {
+    if (cus <= 0) return LOGBQ_ERR_HIP;
+    const int64_t count = m * n;
+    hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)grid_for(count, 256, (int64_t)cus * 16)),
+                       dim3(256), 0, st, y_dev, count);
+    return launch_status();
+  }
+  if (!x_dev || !codes_dev) return LOGBQ_ERR_INVALID_ARG;
+  if (!aligned16(x_dev) || !aligned16(codes_dev)) return LOGBQ_ERR_UNSUPPORTED;
+  if (cus <= 0) return LOGBQ_ERR_HIP;
+  Lut16 lut;
+  float scale;
+  make_lut16(codebook, &lut, &scale);
+  const int N = (int)n, K = (int)k, Mi = (int)m;
+
+  if (Mi <= 8) {
+    const int nchunks = K / 32;
+    const int cplmax = 8 / Mi;
+    int wk = 0, cpl = 0;
+    for (int w = 1; w <= 8; w *= 2) {
+      const int per = (nchunks + 64 * w - 1) / (64 * w);
+      if (per <= cplmax) {
+        wk = w;
+        cpl = 1;
+        while (cpl < per) cpl *= 2;
+        break;
+      }
+    }
+    if (wk > 0) {
+      const int groups = 8 / wk;
+      const int64_t grid = grid_for(N, groups, (int64_t)cus * 2);
+      const int total_groups = (int)grid * groups;
+      const int iters = (N + total_groups - 1) / total_groups;
+      if (!dispatch_gemv(Mi, cpl, dim3((unsigned)grid), st, codes_dev, x_dev, y_dev, N, K, wk,
+                         iters, lut, scale))
+        return LOGBQ_ERR_UNSUPPORTED;
+      return launch_status();
+    }
+  }
+  // MFMA skinny GEMM: up to 128 batch rows per workgroup column.
+  const int mt = Mi >= 97 ? 4 : (Mi >= 65 ? 3 : (Mi >= 33 ? 2 : 1));
+  const int mblock = mt * 32;
+  dim3 grid((unsigned)((N + 127) / 128), (unsigned)((Mi + mblock - 1) / mblock));
+  switch (mt) {
+    case 1: hipLaunchKernelGGL(k_mfma<1>, grid, dim3(256), 0, st, codes_dev, x_dev, y_dev, N, K, Mi, lut, scale); break;
+    case 2: hipLaunchKernelGGL(k_mfma<2>, grid, dim3(256), 0, st, codes_dev, x_dev, y_dev, N, K, Mi, lut, scale); break;
+    case 3: hipLaunchKernelGGL(k_mfma<3>, grid, dim3(256), 0, st, codes_dev, x_dev, y_dev, N, K, Mi, lut, scale); break;
+    default: hipLaunchKernelGGL(k_mfma<4>, grid, dim3(256), 0, st, codes_dev, x_dev, y_dev, N, K, Mi, lut, scale); break;
+  }
+  return launch_status();
+}
+
+}  // extern "C"

@@ -1,0 +1,161 @@
+"""Python binding of liblogbq (ctypes): argument marshalling only.
+
+Every step of the computation runs in the library: ``fit`` in its host code, ``encode``,
+``linear`` and ``dequantize`` in its gfx950 kernels. PyTorch provides device memory and the
+current stream; nothing here computes on the data. If the library is not built, every call
+raises ``LogbqUnavailable``: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_double, c_float, c_int32, c_int64, c_uint8, c_uint16, c_void_p
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblogbq.so")
+
+OK, ERR_INVALID_ARG, ERR_NONFINITE, ERR_DEGENERATE, ERR_UNSUPPORTED, ERR_HIP = range(6)
+
+
+class LogbqUnavailable(RuntimeError):
+    pass
+
+
+class LogbqError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_str(status)} (status {status})")
+
+
+class Params(ctypes.Structure):
+    """Mirror of ``logbq_params`` (include/logbq.h)."""
+    _fields_ = [
+        ("bits", c_int32), ("qmax", c_int32), ("eps", c_double), ("wmin", c_double),
+        ("wmax", c_double), ("base", c_double), ("shift", c_int32), ("reserved", c_int32),
+        ("wmin_index", c_int64), ("codebook", c_float * 16), ("thresholds", c_float * 8),
+    ]
+
+    def codebook_array(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self.codebook).copy()
+
+    def thresholds_array(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self.thresholds).copy()
+
+
+_lib = None
+
+SIGNATURES = {
+    "logbq_abi_version": (c_int32, []),
+    "logbq_status_str": (ctypes.c_char_p, [c_int32]),
+    "logbq_fit": (c_int32, [POINTER(c_float), c_int64, c_int32, c_double, POINTER(Params)]),
+    "logbq_encode": (c_int32, [c_void_p, c_int64, c_int64, POINTER(Params), c_void_p,
+                               POINTER(c_float), c_void_p]),
+    "logbq_linear": (c_int32, [c_void_p, c_int64, c_int64, c_void_p, c_int64, POINTER(c_float),
+                               c_void_p, c_void_p]),
+    "logbq_dequantize": (c_int32, [c_void_p, c_int64, c_int64, POINTER(c_float), c_void_p,
+                                   c_void_p]),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded liblogbq.so (raises LogbqUnavailable if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise LogbqUnavailable(
+                f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        h = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(h, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = h
+    return _lib
+
+
+def status_str(status: int) -> str:
+    return lib().logbq_status_str(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise LogbqError(status, where)
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return c_void_p(stream)
+    return c_void_p(stream.cuda_stream)
+
+
+def _cb_ptr(codebook):
+    if isinstance(codebook, Params):
+        return codebook.codebook, codebook
+    arr = np.ascontiguousarray(np.asarray(codebook, dtype=np.float32))
+    if arr.shape != (16,):
+        raise ValueError("codebook must hold 16 float32 values")
+    return arr.ctypes.data_as(POINTER(c_float)), arr
+
+
+def fit(w, bits: int = 4, eps: float = 4e-3) -> Params:
+    """logbq_fit on host float32 weights (numpy array or CPU torch tensor)."""
+    if hasattr(w, "detach"):
+        w = w.detach().cpu().numpy()
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    p = Params()
+    _check(lib().logbq_fit(w.ctypes.data_as(POINTER(c_float)), w.size, bits, eps,
+                           ctypes.byref(p)), "logbq_fit")
+    return p
+
+
+def encode(w, p: Params, out=None, stream=None):
+    """logbq_encode: float32 [N][K] device tensor -> (uint8 [N][K/2] codes, float32[16])."""
+    import torch
+    if w.dtype != torch.float32 or w.dim() != 2 or not w.is_contiguous():
+        raise ValueError("w must be a contiguous 2-D float32 device tensor")
+    n, k = w.shape
+    if out is None:
+        out = torch.empty((n, k // 2), dtype=torch.uint8, device=w.device)
+    cb = np.zeros(16, dtype=np.float32)
+    _check(lib().logbq_encode(c_void_p(w.data_ptr()), n, k, ctypes.byref(p),
+                              c_void_p(out.data_ptr()), cb.ctypes.data_as(POINTER(c_float)),
+                              _stream(stream)), "logbq_encode")
+    return out, cb
+
+
+def linear(x, codes, codebook, out=None, stream=None):
+    """logbq_linear: y[M][N] = x[M][K] . W_hat^T (x float16, y float32) on packed codes."""
+    import torch
+    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous 2-D float16 device tensor")
+    if codes.dtype != torch.uint8 or codes.dim() != 2 or not codes.is_contiguous():
+        raise ValueError("codes must be a contiguous 2-D uint8 device tensor")
+    m, k = x.shape
+    n = codes.shape[0]
+    if codes.shape[1] * 2 != k:
+        raise ValueError("codes must be [N][K/2]")
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=x.device)
+    cbp, _keep = _cb_ptr(codebook)
+    _check(lib().logbq_linear(c_void_p(x.data_ptr()), m, k, c_void_p(codes.data_ptr()), n, cbp,
+                              c_void_p(out.data_ptr()), _stream(stream)), "logbq_linear")
+    return out
+
+
+def dequantize(codes, codebook, out=None, stream=None):
+    """logbq_dequantize: uint8 [N][K/2] -> float32 [N][K], bit-exact codebook lookup."""
+    import torch
+    if codes.dtype != torch.uint8 or codes.dim() != 2 or not codes.is_contiguous():
+        raise ValueError("codes must be a contiguous 2-D uint8 device tensor")
+    n, h = codes.shape
+    k = 2 * h
+    if out is None:
+        out = torch.empty((n, k), dtype=torch.float32, device=codes.device)
+    cbp, _keep = _cb_ptr(codebook)
+    _check(lib().logbq_dequantize(c_void_p(codes.data_ptr()), n, k, cbp, c_void_p(out.data_ptr()),
+                                  _stream(stream)), "logbq_dequantize")
+    return out

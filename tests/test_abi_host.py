@@ -1,0 +1,183 @@
+"""Host-side tests of liblogbq (no GPU): the library loads, exports every symbol the header
+declares, validates arguments before any HIP call, and its host fit equals the oracle's
+bit for bit (Sec. 3.1 Eq. 3-4, Sec. 3.2 Eq. 5)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import logbq_oracle as O
+from paper_2607_01127_amd import inputs
+from paper_2607_01127_amd import logbq as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "logbq.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(logbq_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = header_functions()
+    assert {"logbq_fit", "logbq_encode", "logbq_linear", "logbq_dequantize",
+            "logbq_status_str", "logbq_abi_version"} <= set(names)
+    h = L.lib()
+    for n in names:
+        assert hasattr(h, n), n
+    assert h.logbq_abi_version() == 1
+    for s in range(6):
+        assert L.status_str(s)
+    assert L.status_str(99) == "unknown status"
+
+
+def _cb():
+    return (ctypes.c_float * 16)(*([0.0] + [2.0 ** (k - 7) for k in range(1, 8)] + [0.0] +
+                                   [-(2.0 ** (k - 7)) for k in range(1, 8)]))
+
+
+P = ctypes.c_void_p
+
+
+def test_linear_validation_before_hip():
+    h = L.lib()
+    cb = _cb()
+    a = P(4096)  # 16-byte aligned dummy address; never dereferenced on these paths
+    assert h.logbq_linear(a, 1, 64, a, 4, None, a, None) == L.ERR_INVALID_ARG       # no codebook
+    assert h.logbq_linear(a, -1, 64, a, 4, cb, a, None) == L.ERR_INVALID_ARG
+    assert h.logbq_linear(a, 1, -32, a, 4, cb, a, None) == L.ERR_INVALID_ARG
+    assert h.logbq_linear(a, 1, 64, a, -4, cb, a, None) == L.ERR_INVALID_ARG
+    assert h.logbq_linear(a, 1, 48, a, 4, cb, a, None) == L.ERR_UNSUPPORTED         # K % 32
+    assert h.logbq_linear(a, 1, 64, a, 4, cb, None, None) == L.ERR_INVALID_ARG      # no y
+    assert h.logbq_linear(None, 1, 64, a, 4, cb, a, None) == L.ERR_INVALID_ARG      # no x
+    assert h.logbq_linear(a, 1, 64, None, 4, cb, a, None) == L.ERR_INVALID_ARG      # no codes
+    assert h.logbq_linear(P(4100), 1, 64, a, 4, cb, a, None) == L.ERR_UNSUPPORTED   # misaligned
+    assert h.logbq_linear(a, 1, 64, a, 4, cb, P(4104), None) == L.ERR_UNSUPPORTED
+    bad = _cb()
+    bad[3] = float("nan")
+    assert h.logbq_linear(a, 1, 64, a, 4, bad, a, None) == L.ERR_INVALID_ARG
+    assert h.logbq_linear(a, 1, 2 ** 33, a, 4, cb, a, None) == L.ERR_UNSUPPORTED
+    # empty calls succeed without touching the device
+    assert h.logbq_linear(None, 0, 64, None, 4, cb, None, None) == L.OK
+    assert h.logbq_linear(None, 3, 64, None, 0, cb, None, None) == L.OK
+
+
+def test_encode_and_dequant_validation_before_hip():
+    h = L.lib()
+    p = L.fit(np.array([0.1, -0.5, 0.25, 1.0] * 8, dtype=np.float32))
+    a = P(4096)
+    assert h.logbq_encode(a, 4, 64, None, a, None, None) == L.ERR_INVALID_ARG
+    assert h.logbq_encode(a, -1, 64, ctypes.byref(p), a, None, None) == L.ERR_INVALID_ARG
+    assert h.logbq_encode(a, 4, 40, ctypes.byref(p), a, None, None) == L.ERR_UNSUPPORTED
+    assert h.logbq_encode(None, 4, 64, ctypes.byref(p), a, None, None) == L.ERR_INVALID_ARG
+    assert h.logbq_encode(P(4097), 4, 64, ctypes.byref(p), a, None, None) == L.ERR_UNSUPPORTED
+    q = L.Params.from_buffer_copy(p)
+    q.bits = 8
+    assert h.logbq_encode(a, 4, 64, ctypes.byref(q), a, None, None) == L.ERR_UNSUPPORTED
+    q = L.Params.from_buffer_copy(p)
+    q.thresholds[2] = q.thresholds[1] / 2                      # not sorted
+    assert h.logbq_encode(a, 4, 64, ctypes.byref(q), a, None, None) == L.ERR_INVALID_ARG
+    cb = (ctypes.c_float * 16)()
+    out = (ctypes.c_float * 16)()
+    assert h.logbq_encode(None, 0, 64, ctypes.byref(p), None, out, None) == L.OK
+    assert list(out) == list(p.codebook)
+    assert h.logbq_dequantize(a, 4, 64, None, a, None) == L.ERR_INVALID_ARG
+    assert h.logbq_dequantize(a, 4, 33, cb, a, None) == L.ERR_UNSUPPORTED
+    assert h.logbq_dequantize(None, 4, 64, cb, a, None) == L.ERR_INVALID_ARG
+    assert h.logbq_dequantize(a, 4, 64, cb, P(4098), None) == L.ERR_UNSUPPORTED
+    assert h.logbq_dequantize(None, 0, 64, cb, None, None) == L.OK
+
+
+def test_fit_errors_match_oracle():
+    cases = [
+        (np.array([1.0, np.nan], dtype=np.float32), L.ERR_NONFINITE, "nonfinite"),
+        (np.array([1.0, -np.inf], dtype=np.float32), L.ERR_NONFINITE, "nonfinite"),
+        (np.zeros(16, dtype=np.float32), L.ERR_DEGENERATE, "degenerate"),
+        (np.array([0.5, -0.5, 0.5, 0.0], dtype=np.float32), L.ERR_DEGENERATE, "degenerate"),
+        (np.array([0.5], dtype=np.float32), L.ERR_INVALID_ARG, "invalid_arg"),
+    ]
+    for w, status, kind in cases:
+        with pytest.raises(L.LogbqError) as e:
+            L.fit(w)
+        assert e.value.status == status
+        with pytest.raises(O.OracleError, match=kind):
+            O.fit(w)
+    for eps in (0.0, 1.0, -1e-3, float("nan")):
+        with pytest.raises(L.LogbqError) as e:
+            L.fit(np.array([0.5, 1.0], dtype=np.float32), eps=eps)
+        assert e.value.status == L.ERR_INVALID_ARG
+    with pytest.raises(L.LogbqError) as e:
+        L.fit(np.array([0.5, 1.0], dtype=np.float32), bits=8)
+    assert e.value.status == L.ERR_UNSUPPORTED
+    h = L.lib()
+    assert h.logbq_fit(None, 4, 4, 4e-3, ctypes.byref(L.Params())) == L.ERR_INVALID_ARG
+
+
+def _assert_fit_equal(w, eps=4e-3):
+    p = L.fit(w, 4, eps)
+    r = O.fit(w, 4, eps)
+    assert p.bits == 4 and p.qmax == 7 and p.eps == eps
+    assert p.wmin == r.wmin and p.wmax == r.wmax
+    assert p.wmin_index == r.wmin_index
+    assert p.base == r.base, (p.base, r.base)
+    assert p.shift == r.shift
+    assert p.codebook_array().view(np.uint32).tolist() == \
+        O.codebook(r.base, r.shift).view(np.uint32).tolist()
+    assert p.thresholds_array()[:7].view(np.uint32).tolist() == \
+        O.magnitude_thresholds(r.base, r.shift).view(np.uint32).tolist()
+    assert np.isinf(p.thresholds[7])
+    return p
+
+
+def test_fit_bit_exact_random():
+    rng = np.random.default_rng(123)
+    for i in range(40):
+        n = int(rng.integers(2, 5000))
+        nu = [2.5, 3, 4, 8][i % 4]
+        w = (rng.standard_t(nu, size=n) * 10 ** rng.uniform(-6, 2)).astype(np.float32)
+        if i % 5 == 0:
+            w[rng.integers(0, n, size=n // 3)] = 0.0
+        if i % 7 == 0:
+            w = np.round(w * 100) / 100                        # many duplicates
+            w = w.astype(np.float32)
+            if np.count_nonzero(w) < 2 or np.unique(np.abs(w[w != 0])).size < 2:
+                continue
+        eps = [4e-3, 1e-6, 0.1][i % 3]
+        try:
+            r = O.fit(w, 4, eps)
+        except O.OracleError:
+            continue
+        del r
+        _assert_fit_equal(w, eps)
+
+
+def test_fit_golden_example():
+    w = np.array([2.0 ** -7] * 66 + [1.0], dtype=np.float32)
+    p = _assert_fit_equal(w)
+    assert p.base == 2.0 and p.shift == 7 and p.wmin_index == 65
+
+
+def test_fit_extreme_scales():
+    rng = np.random.default_rng(9)
+    base = rng.standard_t(3, size=3000).astype(np.float32)
+    for s in (1e-30, 1e-12, 1e12, 1e30):
+        _assert_fit_equal((base * np.float32(s)).astype(np.float32))
+    sub = (rng.standard_t(3, size=3000) * 1e-41).astype(np.float32)   # subnormal weights
+    sub = sub[np.abs(sub) > 0]
+    try:
+        O.fit(sub)
+    except O.OracleError:
+        return
+    _assert_fit_equal(sub)
+
+
+@pytest.mark.parametrize("name", ["linear_2048x2048", "up_2048x8192_outliers"])
+def test_fit_bit_exact_workload_tensors(name):
+    wl = inputs.WORKLOADS[name]
+    lin = wl["layers"][0]
+    w = inputs.student_t_weights(lin.n, lin.k, wl["nu"], wl["scale"],
+                                 seed=[wl["cfg"], 0, 0, 0], outlier_frac=wl["outlier_frac"])
+    _assert_fit_equal(w)

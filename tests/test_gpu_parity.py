@@ -1,0 +1,299 @@
+"""GPU parity of liblogbq against the CPU oracle, through the C ABI.
+
+Bars: codes and dequantized weights bit-exact; y = x . W_hat^T within
+max |y - y_ref| / (||x_m|| * ||W_hat_n||) <= 1e-3 (float32 accumulation). The same seeded
+inputs go to both sides; every expected value comes from the oracle (or, for the exhaustive
+float32 sweep, from the oracle's thresholds).
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import logbq_oracle as O
+from paper_2607_01127_amd import inputs
+from paper_2607_01127_amd import logbq as L
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-3
+DEV = "cuda:0"
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def rel_err(y, x, w_hat):
+    """max over (m, n) of |y - y_ref| / (||x_m|| ||W_hat_n||), with y_ref from the oracle."""
+    y_ref = O.linear(x, w_hat)
+    xn = np.linalg.norm(x.astype(np.float64), axis=1)[:, None]
+    wn = np.linalg.norm(w_hat.astype(np.float64), axis=1)[None, :]
+    den = xn * wn
+    den[den == 0] = 1.0
+    return float(np.max(np.abs(y.astype(np.float64) - y_ref) / den)) if y.size else 0.0
+
+
+def prepare(n, k, seed, nu=4, scale=0.02, outliers=0.0):
+    w = inputs.student_t_weights(n, k, nu, scale, seed=seed, outlier_frac=outliers)
+    p = L.fit(w)
+    r = O.fit(w)
+    assert (p.base, p.shift) == (r.base, r.shift)
+    return w, p, r
+
+
+def gpu_encode(w, p):
+    wd = torch.from_numpy(w).to(DEV)
+    codes, cb = L.encode(wd, p)
+    torch.cuda.synchronize()
+    return codes, cb
+
+
+def oracle_codes(w, r):
+    return O.pack(O.encode(w, r.base, r.shift))
+
+
+# ---------------------------------------------------------------- encode / dequantize
+
+@pytest.mark.parametrize("n,k,seed,nu,scale,outl", [
+    (2048, 2048, [0, 0, 0, 0], 4, 0.02, 0.0),          # 2048 x 2048 linear
+    (8192, 2048, [1, 0, 5, 0], 4, 0.02, 1e-4),          # up-projection with outliers
+    (37, 32, [9, 1, 1, 0], 3, 0.015, 0.0),              # ragged tiny
+    (513, 352, [9, 2, 2, 0], 3, 1.0, 0.0),
+    (3, 14336, [9, 3, 3, 0], 6, 1e-4, 0.0),
+])
+def test_encode_bit_exact(n, k, seed, nu, scale, outl):
+    _say(f"encode n={n} k={k} seed={seed}")
+    w, p, r = prepare(n, k, seed, nu, scale, outl)
+    codes, cb = gpu_encode(w, p)
+    exp = oracle_codes(w, r)
+    got = codes.cpu().numpy()
+    assert got.shape == exp.shape
+    assert np.array_equal(got, exp), f"{np.count_nonzero(got != exp)} bytes differ"
+    assert cb.view(np.uint32).tolist() == O.codebook(r.base, r.shift).view(np.uint32).tolist()
+
+
+def test_encode_special_values():
+    _say("encode special values")
+    w, p, r = prepare(64, 64, [9, 4, 4, 0])
+    thr = O.magnitude_thresholds(r.base, r.shift)
+    specials = [np.nan, -np.nan, np.inf, -np.inf, 0.0, -0.0, 1e-45, -1e-45, 3.4e38, -3.4e38,
+                float(r.wmin), -float(r.wmin), float(r.wmax), -float(r.wmax)]
+    for t in thr:
+        for d in (-2, -1, 0, 1, 2):
+            v = np.array([t], dtype=np.float32).view(np.int32)[0] + d
+            f = np.array([v], dtype=np.int32).view(np.float32)[0]
+            specials += [float(f), -float(f)]
+    flat = w.reshape(-1).copy()
+    flat[: len(specials)] = np.array(specials, dtype=np.float32)
+    w2 = flat.reshape(w.shape)
+    codes, _ = gpu_encode(w2, p)
+    assert np.array_equal(codes.cpu().numpy(), oracle_codes(w2, r))
+
+
+@pytest.mark.parametrize("n,k", [(64, 32), (1000, 2048), (3, 96)])
+def test_dequant_bit_exact(n, k):
+    _say(f"dequant n={n} k={k}")
+    w, p, r = prepare(n, k, [9, 5, n, 0])
+    rng = np.random.default_rng(n)
+    c = rng.integers(0, 16, size=(n, k), dtype=np.uint8)      # every code, including 8
+    packed = torch.from_numpy(O.pack(c)).to(DEV)
+    out = L.dequantize(packed, p)
+    torch.cuda.synchronize()
+    exp = O.dequantize(c, O.codebook(r.base, r.shift))
+    assert out.cpu().numpy().view(np.uint32).tolist() == exp.view(np.uint32).tolist()
+
+
+def test_encode_dequant_roundtrip_idempotent():
+    """encode(dequantize(codes)) == codes with code 8 mapped to 0."""
+    _say("encode(dequantize(codes))")
+    w, p, r = prepare(128, 256, [9, 6, 0, 0])
+    rng = np.random.default_rng(5)
+    c = rng.integers(0, 16, size=(128, 256), dtype=np.uint8)
+    packed = torch.from_numpy(O.pack(c)).to(DEV)
+    wh = L.dequantize(packed, p)
+    back, _ = L.encode(wh, p)
+    torch.cuda.synchronize()
+    exp = c.copy()
+    exp[exp == 8] = 0
+    assert np.array_equal(back.cpu().numpy(), O.pack(exp))
+
+
+@pytest.mark.parametrize("params", ["b2", "c1", "heavy"])
+def test_encode_every_float32(params):
+    """Every float32 bit pattern with the sign clear (2^31 values) and a slice of negatives,
+    against the oracle's exact thresholds."""
+    if params == "b2":
+        base, shift = 2.0, 7
+    else:
+        nu, scale = (4, 0.02) if params == "c1" else (3, 0.015)
+        w = inputs.student_t_weights(1024, 1024, nu, scale, seed=[9, 7, len(params), 0])
+        r = O.fit(w)
+        base, shift = r.base, r.shift
+    thr = O.magnitude_thresholds(base, shift)
+    p = L.Params()
+    p.bits, p.qmax, p.base, p.shift = 4, 7, base, shift
+    for i in range(7):
+        p.thresholds[i] = float(thr[i])
+    p.thresholds[7] = float("inf")
+    thr_t = torch.from_numpy(thr.astype(np.float32)).to(DEV)
+    chunk = 1 << 28
+    rows = chunk // 32768
+    mism = 0
+    shifts = torch.arange(0, 32, 4, device=DEV, dtype=torch.int32)
+    for c0 in list(range(0, 1 << 31, chunk)) + ["neg"]:
+        _say(f"sweep {params} chunk {c0}")
+        if c0 == "neg":
+            bits = torch.arange(0, chunk, device=DEV, dtype=torch.int64) * 7 + 0x80000000
+            bits = (bits & 0xFFFFFFFF).to(torch.int64)
+            bits = torch.where(bits >= 2 ** 31, bits - 2 ** 32, bits).to(torch.int32)
+        else:
+            bits = torch.arange(c0, c0 + chunk, device=DEV, dtype=torch.int64).to(torch.int32)
+        x = bits.view(torch.float32).reshape(rows, 32768)
+        codes, _ = L.encode(x, p)
+        cw = codes.view(torch.int32).reshape(-1)
+        nib = ((cw[:, None] >> shifts[None, :]) & 15).reshape(-1)
+        ax = x.reshape(-1).abs()
+        mag = torch.bucketize(ax, thr_t, right=True).to(torch.int32)
+        mag = torch.where(torch.isnan(ax), torch.zeros_like(mag), mag)
+        neg = (x.reshape(-1) < 0) & (mag > 0)
+        exp = mag + 8 * neg.to(torch.int32)
+        mism += int((nib != exp).sum().item())
+        del x, codes, cw, nib, ax, mag, neg, exp, bits
+    assert mism == 0
+
+
+# ---------------------------------------------------------------- linear
+
+SHAPES = [(2048, 2048), (1000, 352), (37, 32), (512, 14336), (4096, 4096), (64, 8192), (8, 28672)]
+BATCH = [1, 2, 3, 4, 5, 8, 9, 16, 17, 32, 33, 64, 100, 128, 129, 200]
+
+
+@pytest.mark.parametrize("n,k", SHAPES)
+def test_linear_matches_oracle(n, k):
+    w, p, r = prepare(n, k, [8, n, k % 1000, 0])
+    codes, cb = gpu_encode(w, p)
+    c = O.encode(w, r.base, r.shift)
+    wh = O.dequantize(c, O.codebook(r.base, r.shift))
+    for m in BATCH:
+        if m > 32 and n * k > 4096 * 4096:
+            continue
+        _say(f"linear n={n} k={k} m={m}")
+        x = inputs.activations(m, k, seed=[8, n, k % 1000, 1 + m])
+        y = L.linear(torch.from_numpy(x).to(DEV), codes, cb)
+        torch.cuda.synchronize()
+        err = rel_err(y.cpu().numpy(), x, wh)
+        assert err <= TOL, (m, err)
+        assert err <= 2.5e-4, (m, err)   # float16 table + float32 accumulation headroom
+
+
+def test_linear_unit_vectors_and_zero():
+    """x = e_k gives column k of W_hat (up to the float16 table rounding); x = 0 gives +0."""
+    n, k = 300, 256
+    w, p, r = prepare(n, k, [8, 1, 2, 3])
+    codes, cb = gpu_encode(w, p)
+    wh = O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
+    for m in (1, 8, 16, 64):
+        _say(f"unit vectors m={m}")
+        cols = np.arange(m) * 7 % k
+        x = np.zeros((m, k), dtype=np.float16)
+        x[np.arange(m), cols] = 1.0
+        y = L.linear(torch.from_numpy(x).to(DEV), codes, cb).cpu().numpy()
+        exp = wh[:, cols].T.astype(np.float64)
+        assert np.all(np.abs(y - exp) <= np.abs(exp) * 2.0 ** -11)
+        assert np.all(np.sign(y) == np.sign(exp))
+        y0 = L.linear(torch.zeros((m, k), dtype=torch.float16, device=DEV), codes, cb)
+        assert torch.all(y0 == 0).item()
+
+
+def test_linear_sign_flip_negates_exactly():
+    """Flipping the sign bit of every code negates y bit for bit (same summation order)."""
+    n, k = 777, 1024
+    w, p, r = prepare(n, k, [8, 2, 2, 2])
+    codes, cb = gpu_encode(w, p)
+    flipped = codes ^ 0x88
+    for m in (1, 4, 8, 32, 128):
+        _say(f"sign flip m={m}")
+        x = torch.from_numpy(inputs.activations(m, k, seed=[8, 2, 2, m])).to(DEV)
+        y = L.linear(x, codes, cb)
+        yf = L.linear(x, flipped, cb)
+        torch.cuda.synchronize()
+        assert torch.equal(yf, -y)
+
+
+def test_linear_constant_codes():
+    """All codes equal c: y_n = codebook[c] * sum(x) (float32 tolerance)."""
+    n, k = 64, 512
+    w, p, r = prepare(n, k, [8, 3, 3, 3])
+    lut = O.codebook(r.base, r.shift)
+    for c in (1, 7, 12):
+        byte = c | (c << 4)
+        codes = torch.full((n, k // 2), byte, dtype=torch.uint8, device=DEV)
+        for m in (1, 16):
+            _say(f"constant code {c} m={m}")
+            x = inputs.activations(m, k, seed=[8, 3, c, m])
+            y = L.linear(torch.from_numpy(x).to(DEV), codes, p).cpu().numpy()
+            exp = float(lut[c]) * x.astype(np.float64).sum(axis=1)
+            bound = abs(float(lut[c])) * np.abs(x.astype(np.float64)).sum(axis=1) * 1e-3
+            assert np.all(np.abs(y - exp[:, None]) <= bound[:, None])
+
+
+def test_linear_deterministic_and_empty():
+    n, k = 4096, 4096
+    w, p, r = prepare(n, k, [8, 4, 4, 4])
+    codes, cb = gpu_encode(w, p)
+    for m in (1, 3, 8, 32, 128):
+        _say(f"determinism m={m}")
+        x = torch.from_numpy(inputs.activations(m, k, seed=[8, 4, 4, m])).to(DEV)
+        y1 = L.linear(x, codes, cb)
+        y2 = L.linear(x, codes, cb)
+        torch.cuda.synchronize()
+        assert torch.equal(y1, y2)
+    _say("k = 0 and empty shapes")
+    y = torch.full((3, 5), 7.0, device=DEV)
+    L.linear(torch.empty((3, 0), dtype=torch.float16, device=DEV),
+             torch.empty((5, 0), dtype=torch.uint8, device=DEV), cb, out=y)
+    torch.cuda.synchronize()
+    assert torch.all(y == 0).item()
+    y = L.linear(torch.empty((0, 64), dtype=torch.float16, device=DEV),
+                 torch.zeros((5, 32), dtype=torch.uint8, device=DEV), cb)
+    assert y.shape == (0, 5)
+
+
+# ---------------------------------------------------------------- full-size, sampled
+
+def test_full_size_layer_8192x28672_sampled():
+    """The 8192 x 28672 layer (t3 * 0.015 weights) at every batch size of the sweep, in the
+    launch configuration the benchmark uses; codes and y compared on sampled rows."""
+    wl = inputs.WORKLOADS["layer_8192x28672"]
+    lin = wl["layers"][0]
+    n, k = lin.n, lin.k
+    _say("full-size layer: generate + fit")
+    wd = inputs.student_t_weights(n, k, wl["nu"], wl["scale"], seed=[wl["cfg"], 0, 0, 0],
+                                  device=DEV)
+    w = wd.cpu().numpy()
+    _say("full-size layer: oracle fit")
+    r = O.fit(w)
+    p = L.fit(w)
+    assert (p.base, p.shift, p.wmin, p.wmax, p.wmin_index) == \
+        (r.base, r.shift, r.wmin, r.wmax, r.wmin_index)
+    rows = np.sort(np.random.default_rng(0).choice(n, size=48, replace=False))
+    rows = np.concatenate([rows, [0, n - 1]])
+    wsub = w[rows]
+    del w
+    _say("full-size layer: encode")
+    codes, cb = L.encode(wd, p)
+    torch.cuda.synchronize()
+    del wd
+    got = codes[torch.from_numpy(rows).to(DEV)].cpu().numpy()
+    c_sub = O.encode(wsub, r.base, r.shift)
+    assert np.array_equal(got, O.pack(c_sub))
+    wh = O.dequantize(c_sub, O.codebook(r.base, r.shift))
+    for m in wl["batch"]:
+        _say(f"full-size layer: linear m={m}")
+        x = inputs.activations(m, k, seed=[wl["cfg"], 0, 0, 1])
+        y = L.linear(torch.from_numpy(x).to(DEV), codes, cb)
+        torch.cuda.synchronize()
+        ys = y[:, torch.from_numpy(rows).to(DEV)].cpu().numpy()
+        assert rel_err(ys, x, wh) <= TOL
