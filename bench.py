@@ -147,6 +147,7 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup):
                     for c in code_list]
         timed = steps if m == ms[0] else max(64, steps // 4)
         t = time_launches(torch, L, stream, launches, timed, warmup)
+        log(f"layer m={m}: {t * 1e3:.2f} us per launch")
         algo = packed + 2 * m * k + 4 * m * n + 64
         flops = 2.0 * m * n * k
         results[f"linear_8192x28672_m{m}"] = {
@@ -196,6 +197,8 @@ def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):
                 tensors.append((lin, codes, cb))
             torch.cuda.synchronize()
             del hosts, devs
+            if li % 8 == 7:
+                log(f"{name}: {li + 1} layers ready ({time.perf_counter() - t0:.1f} s)")
     setup_s = time.perf_counter() - t0
     bytes_pass = sum(lin.n * lin.k // 2 for lin, _, _ in tensors)
     out = {}
@@ -226,6 +229,7 @@ def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):
         torch.cuda.synchronize()
         assert all(torch.equal(a, b) for a, b in zip(ref, ys)), "graph replay differs"
         t = time_region(torch, stream, lambda i: g.replay(), steps, warmup)
+        log(f"{name} m={m}: {t * 1e3:.1f} us per pass")
         out[f"m{m}"] = {"ms_per_token_pass": t, "tokens_per_s": m / (t * 1e-3),
                         "weight_GB_s": bytes_pass / t / 1e6,
                         "hbm_frac": bytes_pass / t / 1e6 / HBM_PEAK_GBS,
