@@ -41,10 +41,13 @@ def log(msg):
 
 
 class Calls:
-    """Pre-marshalled logbq_linear argument tuples, so the timed loop only calls the library."""
+    """Pre-marshalled logbq_linear / logbq_linear_multi arguments, so that the timed loop (or the
+    graph capture) only calls the library."""
 
     def __init__(self, L, stream):
+        self.L = L
         self.fn = L.lib().logbq_linear
+        self.fn_multi = L.lib().logbq_linear_multi
         self.stream = ctypes.c_void_p(stream)
         self.args = []
         self.keep = []
@@ -52,15 +55,28 @@ class Calls:
     def add(self, x, codes, cb, y):
         cbarr = np.ascontiguousarray(cb, dtype=np.float32)
         self.keep.append(cbarr)
-        self.args.append((ctypes.c_void_p(x.data_ptr()), x.shape[0], x.shape[1],
-                          ctypes.c_void_p(codes.data_ptr()), codes.shape[0],
-                          cbarr.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
-                          ctypes.c_void_p(y.data_ptr()), self.stream))
+        self.args.append((self.fn, (ctypes.c_void_p(x.data_ptr()), x.shape[0], x.shape[1],
+                                    ctypes.c_void_p(codes.data_ptr()), codes.shape[0],
+                                    cbarr.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                    ctypes.c_void_p(y.data_ptr()), self.stream)))
+
+    def add_multi(self, x, codes_list, cbs, ys):
+        cnt = len(codes_list)
+        arrs = [np.ascontiguousarray(cb, dtype=np.float32) for cb in cbs]
+        cptr = (ctypes.c_void_p * cnt)(*[c.data_ptr() for c in codes_list])
+        ns = (ctypes.c_int64 * cnt)(*[c.shape[0] for c in codes_list])
+        cbp = (ctypes.POINTER(ctypes.c_float) * cnt)(
+            *[a.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) for a in arrs])
+        yp = (ctypes.c_void_p * cnt)(*[y.data_ptr() for y in ys])
+        self.keep.append((arrs, cptr, ns, cbp, yp))
+        self.args.append((self.fn_multi, (ctypes.c_void_p(x.data_ptr()), x.shape[0], x.shape[1],
+                                          cnt, cptr, ns, cbp, yp, self.stream)))
 
     def run(self, idx):
-        st = self.fn(*self.args[idx])
+        fn, a = self.args[idx]
+        st = fn(*a)
         if st != 0:
-            raise RuntimeError(f"logbq_linear failed with status {st}")
+            raise RuntimeError(f"logbq launch failed with status {st}")
 
 
 def time_region(torch, stream, fn, steps, warmup):
@@ -111,7 +127,7 @@ def make_tensor(torch, L, inputs, lin, wl, seed, dev):
     return codes, cb
 
 
-def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup):
+def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=True):
     """The 8192 x 28672 layer: rotation copies, M sweep, encode timing."""
     wl = inputs.WORKLOADS["layer_8192x28672"]
     lin = wl["layers"][0]
@@ -131,15 +147,17 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup):
     code_list = [codes] + [codes.clone() for _ in range(copies - 1)]
     results = {}
     # encode: 1 float32 tensor of 0.94 GB is read per call (larger than the last-level cache)
-    enc_out = torch.empty_like(codes)
-    def enc(i):
-        L.encode(wd, p, out=enc_out, stream=stream)
-    enc_ms = time_region(torch, stream, enc, max(5, steps // 20), 2)
-    assert torch.equal(enc_out, codes)
-    enc_bytes = n * k * 4 + packed
-    results["encode_8192x28672"] = {"ms": enc_ms, "GB_s": enc_bytes / enc_ms / 1e6,
-                                    "hbm_frac": enc_bytes / enc_ms / 1e6 / HBM_PEAK_GBS,
-                                    "bytes": enc_bytes}
+    if with_encode:
+        enc_out = torch.empty_like(codes)
+
+        def enc(i):
+            L.encode(wd, p, out=enc_out, stream=stream)
+        enc_ms = time_region(torch, stream, enc, max(5, steps // 20), 2)
+        assert torch.equal(enc_out, codes)
+        enc_bytes = n * k * 4 + packed
+        results["encode_8192x28672"] = {"ms": enc_ms, "GB_s": enc_bytes / enc_ms / 1e6,
+                                        "hbm_frac": enc_bytes / enc_ms / 1e6 / HBM_PEAK_GBS,
+                                        "bytes": enc_bytes}
     del wd
     for m in ms:
         x = inputs.activations(m, k, seed=[wl["cfg"], 0, 0, 1], device=dev)
@@ -202,38 +220,56 @@ def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):
     setup_s = time.perf_counter() - t0
     bytes_pass = sum(lin.n * lin.k // 2 for lin, _, _ in tensors)
     out = {}
+    # Launch plan per layer, in dependency order: linears that read the same activations
+    # (q, k, v) and (gate, up) go in one grouped launch.
+    per_layer = len(wl["layers"])
+    plan = []
+    for li in range(layers):
+        t = tensors[li * per_layer:(li + 1) * per_layer]
+        names = [lin.name for lin, _, _ in t]
+        groups = [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
+        for g in groups:
+            plan.append([t[names.index(nm)] for nm in g])
     for m in batches:
         xs = {}
-        ys = []
+        ys = {}
+        leader = {"q": "q", "k": "q", "v": "q", "o": "o", "gate": "gate", "up": "gate",
+                  "down": "down"}
+        for lin, codes, cb in tensors:
+            key = (lin.k, leader[lin.name])
+            if key not in xs:
+                xs[key] = inputs.activations(m, lin.k, seed=[wl["cfg"], 0, inputs.PROJ[key[1]], 1],
+                                             device=dev)
+            ys[id(codes)] = torch.empty((m, lin.n), dtype=torch.float32, device=dev)
         g = torch.cuda.CUDAGraph()
         cap = torch.cuda.Stream()
-        for lin, codes, cb in tensors:
-            key = (lin.k, lin.name)
-            if key not in xs:
-                xs[key] = inputs.activations(m, lin.k, seed=[wl["cfg"], 0, inputs.PROJ[lin.name], 1],
-                                             device=dev)
-            ys.append(torch.empty((m, lin.n), dtype=torch.float32, device=dev))
         torch.cuda.synchronize()
         with torch.cuda.graph(g, stream=cap):
             calls = Calls(L, torch.cuda.current_stream().cuda_stream)
-            for (lin, codes, cb), y in zip(tensors, ys):
-                calls.add(xs[(lin.k, lin.name)], codes, cb, y)
-            for i in range(len(tensors)):
+            for grp in plan:
+                x = xs[(grp[0][0].k, leader[grp[0][0].name])]
+                if len(grp) == 1:
+                    lin, codes, cb = grp[0]
+                    calls.add(x, codes, cb, ys[id(codes)])
+                else:
+                    calls.add_multi(x, [c for _, c, _ in grp], [cb for _, _, cb in grp],
+                                    [ys[id(c)] for _, c, _ in grp])
+            for i in range(len(plan)):
                 calls.run(i)
-        # check the replay against eager launches
+        # check the replay against eager per-linear launches
         g.replay()
         torch.cuda.synchronize()
-        ref = [y.clone() for y in ys]
-        for (lin, codes, cb), y in zip(tensors, ys):
-            L.linear(xs[(lin.k, lin.name)], codes, cb, out=y)
+        ref = {key: y.clone() for key, y in ys.items()}
+        for lin, codes, cb in tensors:
+            L.linear(xs[(lin.k, leader[lin.name])], codes, cb, out=ys[id(codes)])
         torch.cuda.synchronize()
-        assert all(torch.equal(a, b) for a, b in zip(ref, ys)), "graph replay differs"
+        assert all(torch.equal(ref[key], ys[key]) for key in ys), "graph replay differs"
         t = time_region(torch, stream, lambda i: g.replay(), steps, warmup)
         log(f"{name} m={m}: {t * 1e3:.1f} us per pass")
         out[f"m{m}"] = {"ms_per_token_pass": t, "tokens_per_s": m / (t * 1e-3),
                         "weight_GB_s": bytes_pass / t / 1e6,
                         "hbm_frac": bytes_pass / t / 1e6 / HBM_PEAK_GBS,
-                        "launches": len(tensors)}
+                        "launches": len(plan), "linears": len(tensors)}
         del g
     return {"bytes_per_pass": bytes_pass, "setup_s": setup_s, **out}
 
@@ -254,7 +290,7 @@ def cpu_baseline(L_unused, inputs, target_s=12.0):
         y = O.linear(x, O.dequantize(O.unpack(codes), lut))
         reps += 1
         el = time.perf_counter() - t0
-        if el >= target_s or reps >= 200:
+        if el >= target_s or reps >= 100000:
             break
     del y
     per = el / reps
@@ -278,6 +314,8 @@ def main():
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--quick", action="store_true", help="main layer only, no extra rows")
+    ap.add_argument("--rows", default="layer,small,decode1b,decode8b",
+                    help="comma list of extra rows: layer (M sweep + encode), small, decode1b, decode8b")
     ap.add_argument("--no-cpu", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -293,8 +331,10 @@ def main():
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
 
-    ms = [1] if args.quick else [1, 8, 32, 128]
-    res, info, codes, cb = bench_layer(torch, L, inputs, dev, stream, ms, args.steps, args.warmup)
+    want = set() if args.quick else set(args.rows.split(","))
+    ms = [1, 8, 32, 128] if "layer" in want else [1]
+    res, info, codes, cb = bench_layer(torch, L, inputs, dev, stream, ms, args.steps, args.warmup,
+                                       with_encode="layer" in want)
     main_row = res["linear_8192x28672_m1"]
     t_ms = main_row["ms"]
     packed = info["packed"]
@@ -302,15 +342,17 @@ def main():
     value = packed / t_ms / 1e6
 
     rows = dict(res)
-    if not args.quick:
+    if "small" in want:
         for name in ("up_2048x8192_outliers", "linear_2048x2048"):
             log(name)
             rows[name + "_m1"] = bench_small(torch, L, inputs, dev, stream, name, 2000, 100)
-        del codes
-        torch.cuda.empty_cache()
+    del codes
+    torch.cuda.empty_cache()
+    if "decode1b" in want:
         rows["decode_1b_16x7"] = bench_decode(torch, L, inputs, dev, stream, "decode_1b_16x7",
                                               [1], 200, 20)
         torch.cuda.empty_cache()
+    if "decode8b" in want:
         rows["decode_8b_32x7"] = bench_decode(torch, L, inputs, dev, stream, "decode_8b_32x7",
                                               [1, 4], 100, 10)
         torch.cuda.empty_cache()

@@ -120,6 +120,23 @@ int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t*
                      int64_t n, const float* codebook, float* y_dev, void* stream);
 
 /*
+ * logbq_linear_multi -- y_i = x . W_hat_i^T for 1 <= count <= 4 linears that share the same
+ * activations (the query / key / value projections of a decoder layer, or its gate and up
+ * projections), in one launch when the GEMV path applies (Sec. 3.3 lookup + product).
+ *   x_dev, m, k : as logbq_linear; every W_i has k in features.
+ *   count       : number of linears, 1..4.
+ *   codes_dev   : host array of count device pointers, [n[i]][k/2] packed codes each.
+ *   n           : host array of count out-feature counts (0 allowed).
+ *   codebooks   : host array of count host pointers to 16 floats each.
+ *   y_dev       : host array of count device pointers, [m][n[i]] float32 each.
+ * Each y_i equals, bit for bit, what logbq_linear would write for the same operands.
+ * Errors: INVALID_ARG (count outside 1..4, null arrays or entries), UNSUPPORTED, HIP.
+ */
+int32_t logbq_linear_multi(const uint16_t* x_dev, int64_t m, int64_t k, int32_t count,
+                           const uint8_t* const* codes_dev, const int64_t* n,
+                           const float* const* codebooks, float* const* y_dev, void* stream);
+
+/*
  * logbq_dequantize -- Dequant (Eq. 2) of packed codes into float32 weights, by lookup.
  *   codes_dev : device, [n][k/2]; codebook: host, 16 floats; w_dev: device, [n][k] float32.
  * Bit-exact: w[n][k] = codebook[code(n, k)]. Errors: INVALID_ARG, UNSUPPORTED, HIP.

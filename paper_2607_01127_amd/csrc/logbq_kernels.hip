@@ -33,6 +33,9 @@ typedef half_t half8v __attribute__((ext_vector_type(8)));
 typedef float float16v __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// Pointers into global memory, so that loads through them are global (not flat) loads.
+typedef const __attribute__((address_space(1))) uint8_t* GlobalU8;
+typedef const __attribute__((address_space(1))) u32x4* GlobalU32x4;
 
 struct Thresholds { float t[7]; };
 struct Codebook32 { float v[16]; };
@@ -43,26 +46,48 @@ constexpr int kLutCopies = 64;     // one copy per lane of a wavefront
 constexpr int kLutWords = kLutEntries * kLutCopies;
 
 // ------------------------------------------------------------------ encode
+// A wavefront encodes tiles of 64 * U float4 chunks (4 weights -> one 16-bit code group):
+// load j of lane l reads chunk tile * 64U + 64 j + l, so every load instruction covers 1 KiB of
+// contiguous weights and every store 128 contiguous bytes of codes; U loads are in flight per
+// lane. Chunk indices past the end are clamped for loading and not stored.
+constexpr int kEncU = 8;
+
+__device__ __forceinline__ uint32_t encode4(const f32x4 a, const Thresholds& th) {
+  const float v[4] = {a.x, a.y, a.z, a.w};
+  uint32_t out = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float x = v[j];
+    const float ax = __builtin_fabsf(x);
+    uint32_t mag = 0;
+#pragma unroll
+    for (int t = 0; t < 7; ++t) mag += (ax >= th.t[t]) ? 1u : 0u;
+    const uint32_t sgn = (x < 0.0f && mag != 0u) ? 8u : 0u;
+    out |= (mag | sgn) << (4 * j);
+  }
+  return out;
+}
+
 __global__ __launch_bounds__(256) void k_encode(const f32x4* __restrict__ w,
-                                                uint32_t* __restrict__ codes, int64_t nwords,
+                                                uint16_t* __restrict__ codes, int64_t nchunk,
                                                 Thresholds th) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nwords; i += stride) {
-    const f32x4 a = __builtin_nontemporal_load(w + 2 * i);
-    const f32x4 b = __builtin_nontemporal_load(w + 2 * i + 1);
-    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-    uint32_t out = 0;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  const int64_t ntiles = (nchunk + 64 * kEncU - 1) / (64 * kEncU);
+  for (int64_t t = wave; t < ntiles; t += nwaves) {
+    const int64_t base = t * 64 * kEncU + lane;
+    f32x4 v[kEncU];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float x = v[j];
-      const float ax = __builtin_fabsf(x);
-      uint32_t mag = 0;
-#pragma unroll
-      for (int t = 0; t < 7; ++t) mag += (ax >= th.t[t]) ? 1u : 0u;
-      const uint32_t sgn = (x < 0.0f && mag != 0u) ? 8u : 0u;
-      out |= (mag | sgn) << (4 * j);
+    for (int j = 0; j < kEncU; ++j) {
+      const int64_t idx = base + 64 * j;
+      v[j] = __builtin_nontemporal_load(w + (idx < nchunk ? idx : nchunk - 1));
     }
-    codes[i] = out;
+#pragma unroll
+    for (int j = 0; j < kEncU; ++j) {
+      const int64_t idx = base + 64 * j;
+      if (idx < nchunk) codes[idx] = (uint16_t)encode4(v[j], th);
+    }
   }
 }
 
@@ -95,7 +120,7 @@ __global__ __launch_bounds__(256) void k_fill_zero(float* __restrict__ y, int64_
 // ------------------------------------------------------------------ shared device helpers
 
 // float16 bits of table entry c (0..15).
-__device__ __forceinline__ uint32_t lut16_entry(const Lut16& lut, uint32_t c) {
+__device__ __forceinline__ uint32_t lut16_entry(const Lut16 lut, uint32_t c) {
   const uint32_t i = c >> 1;
   uint32_t w = lut.h[0];
   w = (i == 1) ? lut.h[1] : w; w = (i == 2) ? lut.h[2] : w; w = (i == 3) ? lut.h[3] : w;
@@ -107,7 +132,7 @@ __device__ __forceinline__ uint32_t lut16_entry(const Lut16& lut, uint32_t c) {
 // Fill the LDS pair table: word (e * 64 + lane) = f16(lut[e & 15]) | f16(lut[e >> 4]) << 16,
 // i.e. the two weights of code byte e in k order (low nibble = even k).
 template <int THREADS>
-__device__ __forceinline__ void fill_pair_lut(uint32_t* s_lut, const Lut16& lut) {
+__device__ __forceinline__ void fill_pair_lut(uint32_t* s_lut, const Lut16 lut) {
   constexpr int kThreadsPerEntry = THREADS / kLutEntries;
   constexpr int kWordsPerThread = kLutCopies / kThreadsPerEntry;
   const int t = threadIdx.x;
@@ -151,21 +176,85 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // ------------------------------------------------------------------ GEMV, m <= 8
 //
-// Work split: a workgroup of 8 wavefronts holds one LDS pair table. WK wavefronts share a row
-// (each takes an interleaved slice of the row's 16-byte chunks); the 8 / WK groups of a
-// workgroup take rows round-robin with every other group of the grid. Lane `l` of wavefront `kw`
-// in a group handles chunks c = s * 64 * WK + kw * 64 + l for s < CPL; its activations for those
-// chunks (M rows x 32 values each) stay in registers for the whole kernel. The next row's codes
-// are loaded before the current row is reduced.
+// One launch computes up to kMaxSegs linears that share the activations x (e.g. the query,
+// key and value projections of a layer): segment s owns workgroups [wg_begin, next wg_begin)
+// and its own codes, codebook table and output.
+//
+// Work split inside a segment: a workgroup of 8 wavefronts holds one LDS pair table. WK
+// wavefronts share a row (each takes an interleaved slice of the row's 16-byte chunks); the
+// 8 / WK groups of a workgroup take rows round-robin with the other groups of the segment. Lane
+// `l` of wavefront `kw` in a group handles chunks c = s * 64 * WK + kw * 64 + l for s < CPL; its
+// activations for those chunks (M rows x 32 values each) stay in registers for the whole kernel.
+//
+// Start-up: the first row's code loads are issued first; meanwhile x is staged once per
+// workgroup through LDS (when M * K halves fit the table's 64 KiB) and copied into registers,
+// then the pair table is written over the staging area. The row loop is unrolled by two over
+// two code buffers: the next row's loads are in flight while the current row is looked up,
+// multiplied and reduced. Every load is issued unconditionally (row and chunk indices are
+// clamped into the matrix; a clamped chunk meets zero activations), so the compiler waits for
+// exactly the buffer it is about to use.
+constexpr int kMaxSegs = 4;
+
+struct GemvSeg {
+  const uint8_t* codes;
+  float* y;
+  int n_rows;
+  int wg_begin;
+  int iters;
+  float scale;
+  Lut16 lut;
+};
+struct GemvSegs {
+  GemvSeg s[kMaxSegs];
+  int count;
+};
+
 template <int M, int CPL>
-__global__ __launch_bounds__(512) void k_gemv(const uint8_t* __restrict__ codes,
-                                              const uint16_t* __restrict__ x,
-                                              float* __restrict__ y, int n_rows, int k_cols,
-                                              int wk, int iters, Lut16 lut, float scale) {
+__device__ __forceinline__ void gemv_row(const u32x4 (&q)[CPL], const uint32_t (&xr)[M][CPL][16],
+                                         const uint32_t* s_lut, uint32_t laneoff,
+                                         float (&acc)[M]) {
+  float acc2[M];
+#pragma unroll
+  for (int m = 0; m < M; ++m) { acc[m] = 0.0f; acc2[m] = 0.0f; }
+#pragma unroll
+  for (int s = 0; s < CPL; ++s) {
+    const uint32_t dw[4] = {q[s].x, q[s].y, q[s].z, q[s].w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const half2v wp = as_half2(pair_lookup(s_lut, dw[j], laneoff, i));
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+          float& a = (i & 1) ? acc2[m] : acc[m];
+          a = __builtin_amdgcn_fdot2(wp, as_half2(xr[m][s][4 * j + i]), a, false);
+        }
+      }
+  }
+#pragma unroll
+  for (int m = 0; m < M; ++m) acc[m] += acc2[m];
+}
+
+template <int M, int CPL, bool SPLITK>
+__global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, int k_cols, int wk_arg,
+                                              int stage_x, GemvSegs segs) {
+  const int wk = SPLITK ? wk_arg : 1;
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[kLutWords];
   __shared__ float s_red[8][M];
 
-  fill_pair_lut<512>(s_lut, lut);
+  // Segment of this workgroup: a uniform index, so its fields are scalar kernel-argument loads.
+  const int bid = blockIdx.x;
+  int si = 0;
+#pragma unroll
+  for (int i = 1; i < kMaxSegs; ++i)
+    if (i < segs.count && bid >= segs.s[i].wg_begin) si = i;
+  const GlobalU8 codes = (GlobalU8)segs.s[si].codes;
+  float* __restrict__ y = segs.s[si].y;
+  const int n_rows = segs.s[si].n_rows;
+  const int iters = segs.s[si].iters;
+  const float scale = segs.s[si].scale;
+  const int wg_begin = segs.s[si].wg_begin;
+  const int next_begin = (si + 1 < segs.count) ? segs.s[si + 1].wg_begin : (int)gridDim.x;
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -174,72 +263,71 @@ __global__ __launch_bounds__(512) void k_gemv(const uint8_t* __restrict__ codes,
   const int groups = 8 / wk;
   const int nchunks = k_cols >> 5;
   const int64_t row_bytes = (int64_t)(k_cols >> 1);
+  const int total_groups = (next_begin - wg_begin) * groups;
+  const int gid = (bid - wg_begin) * groups + grp;
+  const uint32_t laneoff = (uint32_t)lane << 2;
 
-  int chunk[CPL];
+  int coff[CPL];   // byte offset of this lane's chunk s within a row (clamped into the row)
   bool cval[CPL];
 #pragma unroll
   for (int s = 0; s < CPL; ++s) {
-    chunk[s] = s * 64 * wk + kw * 64 + lane;
-    cval[s] = chunk[s] < nchunks;
+    const int c = s * 64 * wk + kw * 64 + lane;
+    cval[s] = c < nchunks;
+    coff[s] = (cval[s] ? c : nchunks - 1) * 16;
   }
 
-  uint32_t xr[M][CPL][16];
+  auto load_row = [&](int it, u32x4 (&q)[CPL]) {
+    int r = gid + it * total_groups;
+    r = r < n_rows ? r : n_rows - 1;
+    const GlobalU8 base = codes + (int64_t)r * row_bytes;
 #pragma unroll
-  for (int m = 0; m < M; ++m)
-#pragma unroll
-    for (int s = 0; s < CPL; ++s) {
-      u32x4 q0 = 0, q1 = 0, q2 = 0, q3 = 0;
-      if (cval[s]) {
-        const u32x4* px = reinterpret_cast<const u32x4*>(x + (int64_t)m * k_cols + (int64_t)chunk[s] * 32);
-        q0 = px[0]; q1 = px[1]; q2 = px[2]; q3 = px[3];
-      }
-      xr[m][s][0] = q0.x;  xr[m][s][1] = q0.y;  xr[m][s][2] = q0.z;  xr[m][s][3] = q0.w;
-      xr[m][s][4] = q1.x;  xr[m][s][5] = q1.y;  xr[m][s][6] = q1.z;  xr[m][s][7] = q1.w;
-      xr[m][s][8] = q2.x;  xr[m][s][9] = q2.y;  xr[m][s][10] = q2.z; xr[m][s][11] = q2.w;
-      xr[m][s][12] = q3.x; xr[m][s][13] = q3.y; xr[m][s][14] = q3.z; xr[m][s][15] = q3.w;
-    }
-
-  const int total_groups = gridDim.x * groups;
-  const int gid = blockIdx.x * groups + grp;
-  const uint32_t laneoff = (uint32_t)lane << 2;
-
-  auto load_row = [&](int r, u32x4 (&q)[CPL]) {
-#pragma unroll
-    for (int s = 0; s < CPL; ++s) {
-      q[s] = 0;
-      if (r < n_rows && cval[s])
-        q[s] = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(codes + (int64_t)r * row_bytes + (int64_t)chunk[s] * 16));
-    }
+    for (int s = 0; s < CPL; ++s)
+      q[s] = __builtin_nontemporal_load((GlobalU32x4)(base + coff[s]));
   };
 
-  u32x4 cur[CPL], nxt[CPL];
-  load_row(gid, cur);
-  __syncthreads();  // pair table ready
+  u32x4 qa[CPL], qb[CPL];
 
-  for (int it = 0; it < iters; ++it) {
-    const int r = gid + it * total_groups;
-    if (it + 1 < iters) load_row(r + total_groups, nxt);
-
-    float acc[M];
-#pragma unroll
-    for (int m = 0; m < M; ++m) acc[m] = 0.0f;
+  uint32_t xr[M][CPL][16];
+  if (stage_x) {
+    const int nvec = (M * k_cols) >> 3;   // 16-byte vectors of x
+    for (int i = threadIdx.x; i < nvec; i += 512)
+      *reinterpret_cast<u32x4*>(s_lut + 4 * i) = *reinterpret_cast<const u32x4*>(x + 8 * (int64_t)i);
+    __syncthreads();
 #pragma unroll
     for (int s = 0; s < CPL; ++s) {
-      if (!cval[s]) continue;
-      const uint32_t dw[4] = {cur[s].x, cur[s].y, cur[s].z, cur[s].w};
+      const int c = cval[s] ? s * 64 * wk + kw * 64 + lane : 0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const half2v wp = as_half2(pair_lookup(s_lut, dw[j], laneoff, i));
-#pragma unroll
-          for (int m = 0; m < M; ++m)
-            acc[m] = __builtin_amdgcn_fdot2(wp, as_half2(xr[m][s][4 * j + i]), acc[m], false);
+        for (int q = 0; q < 4; ++q) {
+          u32x4 v = *reinterpret_cast<const u32x4*>(s_lut + ((m * k_cols + c * 32) >> 1) + 4 * q);
+          if (!cval[s]) v = 0;
+          xr[m][s][4 * q] = v.x; xr[m][s][4 * q + 1] = v.y;
+          xr[m][s][4 * q + 2] = v.z; xr[m][s][4 * q + 3] = v.w;
         }
     }
+    __syncthreads();   // staging area is about to become the pair table
+  } else {
+#pragma unroll
+    for (int s = 0; s < CPL; ++s) {
+      const int c = s * 64 * wk + kw * 64 + lane;
+#pragma unroll
+      for (int m = 0; m < M; ++m)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          u32x4 v = 0;
+          if (cval[s]) v = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k_cols + (int64_t)c * 32 + 8 * q);
+          xr[m][s][4 * q] = v.x; xr[m][s][4 * q + 1] = v.y;
+          xr[m][s][4 * q + 2] = v.z; xr[m][s][4 * q + 3] = v.w;
+        }
+    }
+  }
+  fill_pair_lut<512>(s_lut, segs.s[si].lut);
+  load_row(0, qa);
 
-    if (wk == 1) {
+  auto finish_row = [&](int it, float (&acc)[M]) {
+    const int r = gid + it * total_groups;
+    if (!SPLITK) {
 #pragma unroll
       for (int m = 0; m < M; ++m) {
         const float t = wave_sum(acc[m]);
@@ -259,8 +347,30 @@ __global__ __launch_bounds__(512) void k_gemv(const uint8_t* __restrict__ codes,
       }
       __syncthreads();
     }
-#pragma unroll
-    for (int s = 0; s < CPL; ++s) cur[s] = nxt[s];
+  };
+
+  float acc[M];
+  __syncthreads();  // pair table ready
+
+  // Main loop: rows it and it + 1 are computed while rows it + 1 and it + 2 are in flight.
+  int it = 0;
+  for (; it + 2 < iters; it += 2) {
+    load_row(it + 1, qb);
+    gemv_row<M, CPL>(qa, xr, s_lut, laneoff, acc);
+    finish_row(it, acc);
+    load_row(it + 2, qa);
+    gemv_row<M, CPL>(qb, xr, s_lut, laneoff, acc);
+    finish_row(it + 1, acc);
+  }
+  if (it + 2 == iters) {
+    load_row(it + 1, qb);
+    gemv_row<M, CPL>(qa, xr, s_lut, laneoff, acc);
+    finish_row(it, acc);
+    gemv_row<M, CPL>(qb, xr, s_lut, laneoff, acc);
+    finish_row(it + 1, acc);
+  } else if (it + 1 == iters) {
+    gemv_row<M, CPL>(qa, xr, s_lut, laneoff, acc);
+    finish_row(it, acc);
   }
 }
 
@@ -295,45 +405,42 @@ __global__ __launch_bounds__(256) void k_mfma(const uint8_t* __restrict__ codes,
   const int64_t row_bytes = (int64_t)(k_cols >> 1);
   const uint32_t laneoff = (uint32_t)lane << 2;
   const int row = n0 + j;
+  const GlobalU8 crow = (GlobalU8)codes + (int64_t)(row < n_rows ? row : n_rows - 1) * row_bytes;
 
-  auto stage_x = [&](int step, int buf) {
+  // Activation tile of one step: MT * 32 rows x 64 halves, 16 bytes per thread and pass.
+  // Loads are clamped in bounds; rows past m_rows and columns past k_cols are zeroed when the
+  // tile is written to LDS.
+  auto load_x = [&](int step, u32x4 (&v)[MT]) {
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
       const int idx = t + 256 * i;
-      const int m = idx >> 3;
-      const int sg = idx & 7;
-      const int kk = step * 64 + sg * 8;
-      u32x4 v = 0;
-      if (mb + m < m_rows && kk < k_cols)
-        v = *reinterpret_cast<const u32x4*>(x + (int64_t)(mb + m) * k_cols + kk);
-      *reinterpret_cast<u32x4*>(&s_x[buf][m][sg * 8]) = v;
+      const int m = mb + (idx >> 3);
+      const int kk = step * 64 + (idx & 7) * 8;
+      const int mc = m < m_rows ? m : m_rows - 1;
+      const int kc = kk < k_cols ? kk : k_cols - 8;
+      v[i] = *(GlobalU32x4)((const __attribute__((address_space(1))) uint16_t*)x +
+                            (int64_t)mc * k_cols + kc);
     }
   };
+  auto store_x = [&](int step, int buf, const u32x4 (&v)[MT]) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int idx = t + 256 * i;
+      const uint32_t keep =
+          0u - (uint32_t)((mb + (idx >> 3) < m_rows) & (step * 64 + (idx & 7) * 8 < k_cols));
+      u32x4 w;
+      w.x = v[i].x & keep; w.y = v[i].y & keep; w.z = v[i].z & keep; w.w = v[i].w & keep;
+      *reinterpret_cast<u32x4*>(&s_x[buf][idx >> 3][(idx & 7) * 8]) = w;
+    }
+  };
+  // Codes of one step: bytes [32 step + 16 h, +16) of this lane's row (clamped into the row;
+  // a clamped chunk only ever meets zero activations).
   auto load_codes = [&](int step) {
-    u32x4 q = 0;
-    if (row < n_rows && step * 64 + 32 * h < k_cols)
-      q = __builtin_nontemporal_load(
-          reinterpret_cast<const u32x4*>(codes + (int64_t)row * row_bytes + step * 32 + 16 * h));
-    return q;
+    int off = step * 32 + 16 * h;
+    off = (int64_t)off + 16 <= row_bytes ? off : (int)row_bytes - 16;
+    return __builtin_nontemporal_load((GlobalU32x4)(crow + off));
   };
-
-  float16v acc[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
-
-  u32x4 q = load_codes(0);
-  stage_x(0, 0);
-  __syncthreads();
-
-  for (int step = 0; step < nsteps; ++step) {
-    const int buf = step & 1;
-    u32x4 qn = 0;
-    if (step + 1 < nsteps) {
-      qn = load_codes(step + 1);
-      stage_x(step + 1, buf ^ 1);
-    }
+  auto mma_step = [&](int buf, const u32x4 q, float16v (&acc)[MT]) {
     const uint32_t dw[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
@@ -352,7 +459,38 @@ __global__ __launch_bounds__(256) void k_mfma(const uint8_t* __restrict__ codes,
         acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc[mt], 0, 0, 0);
       }
     }
-    q = qn;
+  };
+
+  float16v acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
+
+  // Software pipeline, unrolled by two (buffers a / b): while step s is multiplied out of LDS
+  // buffer s & 1, the activations of step s + 1 sit in registers (written to the other buffer
+  // after the step) and the codes of step s + 1 and the loads of step s + 2 are in flight.
+  // An odd step count runs one extra step past k_cols, whose activations are all zero.
+  const int last = nsteps - 1;
+  const int nsteps2 = (nsteps + 1) & ~1;
+  u32x4 xa[MT], xb[MT];
+  load_x(0, xa);
+  u32x4 qa = load_codes(0);
+  load_x(1 < last ? 1 : last, xb);
+  u32x4 qb = load_codes(1 < last ? 1 : last);
+  store_x(0, 0, xa);
+  __syncthreads();
+
+  for (int step = 0; step < nsteps2; step += 2) {
+    mma_step(0, qa, acc);
+    store_x(step + 1, 1, xb);
+    load_x(step + 2 < last ? step + 2 : last, xa);
+    qa = load_codes(step + 2 < last ? step + 2 : last);
+    __syncthreads();
+    mma_step(1, qb, acc);
+    store_x(step + 2, 0, xa);
+    load_x(step + 3 < last ? step + 3 : last, xb);
+    qb = load_codes(step + 3 < last ? step + 3 : last);
     __syncthreads();
   }
 
@@ -440,24 +578,140 @@ int64_t grid_for(int64_t items, int64_t per_block, int64_t cap) {
 }
 
 template <int M, int CPL>
-void launch_gemv(dim3 grid, hipStream_t st, const uint8_t* codes, const uint16_t* x, float* y,
-                 int n, int k, int wk, int iters, const Lut16& lut, float scale) {
-  hipLaunchKernelGGL((k_gemv<M, CPL>), grid, dim3(512), 0, st, codes, x, y, n, k, wk, iters, lut,
-                     scale);
+void launch_gemv(int grid, hipStream_t st, const uint16_t* x, int k, int wk, int stage_x,
+                 const GemvSegs& segs) {
+  if (wk == 1)
+    hipLaunchKernelGGL((k_gemv<M, CPL, false>), dim3((unsigned)grid), dim3(512), 0, st, x, k, 1,
+                       stage_x, segs);
+  else
+    hipLaunchKernelGGL((k_gemv<M, CPL, true>), dim3((unsigned)grid), dim3(512), 0, st, x, k, wk,
+                       stage_x, segs);
 }
 
-bool dispatch_gemv(int m, int cpl, dim3 grid, hipStream_t st, const uint8_t* codes,
-                   const uint16_t* x, float* y, int n, int k, int wk, int iters, const Lut16& lut,
-                   float scale) {
+bool dispatch_gemv(int m, int cpl, int grid, hipStream_t st, const uint16_t* x, int k, int wk,
+                   int stage_x, const GemvSegs& segs) {
 #define LOGBQ_G(MM, CC) \
-  if (m == MM && cpl == CC) { launch_gemv<MM, CC>(grid, st, codes, x, y, n, k, wk, iters, lut, scale); return true; }
-  LOGBQ_G(1, 1) LOGBQ_G(1, 2) LOGBQ_G(1, 4) LOGBQ_G(1, 8)
-  LOGBQ_G(2, 1) LOGBQ_G(2, 2) LOGBQ_G(2, 4)
+  if (m == MM && cpl == CC) { launch_gemv<MM, CC>(grid, st, x, k, wk, stage_x, segs); return true; }
+  LOGBQ_G(1, 1) LOGBQ_G(1, 2) LOGBQ_G(1, 3) LOGBQ_G(1, 4) LOGBQ_G(1, 5) LOGBQ_G(1, 6) LOGBQ_G(1, 7) LOGBQ_G(1, 8)
+  LOGBQ_G(2, 1) LOGBQ_G(2, 2) LOGBQ_G(2, 3) LOGBQ_G(2, 4)
   LOGBQ_G(3, 1) LOGBQ_G(3, 2)
   LOGBQ_G(4, 1) LOGBQ_G(4, 2)
   LOGBQ_G(5, 1) LOGBQ_G(6, 1) LOGBQ_G(7, 1) LOGBQ_G(8, 1)
 #undef LOGBQ_G
   return false;
+}
+
+// GEMV configuration for m batch rows and k columns: WK wavefronts per row and CPL chunks per
+// lane, keeping the activations at most 8 x 16 registers per lane. Returns false when even
+// WK = 8 does not fit (the MFMA path takes those shapes).
+bool gemv_config(int m, int k, int* wk, int* cpl) {
+  if (m < 1 || m > 8) return false;
+  const int nchunks = k / 32;
+  const int cplmax = 8 / m;
+  for (int w = 1; w <= 8; w *= 2) {
+    const int per = (nchunks + 64 * w - 1) / (64 * w);
+    if (per <= cplmax && (w == 1 || nchunks >= 32 * w)) {
+      *wk = w;
+      *cpl = per < 1 ? 1 : per;
+      return true;
+    }
+  }
+  return false;
+}
+
+struct LinearJob {
+  const uint8_t* codes;
+  int64_t n;
+  const float* codebook;
+  float* y;
+};
+
+int32_t validate_job(const LinearJob& j, int64_t m, int64_t k) {
+  if (!j.codebook || j.n < 0) return LOGBQ_ERR_INVALID_ARG;
+  if (j.n > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
+  for (int i = 0; i < 16; ++i)
+    if (!std::isfinite(j.codebook[i])) return LOGBQ_ERR_INVALID_ARG;
+  if (m == 0 || j.n == 0) return LOGBQ_OK;
+  if (!j.y) return LOGBQ_ERR_INVALID_ARG;
+  if (!aligned16(j.y)) return LOGBQ_ERR_UNSUPPORTED;
+  if (k > 0) {
+    if (!j.codes) return LOGBQ_ERR_INVALID_ARG;
+    if (!aligned16(j.codes)) return LOGBQ_ERR_UNSUPPORTED;
+  }
+  return LOGBQ_OK;
+}
+
+int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st) {
+  Lut16 lut;
+  float scale;
+  make_lut16(j.codebook, &lut, &scale);
+  const int N = (int)j.n;
+  const int mt = M >= 97 ? 4 : (M >= 65 ? 3 : (M >= 33 ? 2 : 1));
+  const int mblock = mt * 32;
+  dim3 grid((unsigned)((N + 127) / 128), (unsigned)((M + mblock - 1) / mblock));
+  switch (mt) {
+    case 1: hipLaunchKernelGGL(k_mfma<1>, grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, lut, scale); break;
+    case 2: hipLaunchKernelGGL(k_mfma<2>, grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, lut, scale); break;
+    case 3: hipLaunchKernelGGL(k_mfma<3>, grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, lut, scale); break;
+    default: hipLaunchKernelGGL(k_mfma<4>, grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, lut, scale); break;
+  }
+  return launch_status();
+}
+
+// y_i = x . W_hat_i^T for up to kMaxSegs linears sharing x (validated by the caller).
+int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jobs, int count,
+                    hipStream_t st) {
+  int live[kMaxSegs];
+  int nlive = 0;
+  int64_t rows = 0;
+  for (int i = 0; i < count; ++i)
+    if (jobs[i].n > 0) { live[nlive++] = i; rows += jobs[i].n; }
+  if (m == 0 || nlive == 0) return LOGBQ_OK;
+  const int cus = device_cus();
+  if (cus <= 0) return LOGBQ_ERR_HIP;
+  if (k == 0) {
+    for (int a = 0; a < nlive; ++a) {
+      const LinearJob& j = jobs[live[a]];
+      const int64_t cnt = m * j.n;
+      hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)grid_for(cnt, 256, (int64_t)cus * 16)),
+                         dim3(256), 0, st, j.y, cnt);
+      if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
+    }
+    return LOGBQ_OK;
+  }
+  const int M = (int)m, K = (int)k;
+  int wk = 0, cpl = 0;
+  if (gemv_config(M, K, &wk, &cpl)) {
+    const int groups = 8 / wk;
+    GemvSegs segs;
+    std::memset(&segs, 0, sizeof(segs));
+    segs.count = nlive;
+    int begin = 0;
+    for (int a = 0; a < nlive; ++a) {
+      const LinearJob& j = jobs[live[a]];
+      const int64_t need = (j.n + groups - 1) / groups;          // workgroups that have rows
+      int64_t share = (int64_t)((double)cus * (double)j.n / (double)rows + 0.5);
+      if (share < 1) share = 1;
+      if (share > need) share = need;
+      GemvSeg& sg = segs.s[a];
+      sg.codes = j.codes;
+      sg.y = j.y;
+      sg.n_rows = (int)j.n;
+      sg.wg_begin = begin;
+      const int64_t tg = share * groups;
+      sg.iters = (int)((j.n + tg - 1) / tg);
+      make_lut16(j.codebook, &sg.lut, &sg.scale);
+      begin += (int)share;
+    }
+    const int stage_x = ((int64_t)M * K * 2 <= (int64_t)kLutWords * 4) ? 1 : 0;
+    if (!dispatch_gemv(M, cpl, begin, st, x, K, wk, stage_x, segs)) return LOGBQ_ERR_UNSUPPORTED;
+    return launch_status();
+  }
+  for (int a = 0; a < nlive; ++a) {
+    const int32_t r = launch_mfma(x, M, K, jobs[live[a]], st);
+    if (r != LOGBQ_OK) return r;
+  }
+  return LOGBQ_OK;
 }
 
 }  // namespace
@@ -485,11 +739,11 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
   if (numel == 0) return LOGBQ_OK;
   const int cus = device_cus();
   if (cus <= 0) return LOGBQ_ERR_HIP;
-  const int64_t nwords = numel / 8;
-  const int64_t grid = grid_for(nwords, 256, (int64_t)cus * 16);
+  const int64_t nchunk = numel / 4;
+  const int64_t grid = grid_for(nchunk, 256 * kEncU, (int64_t)cus * 8);
   hipLaunchKernelGGL(k_encode, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream,
-                     reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint32_t*>(codes_dev),
-                     nwords, th);
+                     reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint16_t*>(codes_dev),
+                     nchunk, th);
   return launch_status();
 }
 
@@ -516,66 +770,41 @@ int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const f
 
 int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
                      int64_t n, const float* codebook, float* y_dev, void* stream) {
-  if (!codebook || m < 0 || k < 0 || n < 0) return LOGBQ_ERR_INVALID_ARG;
+  if (m < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
   if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
-  if (m > INT32_MAX || n > INT32_MAX || k > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
-  for (int i = 0; i < 16; ++i)
-    if (!std::isfinite(codebook[i])) return LOGBQ_ERR_INVALID_ARG;
+  if (m > INT32_MAX || k > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
+  LinearJob j{codes_dev, n, codebook, y_dev};
+  const int32_t v = validate_job(j, m, k);
+  if (v != LOGBQ_OK) return v;
   if (m == 0 || n == 0) return LOGBQ_OK;
-  if (!y_dev) return LOGBQ_ERR_INVALID_ARG;
-  if (!aligned16(y_dev)) return LOGBQ_ERR_UNSUPPORTED;
-  hipStream_t st = (hipStream_t)stream;
-  const int cus = device_cus();
-  if (k == 0) {
-    if (cus <= 0) return LOGBQ_ERR_HIP;
-    const int64_t count = m * n;
-    hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)grid_for(count, 256, (int64_t)cus * 16)),
-                       dim3(256), 0, st, y_dev, count);
-    return launch_status();
+  if (k > 0) {
+    if (!x_dev) return LOGBQ_ERR_INVALID_ARG;
+    if (!aligned16(x_dev)) return LOGBQ_ERR_UNSUPPORTED;
   }
-  if (!x_dev || !codes_dev) return LOGBQ_ERR_INVALID_ARG;
-  if (!aligned16(x_dev) || !aligned16(codes_dev)) return LOGBQ_ERR_UNSUPPORTED;
-  if (cus <= 0) return LOGBQ_ERR_HIP;
-  Lut16 lut;
-  float scale;
-  make_lut16(codebook, &lut, &scale);
-  const int N = (int)n, K = (int)k, Mi = (int)m;
+  return run_linears(x_dev, m, k, &j, 1, (hipStream_t)stream);
+}
 
-  if (Mi <= 8) {
-    const int nchunks = K / 32;
-    const int cplmax = 8 / Mi;
-    int wk = 0, cpl = 0;
-    for (int w = 1; w <= 8; w *= 2) {
-      const int per = (nchunks + 64 * w - 1) / (64 * w);
-      if (per <= cplmax) {
-        wk = w;
-        cpl = 1;
-        while (cpl < per) cpl *= 2;
-        break;
-      }
-    }
-    if (wk > 0) {
-      const int groups = 8 / wk;
-      const int64_t grid = grid_for(N, groups, (int64_t)cus * 2);
-      const int total_groups = (int)grid * groups;
-      const int iters = (N + total_groups - 1) / total_groups;
-      if (!dispatch_gemv(Mi, cpl, dim3((unsigned)grid), st, codes_dev, x_dev, y_dev, N, K, wk,
-                         iters, lut, scale))
-        return LOGBQ_ERR_UNSUPPORTED;
-      return launch_status();
-    }
+int32_t logbq_linear_multi(const uint16_t* x_dev, int64_t m, int64_t k, int32_t count,
+                           const uint8_t* const* codes_dev, const int64_t* n,
+                           const float* const* codebooks, float* const* y_dev, void* stream) {
+  if (m < 0 || k < 0 || count < 1 || count > kMaxSegs) return LOGBQ_ERR_INVALID_ARG;
+  if (!codes_dev || !n || !codebooks || !y_dev) return LOGBQ_ERR_INVALID_ARG;
+  if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
+  if (m > INT32_MAX || k > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
+  LinearJob jobs[kMaxSegs];
+  bool any = false;
+  for (int i = 0; i < count; ++i) {
+    jobs[i] = LinearJob{codes_dev[i], n[i], codebooks[i], y_dev[i]};
+    const int32_t v = validate_job(jobs[i], m, k);
+    if (v != LOGBQ_OK) return v;
+    any = any || n[i] > 0;
   }
-  // MFMA skinny GEMM: up to 128 batch rows per workgroup column.
-  const int mt = Mi >= 97 ? 4 : (Mi >= 65 ? 3 : (Mi >= 33 ? 2 : 1));
-  const int mblock = mt * 32;
-  dim3 grid((unsigned)((N + 127) / 128), (unsigned)((Mi + mblock - 1) / mblock));
-  switch (mt) {
-    case 1: hipLaunchKernelGGL(k_mfma<1>, grid, dim3(256), 0, st, codes_dev, x_dev, y_dev, N, K, Mi, lut, scale); break;
-    case 2: hipLaunchKernelGGL(k_mfma<2>, grid, dim3(256), 0, st, codes_dev, x_dev, y_dev, N, K, Mi, lut, scale); break;
-    case 3: hipLaunchKernelGGL(k_mfma<3>, grid, dim3(256), 0, st, codes_dev, x_dev, y_dev, N, K, Mi, lut, scale); break;
-    default: hipLaunchKernelGGL(k_mfma<4>, grid, dim3(256), 0, st, codes_dev, x_dev, y_dev, N, K, Mi, lut, scale); break;
+  if (m == 0 || !any) return LOGBQ_OK;
+  if (k > 0) {
+    if (!x_dev) return LOGBQ_ERR_INVALID_ARG;
+    if (!aligned16(x_dev)) return LOGBQ_ERR_UNSUPPORTED;
   }
-  return launch_status();
+  return run_linears(x_dev, m, k, jobs, count, (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -55,6 +55,9 @@ SIGNATURES = {
                                c_void_p, c_void_p]),
     "logbq_dequantize": (c_int32, [c_void_p, c_int64, c_int64, POINTER(c_float), c_void_p,
                                    c_void_p]),
+    "logbq_linear_multi": (c_int32, [c_void_p, c_int64, c_int64, c_int32, POINTER(c_void_p),
+                                     POINTER(c_int64), POINTER(POINTER(c_float)),
+                                     POINTER(c_void_p), c_void_p]),
 }
 
 
@@ -144,6 +147,31 @@ def linear(x, codes, codebook, out=None, stream=None):
     _check(lib().logbq_linear(c_void_p(x.data_ptr()), m, k, c_void_p(codes.data_ptr()), n, cbp,
                               c_void_p(out.data_ptr()), _stream(stream)), "logbq_linear")
     return out
+
+
+def linear_multi(x, codes_list, codebooks, outs=None, stream=None):
+    """logbq_linear_multi: y_i = x . W_hat_i^T for up to 4 linears sharing x (one launch)."""
+    import torch
+    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous 2-D float16 device tensor")
+    m, k = x.shape
+    count = len(codes_list)
+    if not 1 <= count <= 4 or len(codebooks) != count:
+        raise ValueError("need 1..4 linears with one codebook each")
+    for c in codes_list:
+        if c.dtype != torch.uint8 or c.dim() != 2 or not c.is_contiguous() or c.shape[1] * 2 != k:
+            raise ValueError("codes must be contiguous uint8 [N][K/2] device tensors")
+    if outs is None:
+        outs = [torch.empty((m, c.shape[0]), dtype=torch.float32, device=x.device)
+                for c in codes_list]
+    keep = [_cb_ptr(cb) for cb in codebooks]
+    cptr = (c_void_p * count)(*[c.data_ptr() for c in codes_list])
+    ns = (c_int64 * count)(*[c.shape[0] for c in codes_list])
+    cbs = (POINTER(c_float) * count)(*[p for p, _ in keep])
+    ys = (c_void_p * count)(*[y.data_ptr() for y in outs])
+    _check(lib().logbq_linear_multi(c_void_p(x.data_ptr()), m, k, count, cptr, ns, cbs, ys,
+                                    _stream(stream)), "logbq_linear_multi")
+    return outs
 
 
 def dequantize(codes, codebook, out=None, stream=None):
