@@ -31,6 +31,7 @@ typedef _Float16 half_t;
 typedef half_t half2v __attribute__((ext_vector_type(2)));
 typedef half_t half8v __attribute__((ext_vector_type(8)));
 typedef float float16v __attribute__((ext_vector_type(16)));
+typedef float float4v __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // Pointers into global memory, so that loads through them are global (not flat) loads.
@@ -130,18 +131,20 @@ __device__ __forceinline__ uint32_t lut16_entry(const Lut16 lut, uint32_t c) {
 }
 
 // Fill the LDS pair table: word (e * 64 + lane) = f16(lut[e & 15]) | f16(lut[e >> 4]) << 16,
-// i.e. the two weights of code byte e in k order (low nibble = even k).
+// i.e. the two weights of code byte e in k order (low nibble = even k). Thread t writes the
+// 16-byte vectors t, t + THREADS, ..., so each store instruction covers contiguous LDS and
+// never conflicts on a bank; vector v holds entry v / 16.
 template <int THREADS>
 __device__ __forceinline__ void fill_pair_lut(uint32_t* s_lut, const Lut16 lut) {
-  constexpr int kThreadsPerEntry = THREADS / kLutEntries;
-  constexpr int kWordsPerThread = kLutCopies / kThreadsPerEntry;
+  constexpr int kVecs = kLutWords / 4;
   const int t = threadIdx.x;
-  const uint32_t e = (uint32_t)(t / kThreadsPerEntry);
-  const uint32_t v = lut16_entry(lut, e & 15u) | (lut16_entry(lut, e >> 4) << 16);
-  const u32x4 vv = v;
-  u32x4* dst = reinterpret_cast<u32x4*>(s_lut + e * kLutCopies + (t % kThreadsPerEntry) * kWordsPerThread);
 #pragma unroll
-  for (int i = 0; i < kWordsPerThread / 4; ++i) dst[i] = vv;
+  for (int i = 0; i < kVecs / THREADS; ++i) {
+    const uint32_t e = (uint32_t)((t + THREADS * i) >> 4);
+    const uint32_t v = lut16_entry(lut, e & 15u) | (lut16_entry(lut, e >> 4) << 16);
+    const u32x4 vv = v;
+    *reinterpret_cast<u32x4*>(s_lut + 4 * (t + THREADS * i)) = vv;
+  }
 }
 
 // The float16 pair for byte `i` (0..3) of code dword `d`, read from this lane's private copy.
@@ -186,14 +189,19 @@ __device__ __forceinline__ float wave_sum(float v) {
 // `l` of wavefront `kw` in a group handles chunks c = s * 64 * WK + kw * 64 + l for s < CPL; its
 // activations for those chunks (M rows x 32 values each) stay in registers for the whole kernel.
 //
-// Start-up: the first row's code loads are issued first; meanwhile x is staged once per
-// workgroup through LDS (when M * K halves fit the table's 64 KiB) and copied into registers,
-// then the pair table is written over the staging area. The row loop is unrolled by two over
+// Start-up: x (when M * K * 2 <= 32 KiB) is requested first and staged once per workgroup
+// through LDS into registers; the first row of codes is requested next; the pair table is
+// written while both are in flight. The row loop is unrolled by two over
 // two code buffers: the next row's loads are in flight while the current row is looked up,
 // multiplied and reduced. Every load is issued unconditionally (row and chunk indices are
 // clamped into the matrix; a clamped chunk meets zero activations), so the compiler waits for
 // exactly the buffer it is about to use.
 constexpr int kMaxSegs = 4;
+constexpr int kStageXBytes = 32768;   // activations staged through LDS when M * K * 2 fits
+// Staged activations keep every 64-byte chunk (the 32 values one lane multiplies with one
+// 16-byte code chunk) at an 80-byte stride, so the four 16-byte reads of consecutive lanes
+// fall on distinct LDS banks.
+constexpr int kStageXPadded = kStageXBytes / 64 * 80;
 
 struct GemvSeg {
   const uint8_t* codes;
@@ -240,6 +248,7 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
                                               int stage_x, GemvSegs segs) {
   const int wk = SPLITK ? wk_arg : 1;
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[kLutWords];
+  __shared__ __attribute__((aligned(16))) uint32_t s_x[kStageXPadded / 4];
   __shared__ float s_red[8][M];
 
   // Segment of this workgroup: a uniform index, so its fields are scalar kernel-argument loads.
@@ -287,11 +296,29 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
 
   u32x4 qa[CPL], qb[CPL];
 
+  // Start-up, ordered so that the memory system is busy from the first cycle: the staged
+  // activations are requested first (they return first), then the first row of codes; the
+  // pair table is written while both are in flight.
+  constexpr int kXVec = kStageXBytes / 16 / 512;     // 16-byte x vectors per thread
+  u32x4 xv[kXVec];
+  const int nvec = (M * k_cols) >> 3;                // 16-byte vectors of x
+  if (stage_x) {
+#pragma unroll
+    for (int v = 0; v < kXVec; ++v) {
+      const int i = threadIdx.x + 512 * v;
+      xv[v] = *reinterpret_cast<const u32x4*>(x + 8 * (int64_t)(i < nvec ? i : 0));
+    }
+  }
+  load_row(0, qa);
+  fill_pair_lut<512>(s_lut, segs.s[si].lut);
+
   uint32_t xr[M][CPL][16];
   if (stage_x) {
-    const int nvec = (M * k_cols) >> 3;   // 16-byte vectors of x
-    for (int i = threadIdx.x; i < nvec; i += 512)
-      *reinterpret_cast<u32x4*>(s_lut + 4 * i) = *reinterpret_cast<const u32x4*>(x + 8 * (int64_t)i);
+#pragma unroll
+    for (int v = 0; v < kXVec; ++v) {
+      const int i = threadIdx.x + 512 * v;
+      if (i < nvec) *reinterpret_cast<u32x4*>(s_x + 4 * (i + (i >> 2))) = xv[v];
+    }
     __syncthreads();
 #pragma unroll
     for (int s = 0; s < CPL; ++s) {
@@ -300,13 +327,13 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
       for (int m = 0; m < M; ++m)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          u32x4 v = *reinterpret_cast<const u32x4*>(s_lut + ((m * k_cols + c * 32) >> 1) + 4 * q);
+          const int vi = ((m * k_cols + c * 32) >> 3) + q;    // 16-byte vector index
+          u32x4 v = *reinterpret_cast<const u32x4*>(s_x + 4 * (vi + (vi >> 2)));
           if (!cval[s]) v = 0;
           xr[m][s][4 * q] = v.x; xr[m][s][4 * q + 1] = v.y;
           xr[m][s][4 * q + 2] = v.z; xr[m][s][4 * q + 3] = v.w;
         }
     }
-    __syncthreads();   // staging area is about to become the pair table
   } else {
 #pragma unroll
     for (int s = 0; s < CPL; ++s) {
@@ -322,8 +349,6 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
         }
     }
   }
-  fill_pair_lut<512>(s_lut, segs.s[si].lut);
-  load_row(0, qa);
 
   auto finish_row = [&](int it, float (&acc)[M]) {
     const int r = gid + it * total_groups;
@@ -350,7 +375,7 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
   };
 
   float acc[M];
-  __syncthreads();  // pair table ready
+  __syncthreads();  // pair table ready (and, when staged, x read out of LDS)
 
   // Main loop: rows it and it + 1 are computed while rows it + 1 and it + 2 are in flight.
   int it = 0;
@@ -374,131 +399,183 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
   }
 }
 
-// ------------------------------------------------------------------ MFMA skinny GEMM
+// ------------------------------------------------------------------ MFMA skinny GEMM, register dequant
 //
-// Workgroup = 4 wavefronts = 128 weight rows (32 per wavefront) x MT * 32 batch rows.
-// K advances 64 per step: lane (j = l % 32, h = l / 32) loads 16 code bytes of row n0 + j at
-// byte 32 * step + 16 h, i.e. k in [64 step + 32 h, +32). Dword d of that load is the B operand
-// of the d-th v_mfma_f32_32x32x16_f16 (8 weights of column j); the A operand of lane (i, h) is
-// x[i][64 step + 32 h + 8 d .. +8], read from the LDS activation tile. Both operands use the
-// same k order, so every MFMA contracts 16 matching (x, w) pairs.
-constexpr int kXPad = 72;   // halves per staged activation row (64 + 8 padding)
+// For sign-symmetric codebooks (codebook[8 + k] = -codebook[k], codebook[k] >= 0 for k < 8,
+// which every fitted codebook is) a code dword is dequantized in registers: the magnitude
+// nibbles index 8-byte tables of the float16 low and high bytes with v_perm_b32, the sign bits
+// are OR-ed into the high bytes, and four more v_perm_b32 assemble the float16 pairs. The B
+// operand then holds the eight weights of the dword in the order k0 k2 k4 k6 k1 k3 k5 k7; the
+// activation tile is written to LDS in that same order, so each MFMA still contracts matching
+// (x, w) pairs. Without the 64 KiB pair table, LDS holds a ring of activation tiles and the
+// codes of STAGES steps stay in flight per wavefront.
+//
+// Tiling: v_mfma_f32_16x16x32_f16 with the activations as A (16 batch rows x 32 K) and the
+// weights as B (32 K x 16 weight rows). A workgroup of 8 wavefronts owns 128 weight rows
+// (16 per wavefront) and MT * 16 batch rows; every wavefront walks the whole K in steps of
+// 256. Lane (j = l % 16, g = l / 16) owns weight row n0 + j and loads code bytes
+// [128 step + 32 g, +32), i.e. k in [256 step + 64 g, +64): eight dwords, one per MFMA.
+// MFMA d multiplies, for lanes g, k = 256 step + 64 g + 8 d + 0..7; the A operand of lane
+// (i, g) is x[i][256 step + 64 g + 8 d .. +8] from the LDS tile (same within-8 order).
+// Activation tiles of STAGES - 1 steps ahead sit in an LDS ring; codes of STAGES - 1 steps
+// ahead are in flight in registers.
+struct LutBytes { uint32_t lo0, lo1, hi0, hi1; };   // float16 bytes of magnitudes 0..3 / 4..7
 
-template <int MT>
-__global__ __launch_bounds__(256) void k_mfma(const uint8_t* __restrict__ codes,
-                                              const uint16_t* __restrict__ x,
-                                              float* __restrict__ y, int n_rows, int k_cols,
-                                              int m_rows, Lut16 lut, float scale) {
-  __shared__ __attribute__((aligned(16))) uint32_t s_lut[kLutWords];
-  __shared__ __attribute__((aligned(16))) uint16_t s_x[2][MT * 32][kXPad];
+constexpr int kM2Step = 256;
+constexpr int kM2Pad = kM2Step + 8;   // halves per staged activation row
 
-  fill_pair_lut<256>(s_lut, lut);
+__device__ __forceinline__ void dequant_dword(uint32_t w, const LutBytes& t, uint32_t (&o)[4]) {
+  const uint32_t me = w & 0x07070707u;            // magnitudes of k0 k2 k4 k6
+  const uint32_t mo = (w >> 4) & 0x07070707u;     // magnitudes of k1 k3 k5 k7
+  const uint32_t le = __builtin_amdgcn_perm(t.lo1, t.lo0, me);
+  const uint32_t lo = __builtin_amdgcn_perm(t.lo1, t.lo0, mo);
+  const uint32_t he = __builtin_amdgcn_perm(t.hi1, t.hi0, me) | ((w << 4) & 0x80808080u);
+  const uint32_t ho = __builtin_amdgcn_perm(t.hi1, t.hi0, mo) | (w & 0x80808080u);
+  o[0] = __builtin_amdgcn_perm(he, le, 0x05010400u);   // (k0, k2)
+  o[1] = __builtin_amdgcn_perm(he, le, 0x07030602u);   // (k4, k6)
+  o[2] = __builtin_amdgcn_perm(ho, lo, 0x05010400u);   // (k1, k3)
+  o[3] = __builtin_amdgcn_perm(ho, lo, 0x07030602u);   // (k5, k7)
+}
+
+// Eight activations x0..x7 (four float16 pairs) reordered to x0 x2 x4 x6 x1 x3 x5 x7.
+__device__ __forceinline__ u32x4 permute_x8(const u32x4 v) {
+  u32x4 o;
+  o.x = __builtin_amdgcn_perm(v.y, v.x, 0x05040100u);
+  o.y = __builtin_amdgcn_perm(v.w, v.z, 0x05040100u);
+  o.z = __builtin_amdgcn_perm(v.y, v.x, 0x07060302u);
+  o.w = __builtin_amdgcn_perm(v.w, v.z, 0x07060302u);
+  return o;
+}
+
+// LDS position (in 16-byte units) of unit u of staged activation row r: rows 8..15 of every
+// 16-row tile are rotated by 8 units, so that the 32 lanes served together by a 128-bit LDS
+// read (rows 0..15 x two k-groups 8 units apart) hit 32 distinct bank groups (measured
+// conflict-free with SQ_LDS_BANK_CONFLICT; the unrotated padded layout is not).
+__device__ __forceinline__ int x_unit(int r, int u) { return (u + 8 * ((r >> 3) & 1)) & 31; }
+
+// PAIRS selects the dequantization: true = the LDS pair table (one v_perm_b32 address and one
+// ds_read_b32 per two weights; activations in natural order), false = the register tables
+// above (no LDS table, 18 VALU instructions per eight weights; activations permuted).
+template <int MT, int STAGES, bool PAIRS>
+__global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes,
+                                               const uint16_t* __restrict__ x,
+                                               float* __restrict__ y, int n_rows, int k_cols,
+                                               int m_rows, LutBytes tb, Lut16 lut, float scale) {
+  static_assert(STAGES % 2 == 0, "the loop is unrolled by STAGES and alternates two tiles");
+  __shared__ __attribute__((aligned(16))) uint16_t s_x[2][MT * 16][kM2Pad];
+  __shared__ __attribute__((aligned(16))) uint32_t s_lut[PAIRS ? kLutWords : 4];
+  if (PAIRS) fill_pair_lut<512>(s_lut, lut);
+  const uint32_t laneoff = (uint32_t)(threadIdx.x & 63) << 2;
 
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = t >> 6;
-  const int j = lane & 31;
-  const int h = lane >> 5;
-  const int n0 = blockIdx.x * 128 + wave * 32;
-  const int mb = blockIdx.y * (MT * 32);
-  const int nsteps = (k_cols + 63) >> 6;
+  const int j = lane & 15;
+  const int g = lane >> 4;
+  const int n0 = blockIdx.x * 128 + wave * 16;
+  const int mb = blockIdx.y * (MT * 16);
+  const int nsteps = (k_cols + kM2Step - 1) / kM2Step;
   const int64_t row_bytes = (int64_t)(k_cols >> 1);
-  const uint32_t laneoff = (uint32_t)lane << 2;
   const int row = n0 + j;
   const GlobalU8 crow = (GlobalU8)codes + (int64_t)(row < n_rows ? row : n_rows - 1) * row_bytes;
 
-  // Activation tile of one step: MT * 32 rows x 64 halves, 16 bytes per thread and pass.
-  // Loads are clamped in bounds; rows past m_rows and columns past k_cols are zeroed when the
-  // tile is written to LDS.
+  // Activation tile of a step: MT*16 rows x 256 halves = MT*512 vectors of 16 bytes, MT per
+  // thread. Loads are clamped in bounds; entries past m_rows / k_cols are zeroed when written.
   auto load_x = [&](int step, u32x4 (&v)[MT]) {
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const int idx = t + 256 * i;
-      const int m = mb + (idx >> 3);
-      const int kk = step * 64 + (idx & 7) * 8;
+      const int idx = t + 512 * i;
+      const int m = mb + (idx >> 5);
+      const int kk = step * kM2Step + (idx & 31) * 8;
       const int mc = m < m_rows ? m : m_rows - 1;
       const int kc = kk < k_cols ? kk : k_cols - 8;
       v[i] = *(GlobalU32x4)((const __attribute__((address_space(1))) uint16_t*)x +
                             (int64_t)mc * k_cols + kc);
     }
   };
-  auto store_x = [&](int step, int buf, const u32x4 (&v)[MT]) {
+  auto store_x = [&](int step, int slot, const u32x4 (&v)[MT]) {
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const int idx = t + 256 * i;
-      const uint32_t keep =
-          0u - (uint32_t)((mb + (idx >> 3) < m_rows) & (step * 64 + (idx & 7) * 8 < k_cols));
-      u32x4 w;
-      w.x = v[i].x & keep; w.y = v[i].y & keep; w.z = v[i].z & keep; w.w = v[i].w & keep;
-      *reinterpret_cast<u32x4*>(&s_x[buf][idx >> 3][(idx & 7) * 8]) = w;
+      const int idx = t + 512 * i;
+      const uint32_t keep = 0u - (uint32_t)((mb + (idx >> 5) < m_rows) &
+                                            (step * kM2Step + (idx & 31) * 8 < k_cols));
+      u32x4 w = PAIRS ? v[i] : permute_x8(v[i]);
+      w.x &= keep; w.y &= keep; w.z &= keep; w.w &= keep;
+      const int r = idx >> 5;
+      *reinterpret_cast<u32x4*>(&s_x[slot][r][x_unit(r, idx & 31) * 8]) = w;
     }
   };
-  // Codes of one step: bytes [32 step + 16 h, +16) of this lane's row (clamped into the row;
-  // a clamped chunk only ever meets zero activations).
-  auto load_codes = [&](int step) {
-    int off = step * 32 + 16 * h;
-    off = (int64_t)off + 16 <= row_bytes ? off : (int)row_bytes - 16;
-    return __builtin_nontemporal_load((GlobalU32x4)(crow + off));
-  };
-  auto mma_step = [&](int buf, const u32x4 q, float16v (&acc)[MT]) {
-    const uint32_t dw[4] = {q.x, q.y, q.z, q.w};
+  // Codes of a step: 32 bytes at [128 step + 32 g, +32) of this lane's row (clamped into the
+  // row; a clamped chunk only meets zero activations).
+  auto load_codes = [&](int step, u32x4 (&q)[2]) {
 #pragma unroll
-    for (int d = 0; d < 4; ++d) {
-      half8v b;
-      {
-        const half2v p0 = as_half2(pair_lookup(s_lut, dw[d], laneoff, 0));
-        const half2v p1 = as_half2(pair_lookup(s_lut, dw[d], laneoff, 1));
-        const half2v p2 = as_half2(pair_lookup(s_lut, dw[d], laneoff, 2));
-        const half2v p3 = as_half2(pair_lookup(s_lut, dw[d], laneoff, 3));
-        b[0] = p0[0]; b[1] = p0[1]; b[2] = p1[0]; b[3] = p1[1];
-        b[4] = p2[0]; b[5] = p2[1]; b[6] = p3[0]; b[7] = p3[1];
-      }
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const half8v a = *reinterpret_cast<const half8v*>(&s_x[buf][mt * 32 + j][32 * h + 8 * d]);
-        acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc[mt], 0, 0, 0);
-      }
+    for (int c = 0; c < 2; ++c) {
+      int64_t off = (int64_t)step * 128 + 32 * g + 16 * c;
+      off = off + 16 <= row_bytes ? off : row_bytes - 16;
+      q[c] = __builtin_nontemporal_load((GlobalU32x4)(crow + off));
     }
   };
 
-  float16v acc[MT];
+  float4v acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
+    for (int r = 0; r < 4; ++r) acc[mt][r] = 0.0f;
 
-  // Software pipeline, unrolled by two (buffers a / b): while step s is multiplied out of LDS
-  // buffer s & 1, the activations of step s + 1 sit in registers (written to the other buffer
-  // after the step) and the codes of step s + 1 and the loads of step s + 2 are in flight.
-  // An odd step count runs one extra step past k_cols, whose activations are all zero.
-  const int last = nsteps - 1;
-  const int nsteps2 = (nsteps + 1) & ~1;
-  u32x4 xa[MT], xb[MT];
-  load_x(0, xa);
-  u32x4 qa = load_codes(0);
-  load_x(1 < last ? 1 : last, xb);
-  u32x4 qb = load_codes(1 < last ? 1 : last);
-  store_x(0, 0, xa);
+  // Pipeline. Activation tile t lives in LDS slot t & 1; it is loaded into register set
+  // xr[t & 1] at step t - 2 and written to LDS at the end of step t - 1, so waiting for it never
+  // waits for code loads issued after it (vector loads complete in issue order). Codes of step
+  // t are loaded at step t - (STAGES - 1) into q[t % STAGES].
+  u32x4 q[STAGES][2];
+  u32x4 xr[2][MT];
+  auto clampstep = [&](int t2) { return t2 < nsteps ? t2 : nsteps - 1; };
+  load_x(0, xr[0]);
+  load_x(clampstep(1), xr[1]);
+#pragma unroll
+  for (int t2 = 0; t2 < STAGES - 1; ++t2) load_codes(clampstep(t2), q[t2]);
+  store_x(0, 0, xr[0]);
   __syncthreads();
 
-  for (int step = 0; step < nsteps2; step += 2) {
-    mma_step(0, qa, acc);
-    store_x(step + 1, 1, xb);
-    load_x(step + 2 < last ? step + 2 : last, xa);
-    qa = load_codes(step + 2 < last ? step + 2 : last);
-    __syncthreads();
-    mma_step(1, qb, acc);
-    store_x(step + 2, 0, xa);
-    load_x(step + 3 < last ? step + 3 : last, xb);
-    qb = load_codes(step + 3 < last ? step + 3 : last);
-    __syncthreads();
+  // Steady state, unrolled by STAGES (even) so every buffer index is static.
+  for (int s0 = 0; s0 < nsteps; s0 += STAGES) {
+#pragma unroll
+    for (int u = 0; u < STAGES; ++u) {
+      const int step = s0 + u;
+      if (step >= nsteps) break;
+      load_x(clampstep(step + 2), xr[u & 1]);
+      load_codes(clampstep(step + STAGES - 1), q[(u + STAGES - 1) % STAGES]);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const uint32_t dws[4] = {q[u][c].x, q[u][c].y, q[u][c].z, q[u][c].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int d = 4 * c + e;
+          uint32_t bw[4];
+          if (PAIRS) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) bw[i] = pair_lookup(s_lut, dws[e], laneoff, i);
+          } else {
+            dequant_dword(dws[e], tb, bw);
+          }
+          const half8v b = __builtin_bit_cast(half8v, u32x4{bw[0], bw[1], bw[2], bw[3]});
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const half8v a = *reinterpret_cast<const half8v*>(
+                &s_x[u & 1][mt * 16 + j][x_unit(j, 8 * g + d) * 8]);
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, acc[mt], 0, 0, 0);
+          }
+        }
+      }
+      store_x(step + 1, (u + 1) & 1, xr[(u + 1) & 1]);
+      __syncthreads();
+    }
   }
 
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = mb + mt * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+    for (int r = 0; r < 4; ++r) {
+      const int m = mb + mt * 16 + 4 * g + r;
       if (m < m_rows && row < n_rows) y[(int64_t)m * n_rows + row] = acc[mt][r] * scale;
     }
 }
@@ -641,20 +718,53 @@ int32_t validate_job(const LinearJob& j, int64_t m, int64_t k) {
   return LOGBQ_OK;
 }
 
+// float16 byte tables for the register dequant; false unless the codebook is sign-symmetric
+// with a non-negative positive half (every fitted codebook is).
+bool make_lut_bytes(const float* cb, LutBytes* tb, float* scale) {
+  for (int k = 0; k < 8; ++k)
+    if (!(cb[k] >= 0.0f)) return false;
+  if (cb[8] != 0.0f) return false;
+  for (int k = 1; k < 8; ++k)
+    if (cb[8 + k] != -cb[k]) return false;
+  Lut16 lut;
+  make_lut16(cb, &lut, scale);
+  uint32_t lo[2] = {0, 0}, hi[2] = {0, 0};
+  for (int k = 0; k < 8; ++k) {
+    const uint32_t h16 = (lut.h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
+    lo[k >> 2] |= (h16 & 0xFFu) << (8 * (k & 3));
+    hi[k >> 2] |= (h16 >> 8) << (8 * (k & 3));
+  }
+  tb->lo0 = lo[0]; tb->lo1 = lo[1]; tb->hi0 = hi[0]; tb->hi1 = hi[1];
+  return true;
+}
+
 int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st) {
+  const int N = (int)j.n;
+  LutBytes tb = {0, 0, 0, 0};
   Lut16 lut;
   float scale;
+  // Register dequantization needs a sign-symmetric codebook (every fitted one is); any other
+  // codebook uses the LDS pair table with at most 4 batch tiles per workgroup column.
+  const bool symmetric = make_lut_bytes(j.codebook, &tb, &scale);
   make_lut16(j.codebook, &lut, &scale);
-  const int N = (int)j.n;
-  const int mt = M >= 97 ? 4 : (M >= 65 ? 3 : (M >= 33 ? 2 : 1));
-  const int mblock = mt * 32;
-  dim3 grid((unsigned)((N + 127) / 128), (unsigned)((M + mblock - 1) / mblock));
-  switch (mt) {
-    case 1: hipLaunchKernelGGL(k_mfma<1>, grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, lut, scale); break;
-    case 2: hipLaunchKernelGGL(k_mfma<2>, grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, lut, scale); break;
-    case 3: hipLaunchKernelGGL(k_mfma<3>, grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, lut, scale); break;
-    default: hipLaunchKernelGGL(k_mfma<4>, grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, lut, scale); break;
+  // Batch tiles of 16 rows: up to 8 per workgroup column (128 rows). Up to 4 tiles use the
+  // LDS pair table; more tiles leave LDS to the activation ring and dequantize in registers.
+  int mt16 = (M + 15) / 16;
+  const int cap = symmetric ? 8 : 4;
+  if (mt16 > cap) mt16 = cap;
+  dim3 grid((unsigned)((N + 127) / 128), (unsigned)((M + 16 * mt16 - 1) / (16 * mt16)));
+#define LOGBQ_M2(MT, ST, PR) hipLaunchKernelGGL((k_mfma2<MT, ST, PR>), grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
+  switch (mt16) {
+    case 1: LOGBQ_M2(1, 4, true); break;
+    case 2: LOGBQ_M2(2, 4, true); break;
+    case 3: LOGBQ_M2(3, 4, true); break;
+    case 4: LOGBQ_M2(4, 4, true); break;
+    case 5: LOGBQ_M2(5, 4, false); break;
+    case 6: LOGBQ_M2(6, 4, false); break;
+    case 7: LOGBQ_M2(7, 4, false); break;
+    default: LOGBQ_M2(8, 4, false); break;
   }
+#undef LOGBQ_M2
   return launch_status();
 }
 
@@ -680,8 +790,17 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
     return LOGBQ_OK;
   }
   const int M = (int)m, K = (int)k;
+  // Path choice (measured on MI355X): the GEMV for m <= 4; for 5 <= m <= 8 the GEMV only while
+  // every matrix has fewer than 8192 rows (the MFMA kernel needs >= 64 workgroups of 128 rows
+  // to fill the chip); the MFMA kernel otherwise.
+  bool gemv = M <= 4;
+  if (M > 4 && M <= 8) {
+    gemv = true;
+    for (int a = 0; a < nlive; ++a)
+      if (jobs[live[a]].n >= 8192) gemv = false;
+  }
   int wk = 0, cpl = 0;
-  if (gemv_config(M, K, &wk, &cpl)) {
+  if (gemv && gemv_config(M, K, &wk, &cpl)) {
     const int groups = 8 / wk;
     GemvSegs segs;
     std::memset(&segs, 0, sizeof(segs));
@@ -703,7 +822,7 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
       make_lut16(j.codebook, &sg.lut, &sg.scale);
       begin += (int)share;
     }
-    const int stage_x = ((int64_t)M * K * 2 <= (int64_t)kLutWords * 4) ? 1 : 0;
+    const int stage_x = ((int64_t)M * K * 2 <= (int64_t)kStageXBytes) ? 1 : 0;
     if (!dispatch_gemv(M, cpl, begin, st, x, K, wk, stage_x, segs)) return LOGBQ_ERR_UNSUPPORTED;
     return launch_status();
   }

@@ -268,6 +268,24 @@ def test_linear_deterministic_and_empty():
     assert y.shape == (0, 5)
 
 
+def test_linear_arbitrary_codebook():
+    """Any 16 finite floats work as a codebook (the table-lookup kernels); a fitted codebook is
+    sign-symmetric and takes the register-dequant MFMA path, any other takes the pair table."""
+    rng = np.random.default_rng(12)
+    n, k = 300, 1024
+    codes_np = rng.integers(0, 16, size=(n, k), dtype=np.uint8)
+    codes = torch.from_numpy(O.pack(codes_np)).to(DEV)
+    for trial in range(2):
+        cb = rng.standard_normal(16).astype(np.float32) * np.float32(10.0 ** (3 * trial - 2))
+        wh = O.dequantize(codes_np, cb)
+        for m in (1, 5, 16, 33, 128):
+            _say(f"arbitrary codebook trial {trial} m={m}")
+            x = inputs.activations(m, k, seed=[8, 9, trial, m])
+            y = L.linear(torch.from_numpy(x).to(DEV), codes, cb)
+            torch.cuda.synchronize()
+            assert rel_err(y.cpu().numpy(), x, wh) <= TOL
+
+
 def test_linear_multi_matches_single_launches():
     """Grouped launch of linears sharing x: every output equals the single-linear call bit for
     bit, and the oracle within tolerance (qkv-like and gate/up-like groups, ragged sizes)."""
