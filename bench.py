@@ -274,6 +274,30 @@ def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):
     return {"bytes_per_pass": bytes_pass, "setup_s": setup_s, **out}
 
 
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "traffic_k_gemv_layer_8192x28672_m1.md")
+
+
+def profiled_traffic():
+    """HBM bytes per launch of the M = 1 layer GEMV from the committed rocprofv3 --pmc summary,
+    or None when there is none or the kernel source changed since it was taken."""
+    try:
+        from paper_2607_01127_amd.prof_summary import source_hash
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    fields = {}
+    for line in text.splitlines():
+        if line.startswith("- ") and ":" in line:
+            key, val = line[2:].split(":", 1)
+            fields[key.strip()] = val.strip()
+    if fields.get("kernel_source_sha256_16") != source_hash():
+        return None
+    try:
+        return float(fields["traffic_bytes"])
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(L_unused, inputs, target_s=12.0):
     """The oracle (unpack + dequantize + float64 matmul) on a row sample of the layer."""
     from oracle import logbq_oracle as O
@@ -317,6 +341,9 @@ def main():
     ap.add_argument("--rows", default="layer,small,decode1b,decode8b",
                     help="comma list of extra rows: layer (M sweep + encode), small, decode1b, decode8b")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 256 MiB device-to-device copy (calibrates the HBM byte "
+                         "counters of rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -324,6 +351,14 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_calibration:
+        src = torch.empty(1 << 28, dtype=torch.uint8, device="cuda:0").fill_(3)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": src.numel(), "copies": 5}))
+        return
     from paper_2607_01127_amd import inputs
     from paper_2607_01127_amd import logbq as L
     L.lib()
@@ -374,8 +409,9 @@ def main():
                    "host_fit_s": info["fit_s"]},
         "roofline": {"bound": "hbm", "achieved": round(algo / t_ms / 1e6, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(algo / t_ms / 1e6 / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "k_gemv<1,4>", "algo_bytes_per_launch": algo,
+                     "frac": round(algo / t_ms / 1e6 / HBM_PEAK_GBS, 4),
+                     "traffic": profiled_traffic(),
+                     "kernel": "k_gemv<1, 4, false>", "algo_bytes_per_launch": algo,
                      "avg_launch_us": t_ms * 1e3},
         "cpu_baseline": cpu,
         "rows": rows,

@@ -1,0 +1,80 @@
+"""Summaries of rocprofv3 output for the profiles/ folder.
+
+kernel-stats: python -m paper_2607_01127_amd.prof_summary stats STATS_CSV CMD > profiles/X.md
+traffic:      python -m paper_2607_01127_amd.prof_summary traffic KERNEL_SUBSTR FETCH_CSV WRITE_CSV \
+                  COPY_FETCH_CSV COPY_WRITE_CSV COPY_BYTES CMD > profiles/X.md
+
+The traffic summary scales the per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the kernel by
+copy_bytes / (what the same counter reads for a plain device copy of copy_bytes bytes), and
+records the sha256 of the kernel source so that bench.py reports the figure only while the
+kernel is unchanged.
+"""
+import csv
+import hashlib
+import os
+import statistics
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCE = os.path.join(HERE, "csrc", "logbq_kernels.hip")
+
+
+def source_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def _short(name: str) -> str:
+    name = name.replace("void ", "").replace("(anonymous namespace)::", "")
+    return name.split("(")[0][:60]
+
+
+def stats(path, cmd):
+    rows = list(csv.DictReader(open(path)))
+    print("# rocprofv3 kernel statistics\n")
+    print(f"Command: `{cmd}`\n")
+    print("| kernel | calls | average (us) | min (us) | max (us) | total % |")
+    print("|---|---|---|---|---|---|")
+    for r in rows:
+        name = _short(r["Name"])
+        if "at::native" in r["Name"] or "rocclr" in r["Name"]:
+            continue
+        avg = float(r["AverageNs"]) / 1e3
+        print(f"| `{name}` | {r['Calls']} | {avg:.2f} | {float(r['MinNs'])/1e3:.2f} | "
+              f"{float(r['MaxNs'])/1e3:.2f} | {float(r['Percentage']):.1f} |")
+
+
+def _counter(path, substr, counter):
+    vals = []
+    for r in csv.DictReader(open(path)):
+        if substr in r["Kernel_Name"] and r["Counter_Name"] == counter:
+            vals.append(float(r["Counter_Value"]))
+    return vals
+
+
+def traffic(substr, fetch, write, cfetch, cwrite, copy_bytes, cmd):
+    f = _counter(fetch, substr, "FETCH_SIZE")
+    w = _counter(write, substr, "WRITE_SIZE")
+    cf = _counter(cfetch, "copy", "FETCH_SIZE") or _counter(cfetch, "Copy", "FETCH_SIZE")
+    cw = _counter(cwrite, "copy", "WRITE_SIZE") or _counter(cwrite, "Copy", "WRITE_SIZE")
+    copy_bytes = float(copy_bytes)
+    kf = copy_bytes / (statistics.median(cf) * 1024.0)
+    kw = copy_bytes / (statistics.median(cw) * 1024.0)
+    fb = statistics.median(f) * 1024.0 * kf
+    wb = statistics.median(w) * 1024.0 * kw
+    print("# HBM traffic per launch (rocprofv3 --pmc)\n")
+    print(f"Command: `{cmd}`\n")
+    print(f"kernel: `{substr}`, dispatches: {len(f)}\n")
+    print(f"- FETCH_SIZE median {statistics.median(f):.1f} KiB, copy calibration factor {kf:.4f}")
+    print(f"- WRITE_SIZE median {statistics.median(w):.1f} KiB, copy calibration factor {kw:.4f}")
+    print(f"- fetch_bytes: {fb:.0f}")
+    print(f"- write_bytes: {wb:.0f}")
+    print(f"- traffic_bytes: {fb + wb:.0f}")
+    print(f"- kernel_source_sha256_16: {source_hash()}")
+
+
+if __name__ == "__main__":
+    if sys.argv[1] == "stats":
+        stats(sys.argv[2], sys.argv[3])
+    elif sys.argv[1] == "traffic":
+        traffic(*sys.argv[2:9])
