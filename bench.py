@@ -83,7 +83,6 @@ def time_region(torch, stream, fn, steps, warmup):
     """Events around `steps` calls of fn on `stream`; returns ms per call."""
     for i in range(warmup):
         fn(i)
-    torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record(stream)
@@ -107,15 +106,34 @@ def _capture(torch, L, launches, count, offset=0):
     return graph
 
 
+WARM_CHUNK = 1000   # launches per captured warmup graph
+
+
 def time_launches(torch, L, stream, launches, steps, warmup):
     """Time exactly `steps` logbq_linear launches back to back after `warmup` untimed ones.
-    `launches` is a list of (x, codes, cb, y); launch i uses entry i % len(launches). Each
-    sequence is captured in one HIP graph so that host launch cost cannot starve the GPU; the
-    timed graph is replayed once between two events. Returns ms per launch."""
-    if warmup > 0:
-        _capture(torch, L, launches, warmup).replay()
+    `launches` is a list of (x, codes, cb, y); launch i uses entry i % len(launches). The
+    launches are captured in HIP graphs so that host launch cost cannot starve the GPU. All
+    graphs are captured first; the warmup graphs are then replayed and the timed graph follows
+    them on the same stream with no host synchronisation in between, so the timed launches run
+    on a GPU that has been busy for the whole warmup (its clocks have ramped up) instead of
+    after an idle gap. Returns ms per launch."""
+    full, rest = divmod(warmup, WARM_CHUNK)
+    warm = _capture(torch, L, launches, WARM_CHUNK) if full else None
+    warm_rest = _capture(torch, L, launches, rest) if rest else None
     timed = _capture(torch, L, launches, steps, offset=warmup)
-    return time_region(torch, stream, lambda i: timed.replay(), 1, 0) / steps
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        for _ in range(full):
+            warm.replay()
+        if warm_rest is not None:
+            warm_rest.replay()
+        e0.record(stream)
+        timed.replay()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
 
 
 def make_tensor(torch, L, inputs, lin, wl, seed, dev):
@@ -152,7 +170,7 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=Tr
 
         def enc(i):
             L.encode(wd, p, out=enc_out, stream=stream)
-        enc_ms = time_region(torch, stream, enc, max(5, steps // 20), 2)
+        enc_ms = time_region(torch, stream, enc, max(5, steps // 20), 100)
         assert torch.equal(enc_out, codes)
         enc_bytes = n * k * 4 + packed
         results["encode_8192x28672"] = {"ms": enc_ms, "GB_s": enc_bytes / enc_ms / 1e6,
@@ -164,7 +182,7 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=Tr
         launches = [(x, c, cb, torch.empty((m, n), dtype=torch.float32, device=dev))
                     for c in code_list]
         timed = steps if m == ms[0] else max(64, steps // 4)
-        t = time_launches(torch, L, stream, launches, timed, warmup)
+        t = time_launches(torch, L, stream, launches, timed, warmup if m == ms[0] else warmup // 4)
         log(f"layer m={m}: {t * 1e3:.2f} us per launch")
         algo = packed + 2 * m * k + 4 * m * n + 64
         flops = 2.0 * m * n * k
@@ -172,7 +190,8 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=Tr
             "ms": t, "us": t * 1e3, "launches_timed": timed, "weight_GB_s": packed / t / 1e6,
             "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
             "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
-            "algo_bytes": algo, "path": "gemv" if m <= 8 else "mfma"}
+            "algo_bytes": algo,
+            "path": "gemv" if m <= 4 or (m <= 8 and n < 8192) else "mfma"}
     return results, {"n": n, "k": k, "packed": packed, "copies": copies, "fit_s": fit_s,
                      "params": {"base": p.base, "shift": p.shift, "wmin": p.wmin,
                                 "wmax": p.wmax}}, codes, cb
@@ -335,8 +354,9 @@ def cpu_baseline(L_unused, inputs, target_s=12.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=500)
-    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=10000,
+                    help="untimed launches before the timed ones (about 0.2 s of GPU work at M = 1)")
     ap.add_argument("--quick", action="store_true", help="main layer only, no extra rows")
     ap.add_argument("--rows", default="layer,small,decode1b,decode8b",
                     help="comma list of extra rows: layer (M sweep + encode), small, decode1b, decode8b")
@@ -380,16 +400,16 @@ def main():
     if "small" in want:
         for name in ("up_2048x8192_outliers", "linear_2048x2048"):
             log(name)
-            rows[name + "_m1"] = bench_small(torch, L, inputs, dev, stream, name, 2000, 100)
+            rows[name + "_m1"] = bench_small(torch, L, inputs, dev, stream, name, 2000, 5000)
     del codes
     torch.cuda.empty_cache()
     if "decode1b" in want:
         rows["decode_1b_16x7"] = bench_decode(torch, L, inputs, dev, stream, "decode_1b_16x7",
-                                              [1], 200, 20)
+                                              [1], 200, 200)
         torch.cuda.empty_cache()
     if "decode8b" in want:
         rows["decode_8b_32x7"] = bench_decode(torch, L, inputs, dev, stream, "decode_8b_32x7",
-                                              [1, 4], 100, 10)
+                                              [1, 4], 100, 100)
         torch.cuda.empty_cache()
 
     cpu = None
@@ -411,7 +431,7 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(algo / t_ms / 1e6 / HBM_PEAK_GBS, 4),
                      "traffic": profiled_traffic(),
-                     "kernel": "k_gemv<1, 4, false>", "algo_bytes_per_launch": algo,
+                     "kernel": "k_gemv<1, 4, false, 2>", "algo_bytes_per_launch": algo,
                      "avg_launch_us": t_ms * 1e3},
         "cpu_baseline": cpu,
         "rows": rows,

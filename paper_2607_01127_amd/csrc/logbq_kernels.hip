@@ -38,6 +38,11 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef const __attribute__((address_space(1))) uint8_t* GlobalU8;
 typedef const __attribute__((address_space(1))) u32x4* GlobalU32x4;
 
+// Word 3 of a gfx9 buffer resource descriptor for untyped (raw) 32-bit access.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+// Cache policy bits of a buffer load: non-temporal (streamed once).
+constexpr int kCachePolicyNT = 2;
+
 struct Thresholds { float t[7]; };
 struct Codebook32 { float v[16]; };
 struct Lut16 { uint32_t h[8]; };   // h[i] = f16(lut[2i]) | f16(lut[2i+1]) << 16
@@ -189,13 +194,18 @@ __device__ __forceinline__ float wave_sum(float v) {
 // `l` of wavefront `kw` in a group handles chunks c = s * 64 * WK + kw * 64 + l for s < CPL; its
 // activations for those chunks (M rows x 32 values each) stay in registers for the whole kernel.
 //
+// Codes are read with buffer loads through a resource descriptor built per row in scalar
+// registers (base = the row, size = its byte length); a row index past the end of the segment
+// gets size 0, so its loads return zeros without touching memory. Chunk indices past the end of
+// a row are clamped into it and meet zero activations.
+//
 // Start-up: x (when M * K * 2 <= 32 KiB) is requested first and staged once per workgroup
 // through LDS into registers; the first row of codes is requested next; the pair table is
-// written while both are in flight. The row loop is unrolled by two over
-// two code buffers: the next row's loads are in flight while the current row is looked up,
-// multiplied and reduced. Every load is issued unconditionally (row and chunk indices are
-// clamped into the matrix; a clamped chunk meets zero activations), so the compiler waits for
-// exactly the buffer it is about to use.
+// written while both are in flight. The row loop keeps NBUF code buffers: while row it is
+// looked up, multiplied and reduced, rows it + 1 .. it + NBUF - 1 are in flight. Every load in
+// the loop is issued unconditionally, so the compiler waits for exactly the buffer it is about
+// to use. NBUF is 3 when a row slice is at most two chunks per lane (and m <= 2) and 2
+// otherwise: measured on MI355X, about 4 to 8 KiB of codes in flight per wavefront streams best.
 constexpr int kMaxSegs = 4;
 constexpr int kStageXBytes = 32768;   // activations staged through LDS when M * K * 2 fits
 // Staged activations keep every 64-byte chunk (the 32 values one lane multiplies with one
@@ -243,7 +253,7 @@ __device__ __forceinline__ void gemv_row(const u32x4 (&q)[CPL], const uint32_t (
   for (int m = 0; m < M; ++m) acc[m] += acc2[m];
 }
 
-template <int M, int CPL, bool SPLITK>
+template <int M, int CPL, bool SPLITK, int NBUF>
 __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, int k_cols, int wk_arg,
                                               int stage_x, GemvSegs segs) {
   const int wk = SPLITK ? wk_arg : 1;
@@ -257,7 +267,7 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
 #pragma unroll
   for (int i = 1; i < kMaxSegs; ++i)
     if (i < segs.count && bid >= segs.s[i].wg_begin) si = i;
-  const GlobalU8 codes = (GlobalU8)segs.s[si].codes;
+  const uint8_t* codes = segs.s[si].codes;
   float* __restrict__ y = segs.s[si].y;
   const int n_rows = segs.s[si].n_rows;
   const int iters = segs.s[si].iters;
@@ -266,7 +276,7 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
   const int next_begin = (si + 1 < segs.count) ? segs.s[si + 1].wg_begin : (int)gridDim.x;
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int kw = wave % wk;
   const int grp = wave / wk;
   const int groups = 8 / wk;
@@ -286,15 +296,17 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
   }
 
   auto load_row = [&](int it, u32x4 (&q)[CPL]) {
-    int r = gid + it * total_groups;
-    r = r < n_rows ? r : n_rows - 1;
-    const GlobalU8 base = codes + (int64_t)r * row_bytes;
+    const int r = gid + it * total_groups;
+    const bool live = r < n_rows;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(codes + (live ? (int64_t)r * row_bytes : 0)), (short)0,
+        live ? (int)row_bytes : 0, kBufferRsrcWord3);
 #pragma unroll
     for (int s = 0; s < CPL; ++s)
-      q[s] = __builtin_nontemporal_load((GlobalU32x4)(base + coff[s]));
+      q[s] = __builtin_amdgcn_raw_buffer_load_b128(rs, coff[s], 0, kCachePolicyNT);
   };
 
-  u32x4 qa[CPL], qb[CPL];
+  u32x4 q[NBUF][CPL];
 
   // Start-up, ordered so that the memory system is busy from the first cycle: the staged
   // activations are requested first (they return first), then the first row of codes; the
@@ -309,7 +321,7 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
       xv[v] = *reinterpret_cast<const u32x4*>(x + 8 * (int64_t)(i < nvec ? i : 0));
     }
   }
-  load_row(0, qa);
+  load_row(0, q[0]);
   fill_pair_lut<512>(s_lut, segs.s[si].lut);
 
   uint32_t xr[M][CPL][16];
@@ -326,12 +338,12 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
 #pragma unroll
       for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int vi = ((m * k_cols + c * 32) >> 3) + q;    // 16-byte vector index
+        for (int qi = 0; qi < 4; ++qi) {
+          const int vi = ((m * k_cols + c * 32) >> 3) + qi;    // 16-byte vector index
           u32x4 v = *reinterpret_cast<const u32x4*>(s_x + 4 * (vi + (vi >> 2)));
           if (!cval[s]) v = 0;
-          xr[m][s][4 * q] = v.x; xr[m][s][4 * q + 1] = v.y;
-          xr[m][s][4 * q + 2] = v.z; xr[m][s][4 * q + 3] = v.w;
+          xr[m][s][4 * qi] = v.x; xr[m][s][4 * qi + 1] = v.y;
+          xr[m][s][4 * qi + 2] = v.z; xr[m][s][4 * qi + 3] = v.w;
         }
     }
   } else {
@@ -341,11 +353,11 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
 #pragma unroll
       for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int qi = 0; qi < 4; ++qi) {
           u32x4 v = 0;
-          if (cval[s]) v = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k_cols + (int64_t)c * 32 + 8 * q);
-          xr[m][s][4 * q] = v.x; xr[m][s][4 * q + 1] = v.y;
-          xr[m][s][4 * q + 2] = v.z; xr[m][s][4 * q + 3] = v.w;
+          if (cval[s]) v = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k_cols + (int64_t)c * 32 + 8 * qi);
+          xr[m][s][4 * qi] = v.x; xr[m][s][4 * qi + 1] = v.y;
+          xr[m][s][4 * qi + 2] = v.z; xr[m][s][4 * qi + 3] = v.w;
         }
     }
   }
@@ -377,25 +389,25 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
   float acc[M];
   __syncthreads();  // pair table ready (and, when staged, x read out of LDS)
 
-  // Main loop: rows it and it + 1 are computed while rows it + 1 and it + 2 are in flight.
+#pragma unroll
+  for (int b = 1; b + 1 < NBUF; ++b) load_row(b, q[b]);
+
+  // Invariant at the top of the loop: q[b] holds (or awaits) row it + b for b < NBUF - 1.
   int it = 0;
-  for (; it + 2 < iters; it += 2) {
-    load_row(it + 1, qb);
-    gemv_row<M, CPL>(qa, xr, s_lut, laneoff, acc);
-    finish_row(it, acc);
-    load_row(it + 2, qa);
-    gemv_row<M, CPL>(qb, xr, s_lut, laneoff, acc);
-    finish_row(it + 1, acc);
+  for (; it + NBUF <= iters; it += NBUF) {
+#pragma unroll
+    for (int b = 0; b < NBUF; ++b) {
+      load_row(it + b + NBUF - 1, q[(b + NBUF - 1) % NBUF]);
+      gemv_row<M, CPL>(q[b], xr, s_lut, laneoff, acc);
+      finish_row(it + b, acc);
+    }
   }
-  if (it + 2 == iters) {
-    load_row(it + 1, qb);
-    gemv_row<M, CPL>(qa, xr, s_lut, laneoff, acc);
-    finish_row(it, acc);
-    gemv_row<M, CPL>(qb, xr, s_lut, laneoff, acc);
-    finish_row(it + 1, acc);
-  } else if (it + 1 == iters) {
-    gemv_row<M, CPL>(qa, xr, s_lut, laneoff, acc);
-    finish_row(it, acc);
+#pragma unroll
+  for (int b = 0; b + 1 < NBUF; ++b) {
+    if (it + b < iters) {
+      gemv_row<M, CPL>(q[b], xr, s_lut, laneoff, acc);
+      finish_row(it + b, acc);
+    }
   }
 }
 
@@ -657,12 +669,13 @@ int64_t grid_for(int64_t items, int64_t per_block, int64_t cap) {
 template <int M, int CPL>
 void launch_gemv(int grid, hipStream_t st, const uint16_t* x, int k, int wk, int stage_x,
                  const GemvSegs& segs) {
+  constexpr int NBUF = (CPL <= 2 && M <= 2) ? 3 : 2;
   if (wk == 1)
-    hipLaunchKernelGGL((k_gemv<M, CPL, false>), dim3((unsigned)grid), dim3(512), 0, st, x, k, 1,
-                       stage_x, segs);
+    hipLaunchKernelGGL((k_gemv<M, CPL, false, NBUF>), dim3((unsigned)grid), dim3(512), 0, st, x,
+                       k, 1, stage_x, segs);
   else
-    hipLaunchKernelGGL((k_gemv<M, CPL, true>), dim3((unsigned)grid), dim3(512), 0, st, x, k, wk,
-                       stage_x, segs);
+    hipLaunchKernelGGL((k_gemv<M, CPL, true, NBUF>), dim3((unsigned)grid), dim3(512), 0, st, x,
+                       k, wk, stage_x, segs);
 }
 
 bool dispatch_gemv(int m, int cpl, int grid, hipStream_t st, const uint16_t* x, int k, int wk,
@@ -687,7 +700,9 @@ bool gemv_config(int m, int k, int* wk, int* cpl) {
   const int cplmax = 8 / m;
   for (int w = 1; w <= 8; w *= 2) {
     const int per = (nchunks + 64 * w - 1) / (64 * w);
-    if (per <= cplmax && (w == 1 || nchunks >= 32 * w)) {
+    // The split-row kernels keep at most 7 chunks per lane (8 would spill registers).
+    const int cap = (w == 1 || cplmax < 7) ? cplmax : 7;
+    if (per <= cap && (w == 1 || nchunks >= 32 * w)) {
       *wk = w;
       *cpl = per < 1 ? 1 : per;
       return true;
