@@ -137,17 +137,27 @@ __device__ __forceinline__ uint32_t lut16_entry(const Lut16 lut, uint32_t c) {
 
 // Fill the LDS pair table: word (e * 64 + lane) = f16(lut[e & 15]) | f16(lut[e >> 4]) << 16,
 // i.e. the two weights of code byte e in k order (low nibble = even k). Thread t writes the
-// 16-byte vectors t, t + THREADS, ..., so each store instruction covers contiguous LDS and
-// never conflicts on a bank; vector v holds entry v / 16.
+// 16-byte vectors t + THREADS * i, so each store instruction covers contiguous LDS and never
+// conflicts on a bank; vector v holds entry v / 16. With THREADS a multiple of 256, the low
+// nibble of every entry a thread writes is the same, (t / 16) % 16, and the high nibbles are
+// t / 256 + (THREADS / 256) * i: one select chain plus one halfword pick per vector.
 template <int THREADS>
 __device__ __forceinline__ void fill_pair_lut(uint32_t* s_lut, const Lut16 lut) {
+  static_assert(THREADS % 256 == 0, "the low nibble must be fixed per thread");
   constexpr int kVecs = kLutWords / 4;
   const int t = threadIdx.x;
+  const uint32_t lo = lut16_entry(lut, ((uint32_t)t >> 4) & 15u);
 #pragma unroll
   for (int i = 0; i < kVecs / THREADS; ++i) {
-    const uint32_t e = (uint32_t)((t + THREADS * i) >> 4);
-    const uint32_t v = lut16_entry(lut, e & 15u) | (lut16_entry(lut, e >> 4) << 16);
-    const u32x4 vv = v;
+    const uint32_t hn = ((uint32_t)t >> 8) + (uint32_t)(THREADS / 256) * (uint32_t)i;
+    uint32_t hi;
+    if (THREADS == 512) {
+      // hn = (t >> 8) + 2 i: entry 2 i + (t >> 8) is a half of pair word h[i]
+      hi = (t & 256) ? (lut.h[i] >> 16) : (lut.h[i] & 0xFFFFu);
+    } else {
+      hi = lut16_entry(lut, hn);
+    }
+    const u32x4 vv = lo | (hi << 16);
     *reinterpret_cast<u32x4*>(s_lut + 4 * (t + THREADS * i)) = vv;
   }
 }
@@ -435,6 +445,7 @@ struct LutBytes { uint32_t lo0, lo1, hi0, hi1; };   // float16 bytes of magnitud
 
 constexpr int kM2Step = 256;
 constexpr int kM2Pad = kM2Step + 8;   // halves per staged activation row
+constexpr int kM2TPitch = 144;        // bytes per row of a wavefront's code transpose buffer
 
 __device__ __forceinline__ void dequant_dword(uint32_t w, const LutBytes& t, uint32_t (&o)[4]) {
   const uint32_t me = w & 0x07070707u;            // magnitudes of k0 k2 k4 k6
@@ -467,8 +478,18 @@ __device__ __forceinline__ int x_unit(int r, int u) { return (u + 8 * ((r >> 3) 
 
 // PAIRS selects the dequantization: true = the LDS pair table (one v_perm_b32 address and one
 // ds_read_b32 per two weights; activations in natural order), false = the register tables
-// above (no LDS table, 18 VALU instructions per eight weights; activations permuted).
-template <int MT, int STAGES, bool PAIRS>
+// above (no LDS table, 14 VALU instructions per eight weights; activations permuted).
+//
+// COAL selects how codes reach the lanes. false: every lane loads its own 32 bytes (two 16-byte
+// pieces 32 bytes apart per row and instruction). true: the wavefront reads its 16 rows as two
+// instructions of 8 rows x 128 contiguous bytes each, writes them to a private LDS buffer and
+// reads them back in the MFMA layout (same wavefront, so no workgroup barrier). On MI355X a
+// pure streaming read of 8 rows x 128 B per instruction runs at about 5.9 TB/s, of 16 rows x
+// 64 B at about 4.6 TB/s. With COAL the activation tile of a step is also requested together
+// with that step's codes, STAGES - 1 steps ahead: vector loads complete in issue order, so an
+// activation load issued later than a code load would wait for it. COAL is used for MT <= 2,
+// where it measured 10-20 % faster; larger MT keep the first scheme.
+template <int MT, int STAGES, bool PAIRS, bool COAL>
 __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes,
                                                const uint16_t* __restrict__ x,
                                                float* __restrict__ y, int n_rows, int k_cols,
@@ -476,6 +497,7 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
   static_assert(STAGES % 2 == 0, "the loop is unrolled by STAGES and alternates two tiles");
   __shared__ __attribute__((aligned(16))) uint16_t s_x[2][MT * 16][kM2Pad];
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[PAIRS ? kLutWords : 4];
+  __shared__ __attribute__((aligned(16))) uint8_t s_ct[COAL ? 8 * 16 * kM2TPitch : 16];
   if (PAIRS) fill_pair_lut<512>(s_lut, lut);
   const uint32_t laneoff = (uint32_t)(threadIdx.x & 63) << 2;
 
@@ -517,15 +539,43 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
       *reinterpret_cast<u32x4*>(&s_x[slot][r][x_unit(r, idx & 31) * 8]) = w;
     }
   };
-  // Codes of a step: 32 bytes at [128 step + 32 g, +32) of this lane's row (clamped into the
-  // row; a clamped chunk only meets zero activations).
+  // Codes of a step: this lane's 32 bytes at [128 step + 32 g, +32) of row n0 + j (clamped into
+  // the row; a clamped chunk only meets zero activations). Without COAL they are loaded as two
+  // 16-byte pieces per lane; with COAL the wavefront loads its rows n0 .. n0 + 15 as two
+  // instructions of 8 rows x 128 bytes (lane l: row n0 + 8 c + l / 8, bytes 16 (l % 8)), and
+  // lane_codes() redistributes them through the wavefront's LDS buffer.
   auto load_codes = [&](int step, u32x4 (&q)[2]) {
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      int64_t off = (int64_t)step * 128 + 32 * g + 16 * c;
-      off = off + 16 <= row_bytes ? off : row_bytes - 16;
-      q[c] = __builtin_nontemporal_load((GlobalU32x4)(crow + off));
+      if (COAL) {
+        int r = n0 + 8 * c + (lane >> 3);
+        r = r < n_rows ? r : n_rows - 1;
+        int64_t off = (int64_t)step * 128 + 16 * (lane & 7);
+        off = off + 16 <= row_bytes ? off : row_bytes - 16;
+        q[c] = __builtin_nontemporal_load(
+            (GlobalU32x4)((GlobalU8)codes + (int64_t)r * row_bytes + off));
+      } else {
+        int64_t off = (int64_t)step * 128 + 32 * g + 16 * c;
+        off = off + 16 <= row_bytes ? off : row_bytes - 16;
+        q[c] = __builtin_nontemporal_load((GlobalU32x4)(crow + off));
+      }
     }
+  };
+  uint8_t* s_cw = s_ct + (COAL ? wave * 16 * kM2TPitch : 0);
+  auto lane_codes = [&](const u32x4 (&q)[2], u32x4 (&o)[2]) {
+    if (!COAL) {
+      o[0] = q[0]; o[1] = q[1];
+      return;
+    }
+    // LDS operations of one wavefront complete in order, so the reads below see the writes.
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+      *reinterpret_cast<u32x4*>(s_cw + (8 * c + (lane >> 3)) * kM2TPitch + 16 * (lane & 7)) = q[c];
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+      o[c] = *reinterpret_cast<const u32x4*>(s_cw + j * kM2TPitch + 32 * g + 16 * c);
+    __builtin_amdgcn_wave_barrier();
   };
 
   float4v acc[MT];
@@ -534,17 +584,27 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[mt][r] = 0.0f;
 
-  // Pipeline. Activation tile t lives in LDS slot t & 1; it is loaded into register set
-  // xr[t & 1] at step t - 2 and written to LDS at the end of step t - 1, so waiting for it never
-  // waits for code loads issued after it (vector loads complete in issue order). Codes of step
-  // t are loaded at step t - (STAGES - 1) into q[t % STAGES].
+  // Pipeline. Activation tile t lives in LDS slot t & 1 and is written there at the end of step
+  // t - 1. Codes of step t are loaded at step t - (STAGES - 1) into q[t % STAGES]. Without COAL
+  // the tile is loaded at step t - 2 into xr[t & 1]; with COAL at step t - (STAGES - 1) into
+  // xr[t % STAGES] (XR = STAGES register sets), so waiting for it never waits for a code load
+  // issued after an older tile.
+  constexpr int XR = COAL ? STAGES : 2;
   u32x4 q[STAGES][2];
-  u32x4 xr[2][MT];
+  u32x4 xr[XR][MT];
   auto clampstep = [&](int t2) { return t2 < nsteps ? t2 : nsteps - 1; };
-  load_x(0, xr[0]);
-  load_x(clampstep(1), xr[1]);
+  if (COAL) {
 #pragma unroll
-  for (int t2 = 0; t2 < STAGES - 1; ++t2) load_codes(clampstep(t2), q[t2]);
+    for (int t2 = 0; t2 < STAGES - 1; ++t2) {
+      load_x(clampstep(t2), xr[t2 % XR]);
+      load_codes(clampstep(t2), q[t2]);
+    }
+  } else {
+    load_x(0, xr[0]);
+    load_x(clampstep(1), xr[1 % XR]);
+#pragma unroll
+    for (int t2 = 0; t2 < STAGES - 1; ++t2) load_codes(clampstep(t2), q[t2]);
+  }
   store_x(0, 0, xr[0]);
   __syncthreads();
 
@@ -554,11 +614,14 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
     for (int u = 0; u < STAGES; ++u) {
       const int step = s0 + u;
       if (step >= nsteps) break;
-      load_x(clampstep(step + 2), xr[u & 1]);
+      if (COAL) load_x(clampstep(step + STAGES - 1), xr[(u + STAGES - 1) % XR]);
+      else load_x(clampstep(step + 2), xr[u % XR]);
       load_codes(clampstep(step + STAGES - 1), q[(u + STAGES - 1) % STAGES]);
+      u32x4 qc[2];
+      lane_codes(q[u], qc);
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const uint32_t dws[4] = {q[u][c].x, q[u][c].y, q[u][c].z, q[u][c].w};
+        const uint32_t dws[4] = {qc[c].x, qc[c].y, qc[c].z, qc[c].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int d = 4 * c + e;
@@ -578,7 +641,7 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
           }
         }
       }
-      store_x(step + 1, (u + 1) & 1, xr[(u + 1) & 1]);
+      store_x(step + 1, (u + 1) & 1, xr[(u + 1) % XR]);
       __syncthreads();
     }
   }
@@ -768,7 +831,7 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
   const int cap = symmetric ? 8 : 4;
   if (mt16 > cap) mt16 = cap;
   dim3 grid((unsigned)((N + 127) / 128), (unsigned)((M + 16 * mt16 - 1) / (16 * mt16)));
-#define LOGBQ_M2(MT, ST, PR) hipLaunchKernelGGL((k_mfma2<MT, ST, PR>), grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
+#define LOGBQ_M2(MT, ST, PR) hipLaunchKernelGGL((k_mfma2<MT, ST, PR, (MT <= 2)>), grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
   switch (mt16) {
     case 1: LOGBQ_M2(1, 4, true); break;
     case 2: LOGBQ_M2(2, 4, true); break;
@@ -788,9 +851,8 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
                     hipStream_t st) {
   int live[kMaxSegs];
   int nlive = 0;
-  int64_t rows = 0;
   for (int i = 0; i < count; ++i)
-    if (jobs[i].n > 0) { live[nlive++] = i; rows += jobs[i].n; }
+    if (jobs[i].n > 0) live[nlive++] = i;
   if (m == 0 || nlive == 0) return LOGBQ_OK;
   const int cus = device_cus();
   if (cus <= 0) return LOGBQ_ERR_HIP;
@@ -805,47 +867,52 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
     return LOGBQ_OK;
   }
   const int M = (int)m, K = (int)k;
-  // Path choice (measured on MI355X): the GEMV for m <= 4; for 5 <= m <= 8 the GEMV only while
-  // every matrix has fewer than 8192 rows (the MFMA kernel needs >= 64 workgroups of 128 rows
-  // to fill the chip); the MFMA kernel otherwise.
-  bool gemv = M <= 4;
-  if (M > 4 && M <= 8) {
-    gemv = true;
-    for (int a = 0; a < nlive; ++a)
-      if (jobs[live[a]].n >= 8192) gemv = false;
-  }
+  // Path choice per linear (measured on MI355X). The GEMV's time grows with m * N * K (its
+  // products are VALU dot2 per weight and batch row); the MFMA kernel's is about flat in m up to
+  // 16 but uses only N / 128 workgroups. Measured crossover: the MFMA kernel wins once m >= 3 and
+  // m * N >= 65536 (e.g. N = 28672 from m = 3, N = 14336 from m = 5, N = 8192 at m = 8); the GEMV
+  // takes everything else up to m = 8. The choice depends only on (m, k, N), so every linear of
+  // a grouped call runs the kernel that a single call would run, with the same result bits.
   int wk = 0, cpl = 0;
-  if (gemv && gemv_config(M, K, &wk, &cpl)) {
-    const int groups = 8 / wk;
-    GemvSegs segs;
-    std::memset(&segs, 0, sizeof(segs));
-    segs.count = nlive;
-    int begin = 0;
-    for (int a = 0; a < nlive; ++a) {
-      const LinearJob& j = jobs[live[a]];
-      const int64_t need = (j.n + groups - 1) / groups;          // workgroups that have rows
-      int64_t share = (int64_t)((double)cus * (double)j.n / (double)rows + 0.5);
-      if (share < 1) share = 1;
-      if (share > need) share = need;
-      GemvSeg& sg = segs.s[a];
-      sg.codes = j.codes;
-      sg.y = j.y;
-      sg.n_rows = (int)j.n;
-      sg.wg_begin = begin;
-      const int64_t tg = share * groups;
-      sg.iters = (int)((j.n + tg - 1) / tg);
-      make_lut16(j.codebook, &sg.lut, &sg.scale);
-      begin += (int)share;
-    }
-    const int stage_x = ((int64_t)M * K * 2 <= (int64_t)kStageXBytes) ? 1 : 0;
-    if (!dispatch_gemv(M, cpl, begin, st, x, K, wk, stage_x, segs)) return LOGBQ_ERR_UNSUPPORTED;
-    return launch_status();
-  }
+  const bool gemv_ok = M <= 8 && gemv_config(M, K, &wk, &cpl);
+  int gl[kMaxSegs];
+  int ng = 0;
+  int64_t grows = 0;
   for (int a = 0; a < nlive; ++a) {
-    const int32_t r = launch_mfma(x, M, K, jobs[live[a]], st);
-    if (r != LOGBQ_OK) return r;
+    const LinearJob& j = jobs[live[a]];
+    if (gemv_ok && !(M >= 3 && (int64_t)M * j.n >= 65536)) {
+      gl[ng++] = live[a];
+      grows += j.n;
+    } else {
+      const int32_t r = launch_mfma(x, M, K, j, st);
+      if (r != LOGBQ_OK) return r;
+    }
   }
-  return LOGBQ_OK;
+  if (ng == 0) return LOGBQ_OK;
+  const int groups = 8 / wk;
+  GemvSegs segs;
+  std::memset(&segs, 0, sizeof(segs));
+  segs.count = ng;
+  int begin = 0;
+  for (int a = 0; a < ng; ++a) {
+    const LinearJob& j = jobs[gl[a]];
+    const int64_t need = (j.n + groups - 1) / groups;          // workgroups that have rows
+    int64_t share = (int64_t)((double)cus * (double)j.n / (double)grows + 0.5);
+    if (share < 1) share = 1;
+    if (share > need) share = need;
+    GemvSeg& sg = segs.s[a];
+    sg.codes = j.codes;
+    sg.y = j.y;
+    sg.n_rows = (int)j.n;
+    sg.wg_begin = begin;
+    const int64_t tg = share * groups;
+    sg.iters = (int)((j.n + tg - 1) / tg);
+    make_lut16(j.codebook, &sg.lut, &sg.scale);
+    begin += (int)share;
+  }
+  const int stage_x = ((int64_t)M * K * 2 <= (int64_t)kStageXBytes) ? 1 : 0;
+  if (!dispatch_gemv(M, cpl, begin, st, x, K, wk, stage_x, segs)) return LOGBQ_ERR_UNSUPPORTED;
+  return launch_status();
 }
 
 }  // namespace

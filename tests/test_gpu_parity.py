@@ -293,20 +293,22 @@ def test_linear_multi_matches_single_launches():
     """Grouped launch of linears sharing x: every output equals the single-linear call bit for
     bit, and the oracle within tolerance (qkv-like and gate/up-like groups, ragged sizes)."""
     k = 2048
-    groups = [[2048, 512, 512], [4096, 4096], [37, 1000, 1, 64], [300]]
+    # the last group mixes paths at m = 8 (8 * 8192 rows picks the MFMA kernel, 64 rows the GEMV)
+    groups = [[2048, 512, 512], [4096, 4096], [37, 1000, 1, 64], [300], [8192, 64]]
     for gi, ns in enumerate(groups):
         tensors = [prepare(n, k, [8, 7, gi, j]) for j, n in enumerate(ns)]
         codes = [gpu_encode(w, p) for w, p, r in tensors]
-        for m in (1, 2, 4, 8, 16):
+        whs = [O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
+               for w, p, r in tensors]
+        for m in (1, 2, 3, 4, 8, 16):
             _say(f"linear_multi group {ns} m={m}")
             x = inputs.activations(m, k, seed=[8, 7, gi, 100 + m])
             xd = torch.from_numpy(x).to(DEV)
             ys = L.linear_multi(xd, [c for c, _ in codes], [cb for _, cb in codes])
-            for (c, cb), y, (w, p, r) in zip(codes, ys, tensors):
+            for (c, cb), y, wh in zip(codes, ys, whs):
                 y1 = L.linear(xd, c, cb)
                 torch.cuda.synchronize()
                 assert torch.equal(y, y1)
-                wh = O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
                 assert rel_err(y.cpu().numpy(), x, wh) <= TOL
 
 
