@@ -198,6 +198,30 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=Tr
                                 "wmax": p.wmax}}, codes, cb
 
 
+def read_ceiling(torch, stream, nbytes=1 << 32, steps=20, warmup=10):
+    """HBM read ceiling: the pure streaming-read kernel of libhbmread.so (128-bit non-temporal
+    loads, the GEMV's access pattern and prefetch depth, no compute) over a 4 GiB buffer."""
+    path = os.path.join(ROOT, "paper_2607_01127_amd", "libhbmread.so")
+    lib = ctypes.CDLL(path)
+    lib.hbm_read.restype = ctypes.c_int32
+    lib.hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32,
+                             ctypes.c_void_p]
+    grid = torch.cuda.get_device_properties(0).multi_processor_count
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    buf.fill_(1)
+    sink = torch.zeros(grid * 512, dtype=torch.int32, device="cuda:0")
+    st = ctypes.c_void_p(stream.cuda_stream)
+
+    def one(i):
+        r = lib.hbm_read(ctypes.c_void_p(buf.data_ptr()), nbytes, ctypes.c_void_p(sink.data_ptr()),
+                         grid, st)
+        assert r == 0, r
+    ms = time_region(torch, stream, one, steps, warmup)
+    del buf, sink
+    return {"GB_s": nbytes / ms / 1e6, "bytes": nbytes, "ms": ms,
+            "kernel": "k_read (libhbmread.so), 4 KiB per wavefront unit, 2 units in flight"}
+
+
 def bench_small(torch, L, inputs, dev, stream, name, steps, warmup):
     wl = inputs.WORKLOADS[name]
     lin = wl["layers"][0]
@@ -286,7 +310,31 @@ def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):
         assert all(torch.equal(ref[key], ys[key]) for key in ys), "graph replay differs"
         t = time_region(torch, stream, lambda i: g.replay(), steps, warmup)
         log(f"{name} m={m}: {t * 1e3:.1f} us per pass")
+        # Sum of launch times: the launches of one group kind (e.g. every layer's gate/up) run
+        # back to back in a graph of their own; the four kinds together are the pass's launches
+        # without the switches between kinds.
+        sum_ms = 0.0
+        kinds = {}
+        for grp in plan:
+            kinds.setdefault(grp[0][0].name, []).append(grp)
+        for kind, grps in kinds.items():
+            gk = torch.cuda.CUDAGraph()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(gk, stream=cap):
+                ck = Calls(L, torch.cuda.current_stream().cuda_stream)
+                for grp in grps:
+                    x = xs[(grp[0][0].k, leader[grp[0][0].name])]
+                    if len(grp) == 1:
+                        ck.add(x, grp[0][1], grp[0][2], ys[id(grp[0][1])])
+                    else:
+                        ck.add_multi(x, [c for _, c, _ in grp], [cb for _, _, cb in grp],
+                                     [ys[id(c)] for _, c, _ in grp])
+                for i in range(len(grps)):
+                    ck.run(i)
+            sum_ms += time_region(torch, stream, lambda i: gk.replay(), max(10, steps // 4), 5)
+            del gk
         out[f"m{m}"] = {"ms_per_token_pass": t, "tokens_per_s": m / (t * 1e-3),
+                        "sum_launch_ms": sum_ms, "switch_overhead_frac": 1.0 - sum_ms / t,
                         "weight_GB_s": bytes_pass / t / 1e6,
                         "hbm_frac": bytes_pass / t / 1e6 / HBM_PEAK_GBS,
                         "launches": len(plan), "linears": len(tensors)}
@@ -318,9 +366,30 @@ def profiled_traffic():
         return None
 
 
-def cpu_baseline(L_unused, inputs, target_s=12.0):
-    """The oracle (unpack + dequantize + float64 matmul) on a row sample of the layer."""
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(L_unused, inputs, target_s=10.0):
+    """The oracle on the host cores of this machine, as it stands (plain float64 numpy).
+
+    Main figure: unpack + dequantize + float64 matmul on a 1024-row sample of the 8192x28672
+    layer at M = 1, repeated for about `target_s` seconds with the BLAS threads pinned to the
+    cores this process may run on. Also: the oracle fit and encode of the 2048x2048 linear, and
+    one single-threaded dequantize + matmul of the 2048x2048, 2048x8192 and layer-sample
+    tensors."""
     from oracle import logbq_oracle as O
+    affinity = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_limits, threadpool_info
+    except ImportError:
+        threadpool_limits = threadpool_info = None
     wl = inputs.WORKLOADS["layer_8192x28672"]
     lin = wl["layers"][0]
     rows = 1024
@@ -329,27 +398,65 @@ def cpu_baseline(L_unused, inputs, target_s=12.0):
     codes = O.pack(O.encode(w, r.base, r.shift))
     lut = O.codebook(r.base, r.shift)
     x = inputs.activations(1, lin.k, seed=[wl["cfg"], 0, 0, 1])
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        y = O.linear(x, O.dequantize(O.unpack(codes), lut))
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= target_s or reps >= 100000:
-            break
-    del y
-    per = el / reps
-    threads = 1
+
+    def matvec(c, xx, lt):
+        return O.linear(xx, O.dequantize(O.unpack(c), lt))
+
+    ctx = threadpool_limits(limits=affinity) if threadpool_limits else None
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([1] + [int(i.get("num_threads", 1)) for i in threadpool_info()])
-    except Exception:
-        pass
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            matvec(codes, x, lut)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= target_s or reps >= 100000:
+                break
+        threads = 1
+        if threadpool_info:
+            threads = max([1] + [int(i.get("num_threads", 1)) for i in threadpool_info()])
+    finally:
+        if ctx is not None:
+            ctx.unregister()
+    per = el / reps
     packed = rows * lin.k // 2
+
+    # oracle fit / encode / single-threaded matvec on the other workloads
+    extra = {}
+    small = inputs.WORKLOADS["linear_2048x2048"]
+    sl = small["layers"][0]
+    ws = inputs.student_t_weights(sl.n, sl.k, small["nu"], small["scale"], seed=[small["cfg"], 0, 0, 0])
+    t0 = time.perf_counter()
+    rs = O.fit(ws)
+    extra["fit_s_2048x2048"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    cs = O.encode(ws, rs.base, rs.shift)
+    extra["encode_s_2048x2048"] = time.perf_counter() - t0
+    up = inputs.WORKLOADS["up_2048x8192_outliers"]
+    ul = up["layers"][0]
+    wu = inputs.student_t_weights(ul.n, ul.k, up["nu"], up["scale"], seed=[up["cfg"], 0, 0, 0],
+                                  outlier_frac=up.get("outlier_frac", 0.0))
+    ru = O.fit(wu)
+    cu = O.pack(O.encode(wu, ru.base, ru.shift))
+    ctx = threadpool_limits(limits=1) if threadpool_limits else None
+    try:
+        for name, c, lt, kk in (("2048x2048", O.pack(cs), O.codebook(rs.base, rs.shift), sl.k),
+                                ("2048x8192", cu, O.codebook(ru.base, ru.shift), ul.k),
+                                ("layer_sample_1024x8192", codes, lut, lin.k)):
+            xx = inputs.activations(1, kk, seed=[0, 0, 0, 1])
+            t0 = time.perf_counter()
+            matvec(c, xx, lt)
+            dt = time.perf_counter() - t0
+            extra[f"linear_1thread_s_{name}"] = dt
+            extra[f"linear_1thread_GB_s_{name}"] = c.size / dt / 1e9
+    finally:
+        if ctx is not None:
+            ctx.unregister()
     return {"value": packed / per / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"{rows} of 28672 rows of the 8192x28672 layer at M=1, {reps} reps, "
                       f"{el:.1f} s; unpack + dequantize + float64 matmul (numpy; BLAS threads "
                       f"{threads}, table lookup single-threaded)",
-            "s_per_rep": per}
+            "s_per_rep": per, "affinity_cores": affinity, "nproc": os.cpu_count(),
+            "cpu_model": _cpu_model(), **{k: round(v, 4) for k, v in extra.items()}}
 
 
 def main():
@@ -398,6 +505,9 @@ def main():
     value = packed / t_ms / 1e6
 
     rows = dict(res)
+    log("HBM read ceiling (4 GiB)")
+    ceiling = read_ceiling(torch, stream)
+    torch.cuda.empty_cache()
     if "small" in want:
         for name in ("up_2048x8192_outliers", "linear_2048x2048"):
             log(name)
@@ -433,7 +543,9 @@ def main():
                      "frac": round(algo / t_ms / 1e6 / HBM_PEAK_GBS, 4),
                      "traffic": profiled_traffic(),
                      "kernel": "k_gemv<1, 4, false, 2>", "algo_bytes_per_launch": algo,
-                     "avg_launch_us": t_ms * 1e3},
+                     "avg_launch_us": t_ms * 1e3,
+                     "read_ceiling_GB_s": round(ceiling["GB_s"], 1),
+                     "frac_of_read_ceiling": round(algo / t_ms / 1e6 / ceiling["GB_s"], 4)},
         "cpu_baseline": cpu,
         "rows": rows,
     }

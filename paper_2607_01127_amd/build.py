@@ -1,4 +1,5 @@
-"""Build liblogbq.so in-tree: the host fit with g++, the gfx950 kernels with hipcc.
+"""Build liblogbq.so in-tree: the host fit with g++, the gfx950 kernels with hipcc. Also builds
+libhbmread.so, the streaming-read kernel bench.py measures the HBM read ceiling with.
 
 The host fit is compiled without -ffast-math and with -ffp-contract=off so that its float64
 arithmetic rounds exactly as written. All HIP code is compiled with packed-fp32 instructions
@@ -14,6 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "liblogbq.so")
+READ_LIB = os.path.join(HERE, "libhbmread.so")
 ARCH = os.environ.get("LOGBQ_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -39,6 +41,9 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, fit_o, ker_o], verbose)
     os.replace(tmp, LIB)
+    tmp = READ_LIB + ".tmp"
+    _run([HIPCC, *HIP_FLAGS, "-shared", "-o", tmp, os.path.join(CSRC, "hbm_read.hip")], verbose)
+    os.replace(tmp, READ_LIB)
     return LIB
 
 

@@ -1,6 +1,8 @@
 """Summaries of rocprofv3 output for the profiles/ folder.
 
 kernel-stats: python -m paper_2607_01127_amd.prof_summary stats STATS_CSV CMD > profiles/X.md
+trace:        python -m paper_2607_01127_amd.prof_summary trace TRACE_CSV CMD > profiles/X.md
+counters:     python -m paper_2607_01127_amd.prof_summary counters PMC_CSV KERNEL_SUBSTR CMD > X.md
 traffic:      python -m paper_2607_01127_amd.prof_summary traffic KERNEL_SUBSTR FETCH_CSV WRITE_CSV \
                   COPY_FETCH_CSV COPY_WRITE_CSV COPY_BYTES CMD > profiles/X.md
 
@@ -44,6 +46,45 @@ def stats(path, cmd):
               f"{float(r['MaxNs'])/1e3:.2f} | {float(r['Percentage']):.1f} |")
 
 
+def _pct(vals, q):
+    v = sorted(vals)
+    if not v:
+        return float("nan")
+    i = min(len(v) - 1, max(0, int(round(q * (len(v) - 1)))))
+    return v[i]
+
+
+def trace(path, cmd):
+    """Per-kernel dispatch-duration distribution from a rocprofv3 kernel trace."""
+    durs = {}
+    for r in csv.DictReader(open(path)):
+        name = r["Kernel_Name"]
+        if "at::native" in name or "rocclr" in name:
+            continue
+        d = (float(r["End_Timestamp"]) - float(r["Start_Timestamp"])) / 1e3
+        durs.setdefault(_short(name), []).append(d)
+    print("# rocprofv3 kernel trace: dispatch durations\n")
+    print(f"Command: `{cmd}`\n")
+    print("| kernel | dispatches | mean (us) | p10 (us) | median (us) | p90 (us) | total (ms) |")
+    print("|---|---|---|---|---|---|---|")
+    for name, v in sorted(durs.items(), key=lambda kv: -sum(kv[1])):
+        print(f"| `{name}` | {len(v)} | {statistics.fmean(v):.2f} | {_pct(v, 0.1):.2f} | "
+              f"{_pct(v, 0.5):.2f} | {_pct(v, 0.9):.2f} | {sum(v) / 1e3:.2f} |")
+
+
+def counters(path, substr, cmd):
+    """Median per-dispatch value of every counter collected for kernels matching substr."""
+    vals = {}
+    for r in csv.DictReader(open(path)):
+        if substr in r["Kernel_Name"]:
+            vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    print("# rocprofv3 counters per dispatch\n")
+    print(f"Command: `{cmd}`\n")
+    print(f"kernel: `{substr}`\n")
+    for name, v in sorted(vals.items()):
+        print(f"- {name}: median {statistics.median(v):.6g} over {len(v)} dispatches")
+
+
 def _counter(path, substr, counter):
     vals = []
     for r in csv.DictReader(open(path)):
@@ -78,3 +119,7 @@ if __name__ == "__main__":
         stats(sys.argv[2], sys.argv[3])
     elif sys.argv[1] == "traffic":
         traffic(*sys.argv[2:9])
+    elif sys.argv[1] == "trace":
+        trace(sys.argv[2], sys.argv[3])
+    elif sys.argv[1] == "counters":
+        counters(sys.argv[2], sys.argv[3], sys.argv[4])
