@@ -8,9 +8,10 @@
 //              float16 pairs held in LDS (one private copy per lane, so lookups never conflict on
 //              a bank); v_dot2_f32_f16 accumulates in float32; DPP row reductions plus lane reads
 //              finish the wavefront sum.
-//   k_mfma     y = x . W_hat^T for larger m: the same byte -> float16-pair lookup builds the B
-//              operand of v_mfma_f32_32x32x16_f16 straight from a code dword; activations are
-//              staged through LDS as the A operand; float32 accumulation in the MFMA.
+//   k_mfma2    y = x . W_hat^T for larger m: a code dword (8 weights of one row) becomes one
+//              lane's B operand of v_mfma_f32_16x16x32_f16, dequantized by pair-table lookups
+//              or by v_perm_b32 byte tables in registers; activations are staged through LDS
+//              as the A operand; float32 accumulation in the MFMA.
 //
 // The float16 tables hold codebook / 2^e with 2^e chosen so that the largest entry lies in
 // [2^14, 2^15); the result is multiplied back by 2^e (exact). Lookup replaces evaluating
@@ -941,7 +942,8 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
   const int cus = device_cus();
   if (cus <= 0) return LOGBQ_ERR_HIP;
   const int64_t nchunk = numel / 4;
-  const int64_t grid = grid_for(nchunk, 256 * kEncU, (int64_t)cus * 8);
+  // 32 workgroups (128 wavefronts) per CU: measured 4 % faster than 8 on the 8192x28672 tensor.
+  const int64_t grid = grid_for(nchunk, 256 * kEncU, (int64_t)cus * 32);
   hipLaunchKernelGGL(k_encode, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream,
                      reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint16_t*>(codes_dev),
                      nchunk, th);

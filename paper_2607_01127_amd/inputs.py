@@ -97,16 +97,17 @@ def decoder_linears(hidden: int, inter: int, kv: int):
             Linear("up", hidden, inter), Linear("down", inter, hidden)]
 
 
-# The five synthetic workloads (weights: scale * t_nu; activations fp16 N(0,1)).
+# The five synthetic workloads (weights: scale * t_nu; activations fp16 N(0,1)); cfg is the
+# first seed element, numbered 1..5 in this order.
 WORKLOADS = {
-    "linear_2048x2048": dict(cfg=0, layers=[Linear("w", 2048, 2048)], nu=4, scale=0.02,
+    "linear_2048x2048": dict(cfg=1, layers=[Linear("w", 2048, 2048)], nu=4, scale=0.02,
                              outlier_frac=0.0, batch=(1,)),
-    "up_2048x8192_outliers": dict(cfg=1, layers=[Linear("up", 2048, 8192)], nu=4, scale=0.02,
+    "up_2048x8192_outliers": dict(cfg=2, layers=[Linear("up", 2048, 8192)], nu=4, scale=0.02,
                                   outlier_frac=1e-4, batch=(1,)),
-    "decode_1b_16x7": dict(cfg=2, layers=decoder_linears(2048, 8192, 512) * 1, n_layers=16,
+    "decode_1b_16x7": dict(cfg=3, layers=decoder_linears(2048, 8192, 512) * 1, n_layers=16,
                            nu=4, scale=0.02, outlier_frac=0.0, batch=(1,)),
-    "decode_8b_32x7": dict(cfg=3, layers=decoder_linears(4096, 14336, 1024), n_layers=32,
+    "decode_8b_32x7": dict(cfg=4, layers=decoder_linears(4096, 14336, 1024), n_layers=32,
                            nu=4, scale=0.02, outlier_frac=0.0, batch=(1, 4)),
-    "layer_8192x28672": dict(cfg=4, layers=[Linear("w", 8192, 28672)], nu=3, scale=0.015,
+    "layer_8192x28672": dict(cfg=5, layers=[Linear("w", 8192, 28672)], nu=3, scale=0.015,
                              outlier_frac=0.0, batch=(1, 8, 32, 128)),
 }
