@@ -105,7 +105,7 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  * logbq_linear -- y = x . W_hat^T on packed codes: weight-only inference with the codebook
  * lookup fused into the product (Sec. 3.3).
  *   x_dev     : device, [m][k] IEEE float16 activations (bit patterns as uint16).
- *   m, k      : batch rows and in features; k % 32 == 0.
+ *   m, k      : batch rows and in features; k % 32 == 0, m <= 4194240 (65535 * 64).
  *   codes_dev : device, [n][k/2] packed codes.
  *   n         : out features.
  *   codebook  : host, 16 floats (logbq_params.codebook); copied into the kernel arguments,

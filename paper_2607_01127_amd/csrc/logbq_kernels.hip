@@ -817,6 +817,9 @@ bool make_lut_bytes(const float* cb, LutBytes* tb, float* scale) {
   return true;
 }
 
+// Largest batch: the MFMA grid's y dimension (at most 65535) covers 64 batch rows or more each.
+constexpr int64_t kMaxBatchRows = 65535LL * 64;
+
 int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st) {
   const int N = (int)j.n;
   LutBytes tb = {0, 0, 0, 0};
@@ -975,7 +978,7 @@ int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t*
                      int64_t n, const float* codebook, float* y_dev, void* stream) {
   if (m < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
   if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
-  if (m > INT32_MAX || k > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
+  if (m > kMaxBatchRows || k > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
   LinearJob j{codes_dev, n, codebook, y_dev};
   const int32_t v = validate_job(j, m, k);
   if (v != LOGBQ_OK) return v;
@@ -993,7 +996,7 @@ int32_t logbq_linear_multi(const uint16_t* x_dev, int64_t m, int64_t k, int32_t 
   if (m < 0 || k < 0 || count < 1 || count > kMaxSegs) return LOGBQ_ERR_INVALID_ARG;
   if (!codes_dev || !n || !codebooks || !y_dev) return LOGBQ_ERR_INVALID_ARG;
   if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
-  if (m > INT32_MAX || k > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
+  if (m > kMaxBatchRows || k > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
   LinearJob jobs[kMaxSegs];
   bool any = false;
   for (int i = 0; i < count; ++i) {

@@ -60,6 +60,7 @@ def test_linear_validation_before_hip():
     bad[3] = float("nan")
     assert h.logbq_linear(a, 1, 64, a, 4, bad, a, None) == L.ERR_INVALID_ARG
     assert h.logbq_linear(a, 1, 2 ** 33, a, 4, cb, a, None) == L.ERR_UNSUPPORTED
+    assert h.logbq_linear(a, 65535 * 64 + 1, 64, a, 4, cb, a, None) == L.ERR_UNSUPPORTED  # grid.y
     # empty calls succeed without touching the device
     assert h.logbq_linear(None, 0, 64, None, 4, cb, None, None) == L.OK
     assert h.logbq_linear(None, 3, 64, None, 0, cb, None, None) == L.OK
