@@ -15,7 +15,8 @@ Python ``fractions`` for the few decisions that must be exact:
                       magnitude index to [0, q_max], attach the sign.
 * ``magnitude_thresholds`` -- the smallest fp32 value whose Quant magnitude is k+1, for each
                       k; by monotonicity of Eq. 1 these describe the same quantizer.
-* ``pack`` / ``unpack`` -- two 4-bit codes per byte (Sec. 3.3: weight packing).
+* ``pack`` / ``unpack`` -- two 4-bit codes per byte (Sec. 3.3: weight packing);
+                      ``pack_codes`` / ``unpack_codes`` also take 8-bit codes, one per byte.
 * ``dequantize``   -- Dequant (Eq. 2) by table lookup (Sec. 3.3: LUT instead of b^x).
 * ``linear``       -- y = x . W_hat^T in float64.
 
@@ -43,7 +44,8 @@ import numpy as np
 
 __all__ = [
     "OracleError", "FitResult", "qmax", "fit", "codebook", "encode", "magnitude_thresholds",
-    "pack", "unpack", "dequantize", "linear", "energy_ratio_exact", "log_nearest_code",
+    "pack", "unpack", "pack_codes", "unpack_codes", "dequantize", "linear", "energy_ratio_exact",
+    "log_nearest_code",
 ]
 
 
@@ -237,6 +239,25 @@ def unpack(packed: np.ndarray) -> np.ndarray:
     out[:, 0::2] = packed & 0x0F
     out[:, 1::2] = packed >> 4
     return out
+
+
+def pack_codes(codes: np.ndarray, bits: int) -> np.ndarray:
+    """Storage layout of n-bit codes: 4-bit codes two per byte (``pack``), 8-bit codes one per
+    byte ([N][K] as is)."""
+    if bits == 4:
+        return pack(codes)
+    if bits == 8:
+        return np.array(codes, dtype=np.uint8, copy=True)
+    raise OracleError("invalid_arg", "bits must be 4 or 8")
+
+
+def unpack_codes(packed: np.ndarray, bits: int) -> np.ndarray:
+    """Inverse of ``pack_codes``."""
+    if bits == 4:
+        return unpack(packed)
+    if bits == 8:
+        return np.array(packed, dtype=np.uint8, copy=True)
+    raise OracleError("invalid_arg", "bits must be 4 or 8")
 
 
 def dequantize(codes: np.ndarray, lut: np.ndarray) -> np.ndarray:
