@@ -47,15 +47,18 @@ class Calls:
     def __init__(self, L, stream):
         self.L = L
         self.fn = L.lib().logbq_linear
+        self.fn8 = L.lib().logbq_linear8
         self.fn_multi = L.lib().logbq_linear_multi
         self.stream = ctypes.c_void_p(stream)
         self.args = []
         self.keep = []
 
     def add(self, x, codes, cb, y):
+        """logbq_linear for 16-entry codebooks, logbq_linear8 for 256-entry ones."""
         cbarr = np.ascontiguousarray(cb, dtype=np.float32)
         self.keep.append(cbarr)
-        self.args.append((self.fn, (ctypes.c_void_p(x.data_ptr()), x.shape[0], x.shape[1],
+        fn = self.fn8 if cbarr.size == 256 else self.fn
+        self.args.append((fn, (ctypes.c_void_p(x.data_ptr()), x.shape[0], x.shape[1],
                                     ctypes.c_void_p(codes.data_ptr()), codes.shape[0],
                                     cbarr.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
                                     ctypes.c_void_p(y.data_ptr()), self.stream)))
@@ -196,6 +199,51 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=Tr
     return results, {"n": n, "k": k, "packed": packed, "copies": copies, "fit_s": fit_s,
                      "params": {"base": p.base, "shift": p.shift, "wmin": p.wmin,
                                 "wmax": p.wmax}}, codes, cb
+
+
+def bench_layer8(torch, L, inputs, dev, stream, ms, steps, warmup):
+    """The 8192 x 28672 layer at 8 bits (q_max = 127, eps = 1e-6): one code byte per weight,
+    256-entry table. Same weights and activations as the 4-bit layer."""
+    wl = inputs.WORKLOADS["layer_8192x28672"]
+    lin = wl["layers"][0]
+    n, k = lin.n, lin.k
+    log("layer 8192x28672 at 8 bits: generate / fit / encode")
+    wd = inputs.student_t_weights(n, k, wl["nu"], wl["scale"], seed=[wl["cfg"], 0, 0, 0],
+                                  device=dev)
+    p = L.fit(wd.cpu().numpy(), 8, 1e-6)
+    codes, cb = L.encode(wd, p)
+    torch.cuda.synchronize()
+    nbytes = n * k
+    enc_out = torch.empty_like(codes)
+
+    def enc(i):
+        L.encode(wd, p, out=enc_out, stream=stream)
+    enc_ms = time_region(torch, stream, enc, max(5, steps // 20), 100)
+    assert torch.equal(enc_out, codes)
+    del wd, enc_out
+    enc_bytes = n * k * 4 + nbytes
+    results = {"encode8_8192x28672": {"ms": enc_ms, "GB_s": enc_bytes / enc_ms / 1e6,
+                                      "hbm_frac": enc_bytes / enc_ms / 1e6 / HBM_PEAK_GBS,
+                                      "bytes": enc_bytes}}
+    copies = max(2, -(-ROTATE_BYTES // nbytes))
+    code_list = [codes] + [codes.clone() for _ in range(copies - 1)]
+    for m in ms:
+        x = inputs.activations(m, k, seed=[wl["cfg"], 0, 0, 1], device=dev)
+        launches = [(x, c, cb, torch.empty((m, n), dtype=torch.float32, device=dev))
+                    for c in code_list]
+        timed = steps if m == ms[0] else max(64, steps // 4)
+        t = time_launches(torch, L, stream, launches, timed, warmup if m == ms[0] else warmup // 4)
+        log(f"layer8 m={m}: {t * 1e3:.2f} us per launch")
+        algo = nbytes + 2 * m * k + 4 * m * n + 1024
+        flops = 2.0 * m * n * k
+        results[f"linear8_8192x28672_m{m}"] = {
+            "ms": t, "us": t * 1e3, "launches_timed": timed, "weight_GB_s": nbytes / t / 1e6,
+            "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
+            "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
+            "algo_bytes": algo, "copies": copies,
+            "path": "gemv" if m <= 8 and not (m >= 3 and m * n >= 65536) else "mfma"}
+    del code_list, codes
+    return results
 
 
 def read_ceiling(torch, stream, nbytes=1 << 32, steps=20, warmup=10):
@@ -466,8 +514,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10000,
                     help="untimed launches before the timed ones (about 0.2 s of GPU work at M = 1)")
     ap.add_argument("--quick", action="store_true", help="main layer only, no extra rows")
-    ap.add_argument("--rows", default="layer,small,decode1b,decode8b",
-                    help="comma list of extra rows: layer (M sweep + encode), small, decode1b, decode8b")
+    ap.add_argument("--rows", default="layer,layer8,small,decode1b,decode8b",
+                    help="comma list of extra rows: layer (M sweep + encode), layer8 (the same "
+                         "layer at 8 bits), small, decode1b, decode8b")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device-to-device copy (calibrates the HBM byte "
@@ -514,6 +563,10 @@ def main():
             rows[name + "_m1"] = bench_small(torch, L, inputs, dev, stream, name, 2000, 5000)
     del codes
     torch.cuda.empty_cache()
+    if "layer8" in want:
+        rows.update(bench_layer8(torch, L, inputs, dev, stream, [1, 8, 32, 128],
+                                 args.steps // 2, args.warmup // 2))
+        torch.cuda.empty_cache()
     if "decode1b" in want:
         rows["decode_1b_16x7"] = bench_decode(torch, L, inputs, dev, stream, "decode_1b_16x7",
                                               [1], 200, 200)
@@ -542,7 +595,7 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(algo / t_ms / 1e6 / HBM_PEAK_GBS, 4),
                      "traffic": profiled_traffic(),
-                     "kernel": "k_gemv<1, 4, false, 2>", "algo_bytes_per_launch": algo,
+                     "kernel": "k_gemv<4, 1, 4, false, 2>", "algo_bytes_per_launch": algo,
                      "avg_launch_us": t_ms * 1e3,
                      "read_ceiling_GB_s": round(ceiling["GB_s"], 1),
                      "frac_of_read_ceiling": round(algo / t_ms / 1e6 / ceiling["GB_s"], 4)},

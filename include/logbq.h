@@ -1,5 +1,6 @@
 /*
- * logbq.h -- C ABI of liblogbq, 4-bit LogbQuant weight-only inference on AMD MI355X (gfx950).
+ * logbq.h -- C ABI of liblogbq, LogbQuant weight-only inference (4-bit and 8-bit codes) on AMD
+ * MI355X (gfx950).
  *
  * LogbQuant (Bohn et al., arXiv 2607.01127) quantizes each weight matrix with its own
  * logarithmic codebook of base b and shift s (Sec. 3.1): a weight x maps to the integer
@@ -17,9 +18,11 @@
  *   - The caller owns every buffer. "device" pointers are HIP device memory of the current
  *     device; "host" pointers are ordinary host memory.
  *   - Weights are row-major [N][K] (N out features, K in features, as a PyTorch Linear).
- *   - Packed codes: row-major [N][K/2] bytes; element (n, k) is the nibble at byte
+ *   - 4-bit codes: row-major [N][K/2] bytes; element (n, k) is the nibble at byte
  *     n*K/2 + k/2, the low nibble when k is even. A nibble is sign<<3 | magnitude: bit 3 set
  *     means negative, magnitude 0..7 is |q|. Code 8 ("-0") is never written and decodes to +0.
+ *   - 8-bit codes: row-major [N][K] bytes, one code per weight: sign<<7 | magnitude (0..127).
+ *     Code 128 ("-0") is never written and decodes to +0.
  *   - Shapes: K must be a multiple of 32 (every packed row is then 16-byte aligned);
  *     device pointers must be 16-byte aligned. N = 0 or M = 0 is a valid empty call.
  */
@@ -32,20 +35,21 @@
 extern "C" {
 #endif
 
-#define LOGBQ_ABI_VERSION 1
+#define LOGBQ_ABI_VERSION 2
 
 typedef enum logbq_status {
   LOGBQ_OK = 0,
   LOGBQ_ERR_INVALID_ARG = 1,   /* null pointer, negative size, eps outside (0,1), ... */
   LOGBQ_ERR_NONFINITE = 2,     /* fit: a weight is NaN or Inf                           */
   LOGBQ_ERR_DEGENERATE = 3,    /* fit: all weights zero, or w_min == w_max (b = 1)      */
-  LOGBQ_ERR_UNSUPPORTED = 4,   /* bits != 4, K % 32 != 0, misaligned pointer, too large */
+  LOGBQ_ERR_UNSUPPORTED = 4,   /* bits not 4 or 8, K % 32 != 0, misaligned, too large    */
   LOGBQ_ERR_HIP = 5            /* a HIP call failed (no device, launch failure, ...)    */
 } logbq_status;
 
-/* Per-tensor codebook parameters (Sec. 3.1, Sec. 3.2). Plain data; copy freely. */
+/* Per-tensor codebook parameters (Sec. 3.1, Sec. 3.2). Plain data; copy freely.
+ * ABI version 2 widened codebook and thresholds for 8-bit codes (version 1 had 16 and 8). */
 typedef struct logbq_params {
-  int32_t bits;            /* codebook bit width n; 4 is supported                        */
+  int32_t bits;            /* codebook bit width n: 4 or 8                                 */
   int32_t qmax;            /* q_max = 2^(n-1) - 1                                          */
   double eps;              /* pruned energy fraction of Eq. 5                               */
   double wmin;             /* w_min of Eq. 5                                                */
@@ -54,9 +58,10 @@ typedef struct logbq_params {
   int32_t shift;           /* s of Eq. 4 (an integer)                                       */
   int32_t reserved;
   int64_t wmin_index;      /* position of w_min in |w| sorted ascending                     */
-  float codebook[16];      /* Dequant (Eq. 2) of every 4-bit code, float32                  */
-  float thresholds[8];     /* [k] = smallest float32 whose magnitude index exceeds k,
-                              k = 0..qmax-1; [7] = +inf (unused)                            */
+  float codebook[256];     /* Dequant (Eq. 2) of every n-bit code, float32; entries from
+                              2^n on are 0                                                  */
+  float thresholds[128];   /* [k] = smallest float32 whose magnitude index exceeds k,
+                              k = 0..qmax-1; entries from qmax on are +inf                  */
 } logbq_params;
 
 /* ABI version of the loaded library (LOGBQ_ABI_VERSION it was built with). */
@@ -68,16 +73,16 @@ const char* logbq_status_str(int32_t status);
 /*
  * logbq_fit -- per-tensor codebook parameters (Sec. 3.1 Eq. 3-4, Sec. 3.2 Eq. 5). Host only.
  *   w_host : host, numel float32 weights, read only.
- *   bits   : codebook width n; must be 4.
- *   eps    : pruned energy fraction, 0 < eps < 1 (the paper uses 4e-3 at 4 bits).
+ *   bits   : codebook width n, 4 or 8.
+ *   eps    : pruned energy fraction, 0 < eps < 1 (the paper uses 4e-3 at 4 bits, 1e-6 at 8).
  *   out    : host, filled on success; untouched on error.
  * w_max = max|w|. w_min is the smallest |w_i| at which the ascending float64 prefix sum of
  * w^2, divided by the total, reaches eps (sequential summation in ascending |w| order).
  * b = (w_max / w_min)^(1/q_max); s = q_max - J with J the largest integer such that
- * b^J <= w_max. codebook[k] = float32(b^(k-s)), codebook[8+k] = -codebook[k] (k = 1..7),
- * codebook[0] = codebook[8] = +0. thresholds[k] is exact: the smallest float32 t with
- * t >= b^(k + 1/2 - s).
- * Errors: INVALID_ARG (null, numel < 2, eps outside (0,1)), UNSUPPORTED (bits != 4),
+ * b^J <= w_max. codebook[k] = float32(b^(k-s)), codebook[h+k] = -codebook[k] (h = 2^(n-1),
+ * k = 1..q_max), codebook[0] = codebook[h] = +0. thresholds[k] is exact: the smallest float32
+ * t with t >= b^(k + 1/2 - s).
+ * Errors: INVALID_ARG (null, numel < 2, eps outside (0,1)), UNSUPPORTED (bits not 4 or 8),
  * NONFINITE (NaN/Inf weight), DEGENERATE (w_max == 0, or w_min == w_max).
  * Reentrant; allocates host scratch of 4*numel bytes internally for the sort.
  */
@@ -85,18 +90,19 @@ int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
                   logbq_params* out);
 
 /*
- * logbq_encode -- Quant (Eq. 1) of a weight matrix into packed 4-bit codes (Sec. 3.3 packing).
+ * logbq_encode -- Quant (Eq. 1) of a weight matrix into 4-bit or 8-bit codes (Sec. 3.3 packing).
  *   w_dev        : device, [n][k] float32 weights.
  *   n, k         : shape; k % 32 == 0.
- *   p            : host, parameters from logbq_fit (bits must be 4).
- *   codes_dev    : device, [n][k/2] bytes, written.
- *   codebook_out : host, 16 floats, receives p->codebook (may be NULL).
+ *   p            : host, parameters from logbq_fit (bits 4 or 8).
+ *   codes_dev    : device, written: [n][k/2] bytes for 4 bits, [n][k] for 8 bits.
+ *   codebook_out : host, 2^bits floats, receives p->codebook[0 .. 2^bits) (may be NULL).
  *   stream       : hipStream_t or NULL.
  * The magnitude index of x is the number of thresholds t with |x| >= t, which equals
- * clamp(round-half-up(log_b|x| + s), 0, q_max); the sign bit is set for negative x with a
- * nonzero magnitude. NaN and +-0 encode to 0, +-Inf to the largest magnitude with its sign.
- * Errors: INVALID_ARG (null, negative size), UNSUPPORTED (bits, k % 32, alignment),
- * HIP (launch failure).
+ * clamp(round-half-up(log_b|x| + s), 0, q_max); the sign bit (bit n-1) is set for negative x
+ * with a nonzero magnitude. NaN and +-0 encode to 0, +-Inf to the largest magnitude with its
+ * sign.
+ * Errors: INVALID_ARG (null, negative size, qmax not 2^(bits-1) - 1, thresholds[0..qmax)
+ * not positive and ascending), UNSUPPORTED (bits, k % 32, alignment), HIP (launch failure).
  */
 int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_params* p,
                      uint8_t* codes_dev, float* codebook_out, void* stream);
@@ -144,6 +150,29 @@ int32_t logbq_linear_multi(const uint16_t* x_dev, int64_t m, int64_t k, int32_t 
  */
 int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const float* codebook,
                          float* w_dev, void* stream);
+
+/*
+ * logbq_linear8 -- y = x . W_hat^T on 8-bit codes (Sec. 3.1 at n = 8, Sec. 3.3 lookup).
+ *   x_dev     : device, [m][k] IEEE float16 activations.
+ *   m, k      : batch rows and in features; k % 32 == 0, m <= 4194240.
+ *   codes_dev : device, [n][k] 8-bit codes.
+ *   n         : out features.
+ *   codebook  : host, 256 floats (logbq_params.codebook of an 8-bit fit); rounded to float16
+ *               after a common power-of-two scaling, as for logbq_linear.
+ *   y_dev     : device, [m][n] float32, written.
+ * Float32 accumulation. The GEMV runs for m <= 8 unless m >= 3 and m * n >= 65536; the
+ * dequantize-into-MFMA skinny GEMM runs otherwise. Errors: as logbq_linear.
+ */
+int32_t logbq_linear8(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
+                      int64_t n, const float* codebook, float* y_dev, void* stream);
+
+/*
+ * logbq_dequantize8 -- Dequant (Eq. 2) of 8-bit codes: w[n][k] = codebook[codes[n][k]].
+ *   codes_dev : device, [n][k]; codebook: host, 256 floats; w_dev: device, [n][k] float32.
+ * Bit-exact. Errors: INVALID_ARG, UNSUPPORTED, HIP.
+ */
+int32_t logbq_dequantize8(const uint8_t* codes_dev, int64_t n, int64_t k, const float* codebook,
+                          float* w_dev, void* stream);
 
 #ifdef __cplusplus
 }

@@ -164,7 +164,7 @@ int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
                   logbq_params* out) {
   if (!w_host || !out || numel < 2) return LOGBQ_ERR_INVALID_ARG;
   if (!(eps > 0.0 && eps < 1.0)) return LOGBQ_ERR_INVALID_ARG;
-  if (bits != 4) return LOGBQ_ERR_UNSUPPORTED;
+  if (bits != 4 && bits != 8) return LOGBQ_ERR_UNSUPPORTED;
   const int32_t qmax = (1 << (bits - 1)) - 1;
 
   // |w| as float32 bit patterns (sign cleared); reject NaN / Inf.
@@ -222,8 +222,10 @@ int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
   }
   p.codebook[0] = 0.0f;
   p.codebook[half] = 0.0f;
-  for (int k = 0; k < qmax; ++k) p.thresholds[k] = exact_threshold(b, p.shift, k);
-  p.thresholds[7] = std::numeric_limits<float>::infinity();
+  const int nthr = (int)(sizeof(p.thresholds) / sizeof(p.thresholds[0]));
+  for (int k = 0; k < nthr; ++k)
+    p.thresholds[k] = k < qmax ? exact_threshold(b, p.shift, k)
+                               : std::numeric_limits<float>::infinity();
   *out = p;
   return LOGBQ_OK;
 }

@@ -45,8 +45,13 @@ constexpr int kBufferRsrcWord3 = 0x00020000;
 constexpr int kCachePolicyNT = 2;
 
 struct Thresholds { float t[7]; };
+struct Thresholds8 { float t[127]; };
 struct Codebook32 { float v[16]; };
-struct Lut16 { uint32_t h[8]; };   // h[i] = f16(lut[2i]) | f16(lut[2i+1]) << 16
+struct Lut16 { uint32_t h[8]; };     // h[i] = f16(lut[2i]) | f16(lut[2i+1]) << 16
+struct Lut256 { uint32_t h[128]; };  // the same for the 256 entries of an 8-bit codebook
+template <int BITS> struct LutOf;
+template <> struct LutOf<4> { using type = Lut16; };
+template <> struct LutOf<8> { using type = Lut256; };
 
 constexpr int kLutEntries = 256;   // one entry per code byte (two nibbles)
 constexpr int kLutCopies = 64;     // one copy per lane of a wavefront
@@ -118,6 +123,66 @@ __global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ co
   }
 }
 
+// 8-bit codes. Encode: the magnitude index of |x| is the number of the 127 sorted thresholds at
+// or below it, found by a 7-step binary search over a copy of the thresholds in LDS; one code
+// byte per weight, four per float4 chunk (stored as one dword). Tiles as in k_encode.
+__global__ __launch_bounds__(256) void k_encode8(const f32x4* __restrict__ w,
+                                                 uint32_t* __restrict__ codes, int64_t nchunk,
+                                                 Thresholds8 th) {
+  __shared__ float s_t[128];
+  if (threadIdx.x < 127) s_t[threadIdx.x] = th.t[threadIdx.x];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  const int64_t ntiles = (nchunk + 64 * kEncU - 1) / (64 * kEncU);
+  for (int64_t t = wave; t < ntiles; t += nwaves) {
+    const int64_t base = t * 64 * kEncU + lane;
+    f32x4 v[kEncU];
+#pragma unroll
+    for (int j = 0; j < kEncU; ++j) {
+      const int64_t idx = base + 64 * j;
+      v[j] = __builtin_nontemporal_load(w + (idx < nchunk ? idx : nchunk - 1));
+    }
+#pragma unroll
+    for (int j = 0; j < kEncU; ++j) {
+      const int64_t idx = base + 64 * j;
+      const float e[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+      uint32_t out = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float ax = __builtin_fabsf(e[q]);
+        uint32_t lo = 0;   // thresholds s_t[0 .. lo) are <= ax; the steps sum to 127
+#pragma unroll
+        for (int step = 64; step >= 1; step >>= 1)
+          if (s_t[lo + step - 1] <= ax) lo += step;
+        const uint32_t sgn = (e[q] < 0.0f && lo != 0u) ? 128u : 0u;
+        out |= (lo | sgn) << (8 * q);
+      }
+      if (idx < nchunk) codes[idx] = out;
+    }
+  }
+}
+
+struct Codebook256 { float v[256]; };
+
+// Dequantize 8-bit codes: four codes per thread and step, one 16-byte store.
+__global__ __launch_bounds__(256) void k_dequant8(const uint32_t* __restrict__ codes,
+                                                  f32x4* __restrict__ w, int64_t nwords,
+                                                  Codebook256 cb) {
+  __shared__ float s_cb[256];
+  s_cb[threadIdx.x] = cb.v[threadIdx.x];
+  __syncthreads();
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nwords; i += stride) {
+    const uint32_t c = codes[i];
+    f32x4 a;
+    a.x = s_cb[c & 255u]; a.y = s_cb[(c >> 8) & 255u];
+    a.z = s_cb[(c >> 16) & 255u]; a.w = s_cb[c >> 24];
+    __builtin_nontemporal_store(a, w + i);
+  }
+}
+
 __global__ __launch_bounds__(256) void k_fill_zero(float* __restrict__ y, int64_t count) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
@@ -174,6 +239,39 @@ __device__ __forceinline__ uint32_t pair_lookup(const uint32_t* s_lut, uint32_t 
 
 __device__ __forceinline__ half2v as_half2(uint32_t u) { return __builtin_bit_cast(half2v, u); }
 
+// 8-bit codes: LDS word (e * 64 + lane) = f16(lut[e]) in its low half, one private copy per
+// lane as for the pair table. Vector v of the fill holds entry v / 16; entry e is half e % 2
+// of lut.h[e / 2] (kernel-argument memory, read with a divergent index).
+template <int THREADS>
+__device__ __forceinline__ void fill_single_lut(uint32_t* s_lut, const Lut256& lut) {
+  constexpr int kVecs = kLutWords / 4;
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < kVecs / THREADS; ++i) {
+    const uint32_t e = (uint32_t)(t + THREADS * i) >> 4;
+    const uint32_t w = lut.h[e >> 1];
+    const u32x4 vv = (e & 1u) ? (w >> 16) : (w & 0xFFFFu);
+    *reinterpret_cast<u32x4*>(s_lut + 4 * (t + THREADS * i)) = vv;
+  }
+}
+
+template <int BITS, int THREADS>
+__device__ __forceinline__ void fill_lut(uint32_t* s_lut, const typename LutOf<BITS>::type& lut) {
+  if constexpr (BITS == 4) fill_pair_lut<THREADS>(s_lut, lut);
+  else fill_single_lut<THREADS>(s_lut, lut);
+}
+
+// The float16 pair of 8-bit codes at bytes 2p and 2p + 1 (p = 0, 1) of code dword `d`.
+__device__ __forceinline__ uint32_t single_pair(const uint32_t* s_lut, uint32_t d,
+                                                uint32_t laneoff, int p) {
+  const char* base = reinterpret_cast<const char*>(s_lut);
+  const uint32_t a0 = __builtin_amdgcn_perm(d, laneoff, 0x0C0C0000u | ((uint32_t)(4 + 2 * p) << 8));
+  const uint32_t a1 = __builtin_amdgcn_perm(d, laneoff, 0x0C0C0000u | ((uint32_t)(5 + 2 * p) << 8));
+  const uint32_t lo = *reinterpret_cast<const uint16_t*>(base + a0);
+  const uint32_t hi = *reinterpret_cast<const uint16_t*>(base + a1);
+  return lo | (hi << 16);
+}
+
 template <int CTRL, int ROW_MASK = 0xF>
 __device__ __forceinline__ float dpp_f(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
@@ -224,6 +322,7 @@ constexpr int kStageXBytes = 32768;   // activations staged through LDS when M *
 // fall on distinct LDS banks.
 constexpr int kStageXPadded = kStageXBytes / 64 * 80;
 
+template <int BITS>
 struct GemvSeg {
   const uint8_t* codes;
   float* y;
@@ -231,15 +330,21 @@ struct GemvSeg {
   int wg_begin;
   int iters;
   float scale;
-  Lut16 lut;
+  typename LutOf<BITS>::type lut;
 };
+template <int BITS>
 struct GemvSegs {
-  GemvSeg s[kMaxSegs];
+  GemvSeg<BITS> s[kMaxSegs];
   int count;
 };
 
-template <int M, int CPL>
-__device__ __forceinline__ void gemv_row(const u32x4 (&q)[CPL], const uint32_t (&xr)[M][CPL][16],
+// Weights per 16-byte code chunk and activation dwords (float16 pairs) per chunk.
+template <int BITS> constexpr int kChunkW = 128 / BITS;
+template <int BITS> constexpr int kChunkX = 64 / BITS;
+
+template <int BITS, int M, int CPL>
+__device__ __forceinline__ void gemv_row(const u32x4 (&q)[CPL],
+                                         const uint32_t (&xr)[M][CPL][kChunkX<BITS>],
                                          const uint32_t* s_lut, uint32_t laneoff,
                                          float (&acc)[M]) {
   float acc2[M];
@@ -249,24 +354,29 @@ __device__ __forceinline__ void gemv_row(const u32x4 (&q)[CPL], const uint32_t (
   for (int s = 0; s < CPL; ++s) {
     const uint32_t dw[4] = {q[s].x, q[s].y, q[s].z, q[s].w};
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 4; ++j) {
+      constexpr int P = BITS == 4 ? 4 : 2;   // float16 pairs per code dword
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const half2v wp = as_half2(pair_lookup(s_lut, dw[j], laneoff, i));
+      for (int i = 0; i < P; ++i) {
+        const half2v wp = as_half2(BITS == 4 ? pair_lookup(s_lut, dw[j], laneoff, i)
+                                             : single_pair(s_lut, dw[j], laneoff, i));
 #pragma unroll
         for (int m = 0; m < M; ++m) {
           float& a = (i & 1) ? acc2[m] : acc[m];
-          a = __builtin_amdgcn_fdot2(wp, as_half2(xr[m][s][4 * j + i]), a, false);
+          a = __builtin_amdgcn_fdot2(wp, as_half2(xr[m][s][P * j + i]), a, false);
         }
       }
+    }
   }
 #pragma unroll
   for (int m = 0; m < M; ++m) acc[m] += acc2[m];
 }
 
-template <int M, int CPL, bool SPLITK, int NBUF>
+template <int BITS, int M, int CPL, bool SPLITK, int NBUF>
 __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, int k_cols, int wk_arg,
-                                              int stage_x, GemvSegs segs) {
+                                              int stage_x, GemvSegs<BITS> segs) {
+  constexpr int CW = kChunkW<BITS>;   // weights per 16-byte code chunk
+  constexpr int CX = kChunkX<BITS>;   // activation dwords per chunk
   const int wk = SPLITK ? wk_arg : 1;
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[kLutWords];
   __shared__ __attribute__((aligned(16))) uint32_t s_x[kStageXPadded / 4];
@@ -291,8 +401,8 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
   const int kw = wave % wk;
   const int grp = wave / wk;
   const int groups = 8 / wk;
-  const int nchunks = k_cols >> 5;
-  const int64_t row_bytes = (int64_t)(k_cols >> 1);
+  const int nchunks = k_cols / CW;
+  const int64_t row_bytes = (int64_t)k_cols * BITS / 8;
   const int total_groups = (next_begin - wg_begin) * groups;
   const int gid = (bid - wg_begin) * groups + grp;
   const uint32_t laneoff = (uint32_t)lane << 2;
@@ -333,9 +443,9 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
     }
   }
   load_row(0, q[0]);
-  fill_pair_lut<512>(s_lut, segs.s[si].lut);
+  fill_lut<BITS, 512>(s_lut, segs.s[si].lut);
 
-  uint32_t xr[M][CPL][16];
+  uint32_t xr[M][CPL][CX];
   if (stage_x) {
 #pragma unroll
     for (int v = 0; v < kXVec; ++v) {
@@ -349,8 +459,8 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
 #pragma unroll
       for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int qi = 0; qi < 4; ++qi) {
-          const int vi = ((m * k_cols + c * 32) >> 3) + qi;    // 16-byte vector index
+        for (int qi = 0; qi < CX / 4; ++qi) {
+          const int vi = ((m * k_cols + c * CW) >> 3) + qi;    // 16-byte vector index
           u32x4 v = *reinterpret_cast<const u32x4*>(s_x + 4 * (vi + (vi >> 2)));
           if (!cval[s]) v = 0;
           xr[m][s][4 * qi] = v.x; xr[m][s][4 * qi + 1] = v.y;
@@ -364,9 +474,9 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
 #pragma unroll
       for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int qi = 0; qi < 4; ++qi) {
+        for (int qi = 0; qi < CX / 4; ++qi) {
           u32x4 v = 0;
-          if (cval[s]) v = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k_cols + (int64_t)c * 32 + 8 * qi);
+          if (cval[s]) v = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k_cols + (int64_t)c * CW + 8 * qi);
           xr[m][s][4 * qi] = v.x; xr[m][s][4 * qi + 1] = v.y;
           xr[m][s][4 * qi + 2] = v.z; xr[m][s][4 * qi + 3] = v.w;
         }
@@ -409,14 +519,14 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
 #pragma unroll
     for (int b = 0; b < NBUF; ++b) {
       load_row(it + b + NBUF - 1, q[(b + NBUF - 1) % NBUF]);
-      gemv_row<M, CPL>(q[b], xr, s_lut, laneoff, acc);
+      gemv_row<BITS, M, CPL>(q[b], xr, s_lut, laneoff, acc);
       finish_row(it + b, acc);
     }
   }
 #pragma unroll
   for (int b = 0; b + 1 < NBUF; ++b) {
     if (it + b < iters) {
-      gemv_row<M, CPL>(q[b], xr, s_lut, laneoff, acc);
+      gemv_row<BITS, M, CPL>(q[b], xr, s_lut, laneoff, acc);
       finish_row(it + b, acc);
     }
   }
@@ -446,7 +556,6 @@ struct LutBytes { uint32_t lo0, lo1, hi0, hi1; };   // float16 bytes of magnitud
 
 constexpr int kM2Step = 256;
 constexpr int kM2Pad = kM2Step + 8;   // halves per staged activation row
-constexpr int kM2TPitch = 144;        // bytes per row of a wavefront's code transpose buffer
 
 __device__ __forceinline__ void dequant_dword(uint32_t w, const LutBytes& t, uint32_t (&o)[4]) {
   const uint32_t me = w & 0x07070707u;            // magnitudes of k0 k2 k4 k6
@@ -490,16 +599,21 @@ __device__ __forceinline__ int x_unit(int r, int u) { return (u + 8 * ((r >> 3) 
 // with that step's codes, STAGES - 1 steps ahead: vector loads complete in issue order, so an
 // activation load issued later than a code load would wait for it. COAL is used for MT <= 2,
 // where it measured 10-20 % faster; larger MT keep the first scheme.
-template <int MT, int STAGES, bool PAIRS, bool COAL>
+template <int BITS, int MT, int STAGES, bool PAIRS, bool COAL>
 __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes,
                                                const uint16_t* __restrict__ x,
                                                float* __restrict__ y, int n_rows, int k_cols,
-                                               int m_rows, LutBytes tb, Lut16 lut, float scale) {
+                                               int m_rows, LutBytes tb,
+                                               typename LutOf<BITS>::type lut, float scale) {
   static_assert(STAGES % 2 == 0, "the loop is unrolled by STAGES and alternates two tiles");
+  static_assert(BITS == 4 || PAIRS, "8-bit codes are dequantized through the LDS table");
+  constexpr int RB = 32 * BITS;          // code bytes of one row per step (256 k)
+  constexpr int CB = RB / 64;            // 16-byte pieces per lane per step
+  constexpr int TP = RB + 16;            // transpose buffer pitch (bytes)
   __shared__ __attribute__((aligned(16))) uint16_t s_x[2][MT * 16][kM2Pad];
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[PAIRS ? kLutWords : 4];
-  __shared__ __attribute__((aligned(16))) uint8_t s_ct[COAL ? 8 * 16 * kM2TPitch : 16];
-  if (PAIRS) fill_pair_lut<512>(s_lut, lut);
+  __shared__ __attribute__((aligned(16))) uint8_t s_ct[COAL ? 8 * 16 * TP : 16];
+  if (PAIRS) fill_lut<BITS, 512>(s_lut, lut);
   const uint32_t laneoff = (uint32_t)(threadIdx.x & 63) << 2;
 
   const int t = threadIdx.x;
@@ -510,7 +624,7 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
   const int n0 = blockIdx.x * 128 + wave * 16;
   const int mb = blockIdx.y * (MT * 16);
   const int nsteps = (k_cols + kM2Step - 1) / kM2Step;
-  const int64_t row_bytes = (int64_t)(k_cols >> 1);
+  const int64_t row_bytes = (int64_t)k_cols * BITS / 8;
   const int row = n0 + j;
   const GlobalU8 crow = (GlobalU8)codes + (int64_t)(row < n_rows ? row : n_rows - 1) * row_bytes;
 
@@ -540,42 +654,45 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
       *reinterpret_cast<u32x4*>(&s_x[slot][r][x_unit(r, idx & 31) * 8]) = w;
     }
   };
-  // Codes of a step: this lane's 32 bytes at [128 step + 32 g, +32) of row n0 + j (clamped into
-  // the row; a clamped chunk only meets zero activations). Without COAL they are loaded as two
-  // 16-byte pieces per lane; with COAL the wavefront loads its rows n0 .. n0 + 15 as two
-  // instructions of 8 rows x 128 bytes (lane l: row n0 + 8 c + l / 8, bytes 16 (l % 8)), and
+  // Codes of a step: this lane's RB / 4 bytes at [RB step + (RB / 4) g, +RB / 4) of row n0 + j
+  // (clamped into the row; a clamped chunk only meets zero activations), i.e. k in
+  // [256 step + 64 g, +64). Without COAL they are loaded as CB 16-byte pieces per lane; with
+  // COAL the wavefront loads its rows n0 .. n0 + 15 as CB instructions of RPI rows x RB
+  // contiguous bytes (lane l: row n0 + RPI c + l / (RB / 16), bytes 16 (l % (RB / 16))), and
   // lane_codes() redistributes them through the wavefront's LDS buffer.
-  auto load_codes = [&](int step, u32x4 (&q)[2]) {
+  constexpr int RPI = 1024 / RB;          // rows per coalesced instruction
+  auto load_codes = [&](int step, u32x4 (&q)[CB]) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
+    for (int c = 0; c < CB; ++c) {
       if (COAL) {
-        int r = n0 + 8 * c + (lane >> 3);
+        int r = n0 + RPI * c + lane / (RB / 16);
         r = r < n_rows ? r : n_rows - 1;
-        int64_t off = (int64_t)step * 128 + 16 * (lane & 7);
+        int64_t off = (int64_t)step * RB + 16 * (lane % (RB / 16));
         off = off + 16 <= row_bytes ? off : row_bytes - 16;
         q[c] = __builtin_nontemporal_load(
             (GlobalU32x4)((GlobalU8)codes + (int64_t)r * row_bytes + off));
       } else {
-        int64_t off = (int64_t)step * 128 + 32 * g + 16 * c;
+        int64_t off = (int64_t)step * RB + (RB / 4) * g + 16 * c;
         off = off + 16 <= row_bytes ? off : row_bytes - 16;
         q[c] = __builtin_nontemporal_load((GlobalU32x4)(crow + off));
       }
     }
   };
-  uint8_t* s_cw = s_ct + (COAL ? wave * 16 * kM2TPitch : 0);
-  auto lane_codes = [&](const u32x4 (&q)[2], u32x4 (&o)[2]) {
+  uint8_t* s_cw = s_ct + (COAL ? wave * 16 * TP : 0);
+  auto lane_codes = [&](const u32x4 (&q)[CB], u32x4 (&o)[CB]) {
     if (!COAL) {
-      o[0] = q[0]; o[1] = q[1];
+#pragma unroll
+      for (int c = 0; c < CB; ++c) o[c] = q[c];
       return;
     }
     // LDS operations of one wavefront complete in order, so the reads below see the writes.
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
-      *reinterpret_cast<u32x4*>(s_cw + (8 * c + (lane >> 3)) * kM2TPitch + 16 * (lane & 7)) = q[c];
+    for (int c = 0; c < CB; ++c)
+      *reinterpret_cast<u32x4*>(s_cw + (RPI * c + lane / (RB / 16)) * TP + 16 * (lane % (RB / 16))) = q[c];
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
-      o[c] = *reinterpret_cast<const u32x4*>(s_cw + j * kM2TPitch + 32 * g + 16 * c);
+    for (int c = 0; c < CB; ++c)
+      o[c] = *reinterpret_cast<const u32x4*>(s_cw + j * TP + (RB / 4) * g + 16 * c);
     __builtin_amdgcn_wave_barrier();
   };
 
@@ -591,7 +708,7 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
   // xr[t % STAGES] (XR = STAGES register sets), so waiting for it never waits for a code load
   // issued after an older tile.
   constexpr int XR = COAL ? STAGES : 2;
-  u32x4 q[STAGES][2];
+  u32x4 q[STAGES][CB];
   u32x4 xr[XR][MT];
   auto clampstep = [&](int t2) { return t2 < nsteps ? t2 : nsteps - 1; };
   if (COAL) {
@@ -618,28 +735,36 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
       if (COAL) load_x(clampstep(step + STAGES - 1), xr[(u + STAGES - 1) % XR]);
       else load_x(clampstep(step + 2), xr[u % XR]);
       load_codes(clampstep(step + STAGES - 1), q[(u + STAGES - 1) % STAGES]);
-      u32x4 qc[2];
+      u32x4 qc[CB];
       lane_codes(q[u], qc);
+      uint32_t dws[4 * CB];
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const uint32_t dws[4] = {qc[c].x, qc[c].y, qc[c].z, qc[c].w};
+      for (int c = 0; c < CB; ++c) {
+        dws[4 * c] = qc[c].x; dws[4 * c + 1] = qc[c].y;
+        dws[4 * c + 2] = qc[c].z; dws[4 * c + 3] = qc[c].w;
+      }
+      // MFMA d multiplies k = 256 step + 64 g + 8 d + 0..7: code dword d (4-bit) or dwords
+      // 2 d, 2 d + 1 (8-bit).
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int d = 4 * c + e;
-          uint32_t bw[4];
-          if (PAIRS) {
+      for (int d = 0; d < 8; ++d) {
+        uint32_t bw[4];
+        if (BITS == 8) {
+          bw[0] = single_pair(s_lut, dws[2 * d], laneoff, 0);
+          bw[1] = single_pair(s_lut, dws[2 * d], laneoff, 1);
+          bw[2] = single_pair(s_lut, dws[2 * d + 1], laneoff, 0);
+          bw[3] = single_pair(s_lut, dws[2 * d + 1], laneoff, 1);
+        } else if (PAIRS) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) bw[i] = pair_lookup(s_lut, dws[e], laneoff, i);
-          } else {
-            dequant_dword(dws[e], tb, bw);
-          }
-          const half8v b = __builtin_bit_cast(half8v, u32x4{bw[0], bw[1], bw[2], bw[3]});
+          for (int i = 0; i < 4; ++i) bw[i] = pair_lookup(s_lut, dws[d], laneoff, i);
+        } else {
+          dequant_dword(dws[d], tb, bw);
+        }
+        const half8v b = __builtin_bit_cast(half8v, u32x4{bw[0], bw[1], bw[2], bw[3]});
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            const half8v a = *reinterpret_cast<const half8v*>(
-                &s_x[u & 1][mt * 16 + j][x_unit(j, 8 * g + d) * 8]);
-            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, acc[mt], 0, 0, 0);
-          }
+        for (int mt = 0; mt < MT; ++mt) {
+          const half8v a = *reinterpret_cast<const half8v*>(
+              &s_x[u & 1][mt * 16 + j][x_unit(j, 8 * g + d) * 8]);
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, acc[mt], 0, 0, 0);
         }
       }
       store_x(step + 1, (u + 1) & 1, xr[(u + 1) % XR]);
@@ -686,20 +811,26 @@ uint16_t f32_to_f16(float f) {
 }
 
 // float16 image of a codebook: lut16 = f16(cb / 2^e), scale = 2^e.
-void make_lut16(const float* cb, Lut16* lut, float* scale) {
+// float16 image of a 2^BITS-entry codebook, scaled by 2^-e so that the largest magnitude lies
+// in [2^14, 2^15); *scale = 2^e multiplies the results back (exactly).
+template <int BITS>
+void make_lut(const float* cb, typename LutOf<BITS>::type* lut, float* scale) {
+  constexpr int kN = 1 << BITS;
   float mx = 0.0f;
-  for (int i = 0; i < 16; ++i) mx = std::fmax(mx, std::fabs(cb[i]));
+  for (int i = 0; i < kN; ++i) mx = std::fmax(mx, std::fabs(cb[i]));
   int e = 0;
   if (mx > 0.0f) {
     int E;
     std::frexp(mx, &E);          // mx = f * 2^E, f in [0.5, 1)
     e = E - 15;                  // mx / 2^e in [2^14, 2^15)
   }
-  uint16_t h[16];
-  for (int i = 0; i < 16; ++i) h[i] = f32_to_f16(std::ldexp(cb[i], -e));
-  for (int i = 0; i < 8; ++i) lut->h[i] = (uint32_t)h[2 * i] | ((uint32_t)h[2 * i + 1] << 16);
+  for (int i = 0; i < kN / 2; ++i)
+    lut->h[i] = (uint32_t)f32_to_f16(std::ldexp(cb[2 * i], -e)) |
+                ((uint32_t)f32_to_f16(std::ldexp(cb[2 * i + 1], -e)) << 16);
   *scale = std::ldexp(1.0f, e);
 }
+
+void make_lut16(const float* cb, Lut16* lut, float* scale) { make_lut<4>(cb, lut, scale); }
 
 struct DeviceInfo { int cus = 0; };
 
@@ -730,22 +861,23 @@ int64_t grid_for(int64_t items, int64_t per_block, int64_t cap) {
   return g;
 }
 
-template <int M, int CPL>
+template <int BITS, int M, int CPL>
 void launch_gemv(int grid, hipStream_t st, const uint16_t* x, int k, int wk, int stage_x,
-                 const GemvSegs& segs) {
+                 const GemvSegs<BITS>& segs) {
   constexpr int NBUF = (CPL <= 2 && M <= 2) ? 3 : 2;
   if (wk == 1)
-    hipLaunchKernelGGL((k_gemv<M, CPL, false, NBUF>), dim3((unsigned)grid), dim3(512), 0, st, x,
-                       k, 1, stage_x, segs);
+    hipLaunchKernelGGL((k_gemv<BITS, M, CPL, false, NBUF>), dim3((unsigned)grid), dim3(512), 0,
+                       st, x, k, 1, stage_x, segs);
   else
-    hipLaunchKernelGGL((k_gemv<M, CPL, true, NBUF>), dim3((unsigned)grid), dim3(512), 0, st, x,
-                       k, wk, stage_x, segs);
+    hipLaunchKernelGGL((k_gemv<BITS, M, CPL, true, NBUF>), dim3((unsigned)grid), dim3(512), 0,
+                       st, x, k, wk, stage_x, segs);
 }
 
+template <int BITS>
 bool dispatch_gemv(int m, int cpl, int grid, hipStream_t st, const uint16_t* x, int k, int wk,
-                   int stage_x, const GemvSegs& segs) {
+                   int stage_x, const GemvSegs<BITS>& segs) {
 #define LOGBQ_G(MM, CC) \
-  if (m == MM && cpl == CC) { launch_gemv<MM, CC>(grid, st, x, k, wk, stage_x, segs); return true; }
+  if (m == MM && cpl == CC) { launch_gemv<BITS, MM, CC>(grid, st, x, k, wk, stage_x, segs); return true; }
   LOGBQ_G(1, 1) LOGBQ_G(1, 2) LOGBQ_G(1, 3) LOGBQ_G(1, 4) LOGBQ_G(1, 5) LOGBQ_G(1, 6) LOGBQ_G(1, 7) LOGBQ_G(1, 8)
   LOGBQ_G(2, 1) LOGBQ_G(2, 2) LOGBQ_G(2, 3) LOGBQ_G(2, 4)
   LOGBQ_G(3, 1) LOGBQ_G(3, 2)
@@ -755,17 +887,18 @@ bool dispatch_gemv(int m, int cpl, int grid, hipStream_t st, const uint16_t* x, 
   return false;
 }
 
-// GEMV configuration for m batch rows and k columns: WK wavefronts per row and CPL chunks per
-// lane, keeping the activations at most 8 x 16 registers per lane. Returns false when even
-// WK = 8 does not fit (the MFMA path takes those shapes).
+// GEMV configuration for m batch rows and k columns of BITS-bit codes: WK wavefronts per row
+// and CPL 16-byte code chunks per lane, keeping at most 8 / m chunks of activations per lane.
+// Returns false when even WK = 8 does not fit (the MFMA path takes those shapes).
+template <int BITS>
 bool gemv_config(int m, int k, int* wk, int* cpl) {
   if (m < 1 || m > 8) return false;
-  const int nchunks = k / 32;
+  const int nchunks = k / kChunkW<BITS>;
   const int cplmax = 8 / m;
   for (int w = 1; w <= 8; w *= 2) {
     const int per = (nchunks + 64 * w - 1) / (64 * w);
-    // The split-row kernels keep at most 7 chunks per lane (8 would spill registers).
-    const int cap = (w == 1 || cplmax < 7) ? cplmax : 7;
+    // The split-row 4-bit kernels keep at most 7 chunks per lane (8 would spill registers).
+    const int cap = (w == 1 || cplmax < 7 || BITS == 8) ? cplmax : 7;
     if (per <= cap && (w == 1 || nchunks >= 32 * w)) {
       *wk = w;
       *cpl = per < 1 ? 1 : per;
@@ -782,10 +915,10 @@ struct LinearJob {
   float* y;
 };
 
-int32_t validate_job(const LinearJob& j, int64_t m, int64_t k) {
+int32_t validate_job(const LinearJob& j, int64_t m, int64_t k, int entries = 16) {
   if (!j.codebook || j.n < 0) return LOGBQ_ERR_INVALID_ARG;
   if (j.n > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
-  for (int i = 0; i < 16; ++i)
+  for (int i = 0; i < entries; ++i)
     if (!std::isfinite(j.codebook[i])) return LOGBQ_ERR_INVALID_ARG;
   if (m == 0 || j.n == 0) return LOGBQ_OK;
   if (!j.y) return LOGBQ_ERR_INVALID_ARG;
@@ -820,37 +953,49 @@ bool make_lut_bytes(const float* cb, LutBytes* tb, float* scale) {
 // Largest batch: the MFMA grid's y dimension (at most 65535) covers 64 batch rows or more each.
 constexpr int64_t kMaxBatchRows = 65535LL * 64;
 
+template <int BITS>
 int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st) {
   const int N = (int)j.n;
   LutBytes tb = {0, 0, 0, 0};
-  Lut16 lut;
+  typename LutOf<BITS>::type lut;
   float scale;
-  // Register dequantization needs a sign-symmetric codebook (every fitted one is); any other
-  // codebook uses the LDS pair table with at most 4 batch tiles per workgroup column.
-  const bool symmetric = make_lut_bytes(j.codebook, &tb, &scale);
-  make_lut16(j.codebook, &lut, &scale);
+  // 4-bit codes: register dequantization needs a sign-symmetric codebook (every fitted one
+  // is); any other codebook, and every 8-bit one, uses the LDS table with at most 4 batch tiles
+  // per workgroup column.
+  const bool symmetric = BITS == 4 && make_lut_bytes(j.codebook, &tb, &scale);
+  make_lut<BITS>(j.codebook, &lut, &scale);
   // Batch tiles of 16 rows: up to 8 per workgroup column (128 rows). Up to 4 tiles use the
-  // LDS pair table; more tiles leave LDS to the activation ring and dequantize in registers.
+  // LDS table; more tiles leave LDS to the activation ring and dequantize in registers.
   int mt16 = (M + 15) / 16;
   const int cap = symmetric ? 8 : 4;
   if (mt16 > cap) mt16 = cap;
   dim3 grid((unsigned)((N + 127) / 128), (unsigned)((M + 16 * mt16 - 1) / (16 * mt16)));
-#define LOGBQ_M2(MT, ST, PR) hipLaunchKernelGGL((k_mfma2<MT, ST, PR, (MT <= 2)>), grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
-  switch (mt16) {
-    case 1: LOGBQ_M2(1, 4, true); break;
-    case 2: LOGBQ_M2(2, 4, true); break;
-    case 3: LOGBQ_M2(3, 4, true); break;
-    case 4: LOGBQ_M2(4, 4, true); break;
-    case 5: LOGBQ_M2(5, 4, false); break;
-    case 6: LOGBQ_M2(6, 4, false); break;
-    case 7: LOGBQ_M2(7, 4, false); break;
-    default: LOGBQ_M2(8, 4, false); break;
+#define LOGBQ_M2(MT, ST, PR) hipLaunchKernelGGL((k_mfma2<BITS, MT, ST, PR, (MT <= 2)>), grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
+  if constexpr (BITS == 4) {
+    switch (mt16) {
+      case 1: LOGBQ_M2(1, 4, true); break;
+      case 2: LOGBQ_M2(2, 4, true); break;
+      case 3: LOGBQ_M2(3, 4, true); break;
+      case 4: LOGBQ_M2(4, 4, true); break;
+      case 5: LOGBQ_M2(5, 4, false); break;
+      case 6: LOGBQ_M2(6, 4, false); break;
+      case 7: LOGBQ_M2(7, 4, false); break;
+      default: LOGBQ_M2(8, 4, false); break;
+    }
+  } else {
+    switch (mt16) {
+      case 1: LOGBQ_M2(1, 4, true); break;
+      case 2: LOGBQ_M2(2, 4, true); break;
+      case 3: LOGBQ_M2(3, 4, true); break;
+      default: LOGBQ_M2(4, 4, true); break;
+    }
   }
 #undef LOGBQ_M2
   return launch_status();
 }
 
 // y_i = x . W_hat_i^T for up to kMaxSegs linears sharing x (validated by the caller).
+template <int BITS>
 int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jobs, int count,
                     hipStream_t st) {
   int live[kMaxSegs];
@@ -878,7 +1023,7 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
   // takes everything else up to m = 8. The choice depends only on (m, k, N), so every linear of
   // a grouped call runs the kernel that a single call would run, with the same result bits.
   int wk = 0, cpl = 0;
-  const bool gemv_ok = M <= 8 && gemv_config(M, K, &wk, &cpl);
+  const bool gemv_ok = M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl);
   int gl[kMaxSegs];
   int ng = 0;
   int64_t grows = 0;
@@ -888,13 +1033,13 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
       gl[ng++] = live[a];
       grows += j.n;
     } else {
-      const int32_t r = launch_mfma(x, M, K, j, st);
+      const int32_t r = launch_mfma<BITS>(x, M, K, j, st);
       if (r != LOGBQ_OK) return r;
     }
   }
   if (ng == 0) return LOGBQ_OK;
   const int groups = 8 / wk;
-  GemvSegs segs;
+  GemvSegs<BITS> segs;
   std::memset(&segs, 0, sizeof(segs));
   segs.count = ng;
   int begin = 0;
@@ -904,18 +1049,18 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
     int64_t share = (int64_t)((double)cus * (double)j.n / (double)grows + 0.5);
     if (share < 1) share = 1;
     if (share > need) share = need;
-    GemvSeg& sg = segs.s[a];
+    GemvSeg<BITS>& sg = segs.s[a];
     sg.codes = j.codes;
     sg.y = j.y;
     sg.n_rows = (int)j.n;
     sg.wg_begin = begin;
     const int64_t tg = share * groups;
     sg.iters = (int)((j.n + tg - 1) / tg);
-    make_lut16(j.codebook, &sg.lut, &sg.scale);
+    make_lut<BITS>(j.codebook, &sg.lut, &sg.scale);
     begin += (int)share;
   }
   const int stage_x = ((int64_t)M * K * 2 <= (int64_t)kStageXBytes) ? 1 : 0;
-  if (!dispatch_gemv(M, cpl, begin, st, x, K, wk, stage_x, segs)) return LOGBQ_ERR_UNSUPPORTED;
+  if (!dispatch_gemv<BITS>(M, cpl, begin, st, x, K, wk, stage_x, segs)) return LOGBQ_ERR_UNSUPPORTED;
   return launch_status();
 }
 
@@ -926,7 +1071,7 @@ extern "C" {
 int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_params* p,
                      uint8_t* codes_dev, float* codebook_out, void* stream) {
   if (!p || n < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
-  if (p->bits != 4) return LOGBQ_ERR_UNSUPPORTED;
+  if (p->bits != 4 && p->bits != 8) return LOGBQ_ERR_UNSUPPORTED;
   if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
   const int64_t numel = n * k;
   if (n != 0 && numel / n != k) return LOGBQ_ERR_UNSUPPORTED;
@@ -934,22 +1079,33 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
     if (!w_dev || !codes_dev) return LOGBQ_ERR_INVALID_ARG;
     if (!aligned16(w_dev) || !aligned16(codes_dev)) return LOGBQ_ERR_UNSUPPORTED;
   }
-  Thresholds th;
-  for (int i = 0; i < 7; ++i) {
-    th.t[i] = p->thresholds[i];
-    if (std::isnan(th.t[i]) || !(th.t[i] > 0.0f)) return LOGBQ_ERR_INVALID_ARG;
-    if (i > 0 && th.t[i] < th.t[i - 1]) return LOGBQ_ERR_INVALID_ARG;
+  const int qmax = (1 << (p->bits - 1)) - 1;
+  if (p->qmax != qmax) return LOGBQ_ERR_INVALID_ARG;
+  for (int i = 0; i < qmax; ++i) {
+    const float t = p->thresholds[i];
+    if (std::isnan(t) || !(t > 0.0f)) return LOGBQ_ERR_INVALID_ARG;
+    if (i > 0 && t < p->thresholds[i - 1]) return LOGBQ_ERR_INVALID_ARG;
   }
-  if (codebook_out) std::memcpy(codebook_out, p->codebook, sizeof(p->codebook));
+  if (codebook_out) std::memcpy(codebook_out, p->codebook, sizeof(float) << p->bits);
   if (numel == 0) return LOGBQ_OK;
   const int cus = device_cus();
   if (cus <= 0) return LOGBQ_ERR_HIP;
   const int64_t nchunk = numel / 4;
   // 32 workgroups (128 wavefronts) per CU: measured 4 % faster than 8 on the 8192x28672 tensor.
   const int64_t grid = grid_for(nchunk, 256 * kEncU, (int64_t)cus * 32);
-  hipLaunchKernelGGL(k_encode, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream,
-                     reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint16_t*>(codes_dev),
-                     nchunk, th);
+  if (p->bits == 4) {
+    Thresholds th;
+    for (int i = 0; i < 7; ++i) th.t[i] = p->thresholds[i];
+    hipLaunchKernelGGL(k_encode, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream,
+                       reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint16_t*>(codes_dev),
+                       nchunk, th);
+  } else {
+    Thresholds8 th;
+    for (int i = 0; i < 127; ++i) th.t[i] = p->thresholds[i];
+    hipLaunchKernelGGL(k_encode8, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream,
+                       reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint32_t*>(codes_dev),
+                       nchunk, th);
+  }
   return launch_status();
 }
 
@@ -987,7 +1143,7 @@ int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t*
     if (!x_dev) return LOGBQ_ERR_INVALID_ARG;
     if (!aligned16(x_dev)) return LOGBQ_ERR_UNSUPPORTED;
   }
-  return run_linears(x_dev, m, k, &j, 1, (hipStream_t)stream);
+  return run_linears<4>(x_dev, m, k, &j, 1, (hipStream_t)stream);
 }
 
 int32_t logbq_linear_multi(const uint16_t* x_dev, int64_t m, int64_t k, int32_t count,
@@ -1010,7 +1166,43 @@ int32_t logbq_linear_multi(const uint16_t* x_dev, int64_t m, int64_t k, int32_t 
     if (!x_dev) return LOGBQ_ERR_INVALID_ARG;
     if (!aligned16(x_dev)) return LOGBQ_ERR_UNSUPPORTED;
   }
-  return run_linears(x_dev, m, k, jobs, count, (hipStream_t)stream);
+  return run_linears<4>(x_dev, m, k, jobs, count, (hipStream_t)stream);
+}
+
+int32_t logbq_linear8(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
+                      int64_t n, const float* codebook, float* y_dev, void* stream) {
+  if (m < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
+  if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
+  if (m > kMaxBatchRows || k > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
+  LinearJob j{codes_dev, n, codebook, y_dev};
+  const int32_t v = validate_job(j, m, k, 256);
+  if (v != LOGBQ_OK) return v;
+  if (m == 0 || n == 0) return LOGBQ_OK;
+  if (k > 0) {
+    if (!x_dev) return LOGBQ_ERR_INVALID_ARG;
+    if (!aligned16(x_dev)) return LOGBQ_ERR_UNSUPPORTED;
+  }
+  return run_linears<8>(x_dev, m, k, &j, 1, (hipStream_t)stream);
+}
+
+int32_t logbq_dequantize8(const uint8_t* codes_dev, int64_t n, int64_t k, const float* codebook,
+                          float* w_dev, void* stream) {
+  if (!codebook || n < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
+  if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
+  const int64_t numel = n * k;
+  if (n != 0 && numel / n != k) return LOGBQ_ERR_UNSUPPORTED;
+  if (numel == 0) return LOGBQ_OK;
+  if (!codes_dev || !w_dev) return LOGBQ_ERR_INVALID_ARG;
+  if (!aligned16(codes_dev) || !aligned16(w_dev)) return LOGBQ_ERR_UNSUPPORTED;
+  const int cus = device_cus();
+  if (cus <= 0) return LOGBQ_ERR_HIP;
+  Codebook256 cb;
+  std::memcpy(cb.v, codebook, sizeof(cb.v));
+  const int64_t nwords = numel / 4;
+  hipLaunchKernelGGL(k_dequant8, dim3((unsigned)grid_for(nwords, 256, (int64_t)cus * 16)),
+                     dim3(256), 0, (hipStream_t)stream, reinterpret_cast<const uint32_t*>(codes_dev),
+                     reinterpret_cast<f32x4*>(w_dev), nwords, cb);
+  return launch_status();
 }
 
 }  // extern "C"

@@ -33,14 +33,16 @@ class Params(ctypes.Structure):
     _fields_ = [
         ("bits", c_int32), ("qmax", c_int32), ("eps", c_double), ("wmin", c_double),
         ("wmax", c_double), ("base", c_double), ("shift", c_int32), ("reserved", c_int32),
-        ("wmin_index", c_int64), ("codebook", c_float * 16), ("thresholds", c_float * 8),
+        ("wmin_index", c_int64), ("codebook", c_float * 256), ("thresholds", c_float * 128),
     ]
 
     def codebook_array(self) -> np.ndarray:
-        return np.ctypeslib.as_array(self.codebook).copy()
+        """The 2^bits codebook entries (16 for 4-bit, 256 for 8-bit codes)."""
+        return np.ctypeslib.as_array(self.codebook)[: 1 << self.bits].copy()
 
     def thresholds_array(self) -> np.ndarray:
-        return np.ctypeslib.as_array(self.thresholds).copy()
+        """thresholds[0 .. qmax - 1] followed by +inf padding up to 2^(bits-1) entries."""
+        return np.ctypeslib.as_array(self.thresholds)[: 1 << (self.bits - 1)].copy()
 
 
 _lib = None
@@ -58,7 +60,13 @@ SIGNATURES = {
     "logbq_linear_multi": (c_int32, [c_void_p, c_int64, c_int64, c_int32, POINTER(c_void_p),
                                      POINTER(c_int64), POINTER(POINTER(c_float)),
                                      POINTER(c_void_p), c_void_p]),
+    "logbq_linear8": (c_int32, [c_void_p, c_int64, c_int64, c_void_p, c_int64, POINTER(c_float),
+                                c_void_p, c_void_p]),
+    "logbq_dequantize8": (c_int32, [c_void_p, c_int64, c_int64, POINTER(c_float), c_void_p,
+                                    c_void_p]),
 }
+
+ABI_VERSION = 2
 
 
 def lib() -> ctypes.CDLL:
@@ -73,6 +81,9 @@ def lib() -> ctypes.CDLL:
             fn = getattr(h, name)
             fn.restype = res
             fn.argtypes = args
+        if h.logbq_abi_version() != ABI_VERSION:
+            raise LogbqUnavailable(f"{LIB_PATH} has ABI {h.logbq_abi_version()}, "
+                                   f"the binding expects {ABI_VERSION}; rebuild it")
         _lib = h
     return _lib
 
@@ -95,12 +106,14 @@ def _stream(stream):
     return c_void_p(stream.cuda_stream)
 
 
-def _cb_ptr(codebook):
+def _cb_ptr(codebook, entries=16):
     if isinstance(codebook, Params):
+        if (1 << codebook.bits) != entries:
+            raise ValueError(f"parameters of a {codebook.bits}-bit fit, call needs {entries} entries")
         return codebook.codebook, codebook
     arr = np.ascontiguousarray(np.asarray(codebook, dtype=np.float32))
-    if arr.shape != (16,):
-        raise ValueError("codebook must hold 16 float32 values")
+    if arr.shape != (entries,):
+        raise ValueError(f"codebook must hold {entries} float32 values")
     return arr.ctypes.data_as(POINTER(c_float)), arr
 
 
@@ -116,14 +129,18 @@ def fit(w, bits: int = 4, eps: float = 4e-3) -> Params:
 
 
 def encode(w, p: Params, out=None, stream=None):
-    """logbq_encode: float32 [N][K] device tensor -> (uint8 [N][K/2] codes, float32[16])."""
+    """logbq_encode: float32 [N][K] device tensor -> (uint8 codes, float32 codebook).
+
+    Codes are [N][K/2] for a 4-bit fit, [N][K] for an 8-bit one; the codebook has 2^bits
+    entries."""
     import torch
     if w.dtype != torch.float32 or w.dim() != 2 or not w.is_contiguous():
         raise ValueError("w must be a contiguous 2-D float32 device tensor")
     n, k = w.shape
     if out is None:
-        out = torch.empty((n, k // 2), dtype=torch.uint8, device=w.device)
-    cb = np.zeros(16, dtype=np.float32)
+        cols = k // 2 if p.bits == 4 else k
+        out = torch.empty((n, cols), dtype=torch.uint8, device=w.device)
+    cb = np.zeros(1 << p.bits, dtype=np.float32)
     _check(lib().logbq_encode(c_void_p(w.data_ptr()), n, k, ctypes.byref(p),
                               c_void_p(out.data_ptr()), cb.ctypes.data_as(POINTER(c_float)),
                               _stream(stream)), "logbq_encode")
@@ -186,4 +203,37 @@ def dequantize(codes, codebook, out=None, stream=None):
     cbp, _keep = _cb_ptr(codebook)
     _check(lib().logbq_dequantize(c_void_p(codes.data_ptr()), n, k, cbp, c_void_p(out.data_ptr()),
                                   _stream(stream)), "logbq_dequantize")
+    return out
+
+
+def linear8(x, codes, codebook, out=None, stream=None):
+    """logbq_linear8: y[M][N] = x[M][K] . W_hat^T on 8-bit codes [N][K] (x float16, y float32)."""
+    import torch
+    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous 2-D float16 device tensor")
+    if codes.dtype != torch.uint8 or codes.dim() != 2 or not codes.is_contiguous():
+        raise ValueError("codes must be a contiguous 2-D uint8 device tensor")
+    m, k = x.shape
+    n = codes.shape[0]
+    if codes.shape[1] != k:
+        raise ValueError("8-bit codes must be [N][K]")
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=x.device)
+    cbp, _keep = _cb_ptr(codebook, 256)
+    _check(lib().logbq_linear8(c_void_p(x.data_ptr()), m, k, c_void_p(codes.data_ptr()), n, cbp,
+                               c_void_p(out.data_ptr()), _stream(stream)), "logbq_linear8")
+    return out
+
+
+def dequantize8(codes, codebook, out=None, stream=None):
+    """logbq_dequantize8: uint8 [N][K] 8-bit codes -> float32 [N][K], bit-exact lookup."""
+    import torch
+    if codes.dtype != torch.uint8 or codes.dim() != 2 or not codes.is_contiguous():
+        raise ValueError("codes must be a contiguous 2-D uint8 device tensor")
+    n, k = codes.shape
+    if out is None:
+        out = torch.empty((n, k), dtype=torch.float32, device=codes.device)
+    cbp, _keep = _cb_ptr(codebook, 256)
+    _check(lib().logbq_dequantize8(c_void_p(codes.data_ptr()), n, k, cbp, c_void_p(out.data_ptr()),
+                                   _stream(stream)), "logbq_dequantize8")
     return out

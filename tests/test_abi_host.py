@@ -23,12 +23,13 @@ def header_functions():
 
 def test_library_exports_every_declared_symbol():
     names = header_functions()
-    assert {"logbq_fit", "logbq_encode", "logbq_linear", "logbq_dequantize",
-            "logbq_status_str", "logbq_abi_version"} <= set(names)
+    assert {"logbq_fit", "logbq_encode", "logbq_linear", "logbq_dequantize", "logbq_linear8",
+            "logbq_dequantize8", "logbq_status_str", "logbq_abi_version"} <= set(names)
     h = L.lib()
     for n in names:
         assert hasattr(h, n), n
-    assert h.logbq_abi_version() == 1
+    assert h.logbq_abi_version() == 2
+    assert ctypes.sizeof(L.Params) == 4 + 4 + 8 * 4 + 4 + 4 + 8 + 4 * 256 + 4 * 128
     for s in range(6):
         assert L.status_str(s)
     assert L.status_str(99) == "unknown status"
@@ -76,7 +77,9 @@ def test_encode_and_dequant_validation_before_hip():
     assert h.logbq_encode(None, 4, 64, ctypes.byref(p), a, None, None) == L.ERR_INVALID_ARG
     assert h.logbq_encode(P(4097), 4, 64, ctypes.byref(p), a, None, None) == L.ERR_UNSUPPORTED
     q = L.Params.from_buffer_copy(p)
-    q.bits = 8
+    q.bits = 8                                                  # q_max still 7
+    assert h.logbq_encode(a, 4, 64, ctypes.byref(q), a, None, None) == L.ERR_INVALID_ARG
+    q.bits = 5
     assert h.logbq_encode(a, 4, 64, ctypes.byref(q), a, None, None) == L.ERR_UNSUPPORTED
     q = L.Params.from_buffer_copy(p)
     q.thresholds[2] = q.thresholds[1] / 2                      # not sorted
@@ -84,7 +87,7 @@ def test_encode_and_dequant_validation_before_hip():
     cb = (ctypes.c_float * 16)()
     out = (ctypes.c_float * 16)()
     assert h.logbq_encode(None, 0, 64, ctypes.byref(p), None, out, None) == L.OK
-    assert list(out) == list(p.codebook)
+    assert list(out) == list(p.codebook)[:16]
     assert h.logbq_dequantize(a, 4, 64, None, a, None) == L.ERR_INVALID_ARG
     assert h.logbq_dequantize(a, 4, 33, cb, a, None) == L.ERR_UNSUPPORTED
     assert h.logbq_dequantize(None, 4, 64, cb, a, None) == L.ERR_INVALID_ARG
@@ -110,26 +113,29 @@ def test_fit_errors_match_oracle():
         with pytest.raises(L.LogbqError) as e:
             L.fit(np.array([0.5, 1.0], dtype=np.float32), eps=eps)
         assert e.value.status == L.ERR_INVALID_ARG
-    with pytest.raises(L.LogbqError) as e:
-        L.fit(np.array([0.5, 1.0], dtype=np.float32), bits=8)
-    assert e.value.status == L.ERR_UNSUPPORTED
+    for bits in (2, 3, 5, 16):
+        with pytest.raises(L.LogbqError) as e:
+            L.fit(np.array([0.5, 1.0], dtype=np.float32), bits=bits)
+        assert e.value.status == L.ERR_UNSUPPORTED
     h = L.lib()
     assert h.logbq_fit(None, 4, 4, 4e-3, ctypes.byref(L.Params())) == L.ERR_INVALID_ARG
 
 
-def _assert_fit_equal(w, eps=4e-3):
-    p = L.fit(w, 4, eps)
-    r = O.fit(w, 4, eps)
-    assert p.bits == 4 and p.qmax == 7 and p.eps == eps
+def _assert_fit_equal(w, eps=4e-3, bits=4):
+    p = L.fit(w, bits, eps)
+    r = O.fit(w, bits, eps)
+    q = 2 ** (bits - 1) - 1
+    assert p.bits == bits and p.qmax == q and p.eps == eps
     assert p.wmin == r.wmin and p.wmax == r.wmax
     assert p.wmin_index == r.wmin_index
     assert p.base == r.base, (p.base, r.base)
     assert p.shift == r.shift
     assert p.codebook_array().view(np.uint32).tolist() == \
-        O.codebook(r.base, r.shift).view(np.uint32).tolist()
-    assert p.thresholds_array()[:7].view(np.uint32).tolist() == \
-        O.magnitude_thresholds(r.base, r.shift).view(np.uint32).tolist()
-    assert np.isinf(p.thresholds[7])
+        O.codebook(r.base, r.shift, bits).view(np.uint32).tolist()
+    assert p.thresholds_array()[:q].view(np.uint32).tolist() == \
+        O.magnitude_thresholds(r.base, r.shift, bits).view(np.uint32).tolist()
+    assert all(np.isinf(p.thresholds[i]) for i in range(q, 128))
+    assert all(p.codebook[i] == 0.0 for i in range(2 ** bits, 256))
     return p
 
 
@@ -182,3 +188,45 @@ def test_fit_bit_exact_workload_tensors(name):
     w = inputs.student_t_weights(lin.n, lin.k, wl["nu"], wl["scale"],
                                  seed=[wl["cfg"], 0, 0, 0], outlier_frac=wl["outlier_frac"])
     _assert_fit_equal(w)
+
+
+def test_fit8_bit_exact_random():
+    """The 8-bit fit (q_max = 127, eps = 1e-6 as in Sec. 3.2) equals the oracle bit for bit:
+    w_min, w_max, b, s, all 256 codebook entries and all 127 exact thresholds."""
+    rng = np.random.default_rng(808)
+    done = 0
+    for i in range(16):
+        n = int(rng.integers(64, 20000))
+        w = (rng.standard_t([3, 4, 8][i % 3], size=n) * 10 ** rng.uniform(-5, 1)).astype(np.float32)
+        eps = [1e-6, 1e-3, 0.05][i % 3]
+        try:
+            O.fit(w, 8, eps)
+        except O.OracleError:
+            continue
+        _assert_fit_equal(w, eps, bits=8)
+        done += 1
+    assert done >= 10
+
+
+def test_8bit_validation_before_hip():
+    h = L.lib()
+    cb = (ctypes.c_float * 256)(*([0.0] * 256))
+    a = P(4096)
+    assert h.logbq_linear8(a, 1, 64, a, 4, None, a, None) == L.ERR_INVALID_ARG
+    assert h.logbq_linear8(a, 1, 48, a, 4, cb, a, None) == L.ERR_UNSUPPORTED
+    assert h.logbq_linear8(a, 1, 64, a, 4, cb, None, None) == L.ERR_INVALID_ARG
+    assert h.logbq_linear8(P(4100), 1, 64, a, 4, cb, a, None) == L.ERR_UNSUPPORTED
+    bad = (ctypes.c_float * 256)(*([0.0] * 256))
+    bad[200] = float("inf")                     # an entry only an 8-bit call reads
+    assert h.logbq_linear8(a, 1, 64, a, 4, bad, a, None) == L.ERR_INVALID_ARG
+    assert h.logbq_linear8(None, 0, 64, None, 4, cb, None, None) == L.OK
+    assert h.logbq_dequantize8(a, 4, 64, None, a, None) == L.ERR_INVALID_ARG
+    assert h.logbq_dequantize8(a, 4, 48, cb, a, None) == L.ERR_UNSUPPORTED
+    assert h.logbq_dequantize8(None, 0, 64, cb, None, None) == L.OK
+    p = L.fit(np.array([0.1, -0.5, 0.25, 1.0] * 8, dtype=np.float32), bits=8)
+    assert p.bits == 8 and p.qmax == 127
+    out = (ctypes.c_float * 256)()
+    assert h.logbq_encode(None, 0, 64, ctypes.byref(p), None, out, None) == L.OK
+    assert list(out) == list(p.codebook)
+    p.bits = 6
+    assert h.logbq_encode(a, 1, 64, ctypes.byref(p), a, None, None) == L.ERR_UNSUPPORTED
