@@ -19,8 +19,12 @@ READ_LIB = os.path.join(HERE, "libhbmread.so")
 ARCH = os.environ.get("LOGBQ_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+# The GEMV hands out rows with a one-lane LDS atomic whose result it reads only after the next
+# row's products; the atomic optimizer would rewrite that atomic into a wavefront-wide one that
+# reads its result at once, stalling the wavefront on the LDS round trip.
 HIP_FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-I", INCLUDE,
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
              "-Wall", "-Wno-unused-function"]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-fast-math", "-Wall",
               "-I", INCLUDE]

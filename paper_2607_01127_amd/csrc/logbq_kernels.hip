@@ -241,16 +241,22 @@ __device__ __forceinline__ half2v as_half2(uint32_t u) { return __builtin_bit_ca
 
 // 8-bit codes: LDS word (e * 64 + lane) = f16(lut[e]) in its low half, one private copy per
 // lane as for the pair table. Vector v of the fill holds entry v / 16; entry e is half e % 2
-// of lut.h[e / 2] (kernel-argument memory, read with a divergent index).
+// of lut.h[e / 2]. For thread t = 64 w + l, e / 2 = 2 w + l / 32 + (THREADS / 32) i takes two
+// values per wavefront, both read with uniform (scalar) loads of the kernel arguments: a load
+// with a per-lane index would be a vector load that waits behind the code loads in flight.
 template <int THREADS>
 __device__ __forceinline__ void fill_single_lut(uint32_t* s_lut, const Lut256& lut) {
   constexpr int kVecs = kLutWords / 4;
   const int t = threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const bool upper = (t & 32) != 0;
+  const bool hi_half = (t & 16) != 0;
 #pragma unroll
   for (int i = 0; i < kVecs / THREADS; ++i) {
-    const uint32_t e = (uint32_t)(t + THREADS * i) >> 4;
-    const uint32_t w = lut.h[e >> 1];
-    const u32x4 vv = (e & 1u) ? (w >> 16) : (w & 0xFFFFu);
+    const int j = 2 * w + (THREADS / 32) * i;      // uniform
+    const uint32_t h0 = lut.h[j], h1 = lut.h[j + 1];
+    const uint32_t word = upper ? h1 : h0;
+    const u32x4 vv = hi_half ? (word >> 16) : (word & 0xFFFFu);
     *reinterpret_cast<u32x4*>(s_lut + 4 * (t + THREADS * i)) = vv;
   }
 }
@@ -298,9 +304,8 @@ __device__ __forceinline__ float wave_sum(float v) {
 // and its own codes, codebook table and output.
 //
 // Work split inside a segment: a workgroup of 8 wavefronts holds one LDS pair table. WK
-// wavefronts share a row (each takes an interleaved slice of the row's 16-byte chunks); the
-// 8 / WK groups of a workgroup take rows round-robin with the other groups of the segment. Lane
-// `l` of wavefront `kw` in a group handles chunks c = s * 64 * WK + kw * 64 + l for s < CPL; its
+// wavefronts share a row (each takes an interleaved slice of the row's 16-byte chunks). Lane `l`
+// of wavefront `kw` in a group handles chunks c = s * 64 * WK + kw * 64 + l for s < CPL; its
 // activations for those chunks (M rows x 32 values each) stay in registers for the whole kernel.
 //
 // Codes are read with buffer loads through a resource descriptor built per row in scalar
@@ -308,13 +313,25 @@ __device__ __forceinline__ float wave_sum(float v) {
 // gets size 0, so its loads return zeros without touching memory. Chunk indices past the end of
 // a row are clamped into it and meet zero activations.
 //
+// Rows, WK = 1: workgroup g (counted from the segment's first) owns the rows
+// 8 g + t % 8 + (t / 8) * 8 G of its segment (G = the segment's workgroups), numbered by
+// tickets t = 0, 1, ... in that order, so at any moment the chip streams one band of about 8 G
+// consecutive rows. Wavefront w starts with tickets w, w + 8, ..., w + 8 (NBUF - 1) and takes
+// every further ticket from an LDS counter as it finishes a row: the eight wavefronts of a CU
+// share its rows dynamically and finish together (measured on MI355X: with fixed rows the
+// wavefronts of one CU finished 1.5 to 2 us apart). Results stay in lanes (lane i holds the
+// wavefront's i-th row) and are written 64 rows at a time, so no store waits among the code
+// loads of the row loop.
+// Rows, WK > 1: the 8 / WK groups of a workgroup take rows round-robin with the other groups
+// of the segment, and reduce each row through LDS.
+//
 // Start-up: x (when M * K * 2 <= 32 KiB) is requested first and staged once per workgroup
 // through LDS into registers; the first row of codes is requested next; the pair table is
-// written while both are in flight. The row loop keeps NBUF code buffers: while row it is
-// looked up, multiplied and reduced, rows it + 1 .. it + NBUF - 1 are in flight. Every load in
-// the loop is issued unconditionally, so the compiler waits for exactly the buffer it is about
-// to use. NBUF is 3 when a row slice is at most two chunks per lane (and m <= 2) and 2
-// otherwise: measured on MI355X, about 4 to 8 KiB of codes in flight per wavefront streams best.
+// written while both are in flight; the rest of the ring follows. The row loop keeps NBUF code buffers: while one row is
+// looked up, multiplied and reduced, the other NBUF - 1 are in flight. Every path through the
+// loop issues the same loads, so the compiler waits for exactly the buffer it is about to use.
+// NBUF is 3 when a row slice is at most two chunks per lane (and m <= 2) and 2 otherwise:
+// measured on MI355X, about 4 to 8 KiB of codes in flight per wavefront streams best.
 constexpr int kMaxSegs = 4;
 constexpr int kStageXBytes = 32768;   // activations staged through LDS when M * K * 2 fits
 // Staged activations keep every 64-byte chunk (the 32 values one lane multiplies with one
@@ -381,6 +398,7 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[kLutWords];
   __shared__ __attribute__((aligned(16))) uint32_t s_x[kStageXPadded / 4];
   __shared__ float s_red[8][M];
+  __shared__ uint32_t s_ticket;
 
   // Segment of this workgroup: a uniform index, so its fields are scalar kernel-argument loads.
   const int bid = blockIdx.x;
@@ -416,8 +434,7 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
     coff[s] = (cval[s] ? c : nchunks - 1) * 16;
   }
 
-  auto load_row = [&](int it, u32x4 (&q)[CPL]) {
-    const int r = gid + it * total_groups;
+  auto load_row = [&](int r, u32x4 (&q)[CPL]) {
     const bool live = r < n_rows;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(codes + (live ? (int64_t)r * row_bytes : 0)), (short)0,
@@ -426,27 +443,52 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
     for (int s = 0; s < CPL; ++s)
       q[s] = __builtin_amdgcn_raw_buffer_load_b128(rs, coff[s], 0, kCachePolicyNT);
   };
+  // Row of ticket t of this workgroup (WK = 1).
+  const int wg_row0 = (bid - wg_begin) * 8;
+  auto ticket_row = [&](uint32_t t) {
+    return wg_row0 + (int)(t & 7u) + (int)(t >> 3) * total_groups;
+  };
 
   u32x4 q[NBUF][CPL];
+  int rq[NBUF];   // row held (or awaited) by buffer b; n_rows when none
 
   // Start-up, ordered so that the memory system is busy from the first cycle: the staged
   // activations are requested first (they return first), then the first row of codes; the
-  // pair table is written while both are in flight.
+  // pair table is written while both are in flight. With WK = 1 a lane holds at most 8 / M
+  // chunks, so M * K * 2 <= 8 * 64 * 32 * 2 bytes and x is always staged; only split rows may
+  // read x directly (after the pair table is written, which keeps their register use low).
   constexpr int kXVec = kStageXBytes / 16 / 512;     // 16-byte x vectors per thread
   u32x4 xv[kXVec];
   const int nvec = (M * k_cols) >> 3;                // 16-byte vectors of x
-  if (stage_x) {
+  const bool staged = !SPLITK || stage_x != 0;
+  if (staged) {
 #pragma unroll
     for (int v = 0; v < kXVec; ++v) {
       const int i = threadIdx.x + 512 * v;
       xv[v] = *reinterpret_cast<const u32x4*>(x + 8 * (int64_t)(i < nvec ? i : 0));
     }
   }
-  load_row(0, q[0]);
+  // The first row goes out at once; the other NBUF - 1 rows right after the pair table is
+  // written when the ring is three deep, after the barrier below when it is two deep (measured
+  // on MI355X: issuing every ring row at once makes the first row arrive later, so with one or
+  // two rows per wavefront both rows are computed after the last bytes land).
+  constexpr bool kRestAfterFill = NBUF >= 3;
+  if constexpr (!SPLITK) {
+#pragma unroll
+    for (int b = 0; b < NBUF; ++b) rq[b] = ticket_row((uint32_t)(wave + 8 * b));
+    load_row(rq[0], q[0]);
+    if (threadIdx.x == 0) s_ticket = 8 * NBUF;
+  } else {
+    load_row(gid, q[0]);
+  }
   fill_lut<BITS, 512>(s_lut, segs.s[si].lut);
+  if constexpr (!SPLITK && kRestAfterFill) {
+#pragma unroll
+    for (int b = 1; b < NBUF; ++b) load_row(rq[b], q[b]);
+  }
 
   uint32_t xr[M][CPL][CX];
-  if (stage_x) {
+  if (staged) {
 #pragma unroll
     for (int v = 0; v < kXVec; ++v) {
       const int i = threadIdx.x + 512 * v;
@@ -483,15 +525,60 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
     }
   }
 
-  auto finish_row = [&](int it, float (&acc)[M]) {
-    const int r = gid + it * total_groups;
-    if (!SPLITK) {
+  float acc[M];
+  __syncthreads();  // pair table and ticket counter ready (and, when staged, x read out of LDS)
+  if constexpr (!SPLITK && !kRestAfterFill) {
 #pragma unroll
-      for (int m = 0; m < M; ++m) {
-        const float t = wave_sum(acc[m]);
-        if (lane == 0 && r < n_rows) y[(int64_t)m * n_rows + r] = t * scale;
+    for (int b = 1; b < NBUF; ++b) load_row(rq[b], q[b]);
+  }
+
+  if constexpr (!SPLITK) {
+    float res[M];        // lane i: results of the wavefront's i-th held row
+    int res_row = n_rows;
+    int held = 0;
+#pragma unroll
+    for (int m = 0; m < M; ++m) res[m] = 0.0f;
+    auto flush = [&]() {
+      if (lane < held && res_row < n_rows) {
+#pragma unroll
+        for (int m = 0; m < M; ++m) y[(int64_t)m * n_rows + res_row] = res[m];
       }
-    } else {
+      held = 0;
+    };
+    // One slot: ask for the next ticket (when rows remain), compute the row in buffer b, then
+    // load the ticket's row into b. The ticket is read only after the row's products (the asm
+    // ties it to their sum): an earlier read would make the wavefront wait for the LDS lookups.
+    auto step = [&](int b) {
+      const int newest = rq[(b + NBUF - 1) % NBUF];
+      uint32_t tk = 0;
+      if (newest < n_rows && lane == 0)
+        tk = __hip_atomic_fetch_add(&s_ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      float dep = 0.0f;
+      if (rq[b] < n_rows) {
+        gemv_row<BITS, M, CPL>(q[b], xr, s_lut, laneoff, acc);
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+          const float t = wave_sum(acc[m]) * scale;
+          res[m] = (lane == held) ? t : res[m];
+          dep += t;
+        }
+        res_row = (lane == held) ? rq[b] : res_row;
+        if (++held == 64) flush();
+      }
+      uint32_t tks;
+      asm volatile("v_readfirstlane_b32 %0, %1" : "=s"(tks) : "v"(tk), "v"(dep));
+      rq[b] = newest < n_rows ? ticket_row(tks) : n_rows;
+      load_row(rq[b], q[b]);
+    };
+    // Rows come in increasing order, so once the oldest buffer holds no row, none does.
+    while (rq[0] < n_rows) {
+#pragma unroll
+      for (int b = 0; b < NBUF; ++b) step(b);
+    }
+    flush();
+  } else {
+    auto finish_row = [&](int it) {
+      const int r = gid + it * total_groups;
 #pragma unroll
       for (int m = 0; m < M; ++m) {
         const float t = wave_sum(acc[m]);
@@ -504,30 +591,25 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
         y[(int64_t)lane * n_rows + r] = t * scale;
       }
       __syncthreads();
+    };
+#pragma unroll
+    for (int b = 1; b + 1 < NBUF; ++b) load_row(gid + b * total_groups, q[b]);
+    // Invariant at the top of the loop: q[b] holds (or awaits) row it + b for b < NBUF - 1.
+    int it = 0;
+    for (; it + NBUF <= iters; it += NBUF) {
+#pragma unroll
+      for (int b = 0; b < NBUF; ++b) {
+        load_row(gid + (it + b + NBUF - 1) * total_groups, q[(b + NBUF - 1) % NBUF]);
+        gemv_row<BITS, M, CPL>(q[b], xr, s_lut, laneoff, acc);
+        finish_row(it + b);
+      }
     }
-  };
-
-  float acc[M];
-  __syncthreads();  // pair table ready (and, when staged, x read out of LDS)
-
 #pragma unroll
-  for (int b = 1; b + 1 < NBUF; ++b) load_row(b, q[b]);
-
-  // Invariant at the top of the loop: q[b] holds (or awaits) row it + b for b < NBUF - 1.
-  int it = 0;
-  for (; it + NBUF <= iters; it += NBUF) {
-#pragma unroll
-    for (int b = 0; b < NBUF; ++b) {
-      load_row(it + b + NBUF - 1, q[(b + NBUF - 1) % NBUF]);
-      gemv_row<BITS, M, CPL>(q[b], xr, s_lut, laneoff, acc);
-      finish_row(it + b, acc);
-    }
-  }
-#pragma unroll
-  for (int b = 0; b + 1 < NBUF; ++b) {
-    if (it + b < iters) {
-      gemv_row<BITS, M, CPL>(q[b], xr, s_lut, laneoff, acc);
-      finish_row(it + b, acc);
+    for (int b = 0; b + 1 < NBUF; ++b) {
+      if (it + b < iters) {
+        gemv_row<BITS, M, CPL>(q[b], xr, s_lut, laneoff, acc);
+        finish_row(it + b);
+      }
     }
   }
 }

@@ -169,7 +169,9 @@ def test_encode_every_float32(params):
 SHAPES = [(2048, 2048), (1000, 352), (37, 32), (512, 14336), (4096, 4096), (64, 8192), (8, 28672),
           # row counts that leave 1 or 2 rows after the last full group of the code-buffer
           # ring; a K whose rows are split over four wavefronts; 3 chunks per lane
-          (8197, 2048), (6145, 4096), (16, 32768), (3000, 6144)]
+          (8197, 2048), (6145, 4096), (16, 32768), (3000, 6144),
+          # more than 64 rows per wavefront (results are written 64 rows at a time)
+          (140001, 32)]
 BATCH = [1, 2, 3, 4, 5, 8, 9, 16, 17, 32, 33, 64, 100, 128, 129, 200]
 
 
