@@ -194,8 +194,8 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=Tr
             "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
             "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
             "algo_bytes": algo,
-            # the library's path rule: GEMV for m <= 8 unless m >= 3 and m * N >= 65536
-            "path": "gemv" if m <= 8 and not (m >= 3 and m * n >= 65536) else "mfma"}
+            # the library's path rule: GEMV for m <= 8 unless m >= 3 and m * N > 65536
+            "path": "gemv" if m <= 8 and not (m >= 3 and m * n > 65536) else "mfma"}
     return results, {"n": n, "k": k, "packed": packed, "copies": copies, "fit_s": fit_s,
                      "params": {"base": p.base, "shift": p.shift, "wmin": p.wmin,
                                 "wmax": p.wmax}}, codes, cb
@@ -241,7 +241,7 @@ def bench_layer8(torch, L, inputs, dev, stream, ms, steps, warmup):
             "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
             "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
             "algo_bytes": algo, "copies": copies,
-            "path": "gemv" if m <= 8 and not (m >= 3 and m * n >= 65536) else "mfma"}
+            "path": "gemv" if m <= 8 and not (m >= 3 and m * n > 65536) else "mfma"}
     del code_list, codes
     return results
 

@@ -119,7 +119,7 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  *               a common power-of-two scaling, exact in the result up to float16 rounding.
  *   y_dev     : device, [m][n] float32, written.
  * Accumulation is float32. The wavefront-reduced GEMV runs for m <= 8 unless m >= 3 and
- * m * n >= 65536; everything else (and shapes whose activations do not fit the GEMV's
+ * m * n > 65536; everything else (and shapes whose activations do not fit the GEMV's
  * registers) runs the dequantize-into-MFMA skinny GEMM.
  * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment), HIP.
  */
@@ -160,7 +160,7 @@ int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const f
  *   codebook  : host, 256 floats (logbq_params.codebook of an 8-bit fit); rounded to float16
  *               after a common power-of-two scaling, as for logbq_linear.
  *   y_dev     : device, [m][n] float32, written.
- * Float32 accumulation. The GEMV runs for m <= 8 unless m >= 3 and m * n >= 65536; the
+ * Float32 accumulation. The GEMV runs for m <= 8 unless m >= 3 and m * n > 65536; the
  * dequantize-into-MFMA skinny GEMM runs otherwise. Errors: as logbq_linear.
  */
 int32_t logbq_linear8(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
