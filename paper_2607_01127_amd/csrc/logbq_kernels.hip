@@ -397,7 +397,9 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
   const int wk = SPLITK ? wk_arg : 1;
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[kLutWords];
   __shared__ __attribute__((aligned(16))) uint32_t s_x[kStageXPadded / 4];
-  __shared__ float s_red[8][M];
+  // Split rows: partial sums of kRed rows per wavefront, in two sets (see the loop below).
+  constexpr int kRed = M <= 4 ? 16 : 8;
+  __shared__ float s_part[SPLITK ? 2 : 1][SPLITK ? kRed : 1][8][M];
   __shared__ uint32_t s_ticket;
 
   // Segment of this workgroup: a uniform index, so its fields are scalar kernel-argument loads.
@@ -577,20 +579,31 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
     }
     flush();
   } else {
+    // Each wavefront leaves its row partials in slot it % kRed of set (it / kRed) % 2; after
+    // every kRed rows (and after the last) one barrier, then wavefront kw = 0 of each group sums
+    // the WK partials of those rows and stores them. The next kRed rows fill the other set, so
+    // no second barrier is needed before a set is written again (its readers have passed the
+    // barrier that ends the rows in between).
     auto finish_row = [&](int it) {
-      const int r = gid + it * total_groups;
+      const int slot = it % kRed, set = (it / kRed) & 1;
 #pragma unroll
       for (int m = 0; m < M; ++m) {
         const float t = wave_sum(acc[m]);
-        if (lane == 0) s_red[wave][m] = t;
+        if (lane == 0) s_part[set][slot][wave][m] = t;
       }
-      __syncthreads();
-      if (kw == 0 && lane < M && r < n_rows) {
-        float t = 0.0f;
-        for (int w2 = 0; w2 < wk; ++w2) t += s_red[grp * wk + w2][lane];
-        y[(int64_t)lane * n_rows + r] = t * scale;
+      if (slot == kRed - 1 || it == iters - 1) {
+        __syncthreads();
+        if (kw == 0 && lane < kRed * M) {
+          const int sl = lane / M, m = lane % M;
+          const int it2 = it - slot + sl;
+          const int r = gid + it2 * total_groups;
+          if (sl <= slot && r < n_rows) {
+            float t = 0.0f;
+            for (int w2 = 0; w2 < wk; ++w2) t += s_part[set][sl][grp * wk + w2][m];
+            y[(int64_t)m * n_rows + r] = t * scale;
+          }
+        }
       }
-      __syncthreads();
     };
 #pragma unroll
     for (int b = 1; b + 1 < NBUF; ++b) load_row(gid + b * total_groups, q[b]);
