@@ -118,9 +118,12 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  *               so the call is capturable in a HIP graph. Entries are rounded to float16 after
  *               a common power-of-two scaling, exact in the result up to float16 rounding.
  *   y_dev     : device, [m][n] float32, written.
- * Accumulation is float32. The wavefront-reduced GEMV runs for m <= 8 unless m >= 3 and
- * m * n > 65536; everything else (and shapes whose activations do not fit the GEMV's
- * registers) runs the dequantize-into-MFMA skinny GEMM.
+ * Accumulation is float32. Three kernels, chosen from (m, k, n) alone: for 2 <= m <= 16 and
+ * k in {1024, 2048, 4096, 8192}, a split-K dequantize-into-MFMA kernel takes m >= 5, m = 4 at
+ * n >= 8192 and m = 3 at n >= 16384 (except m > 12 at n >= 16384); otherwise the
+ * wavefront-reduced GEMV runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and
+ * shapes whose activations do not fit the GEMV's registers) runs the stepped
+ * dequantize-into-MFMA skinny GEMM.
  * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment), HIP.
  */
 int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,

@@ -12,6 +12,9 @@
 //              lane's B operand of v_mfma_f32_16x16x32_f16, dequantized by pair-table lookups
 //              or by v_perm_b32 byte tables in registers; activations are staged through LDS
 //              as the A operand; float32 accumulation in the MFMA.
+//   k_mfma_sk  the same product for 2 <= m <= 16 split over K: the 8 wavefronts of a workgroup
+//              share a block of 16 rows (one K slice each, activations held in registers) and
+//              sum their partial tiles through LDS.
 //
 // The float16 tables hold codebook / 2^e with 2^e chosen so that the largest entry lies in
 // [2^14, 2^15); the result is multiplied back by 2^e (exact). Lookup replaces evaluating
@@ -876,6 +879,156 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
     }
 }
 
+// ------------------------------------------------------------------ split-K MFMA, m <= 16
+//
+// For one batch tile (m <= 16) and K = 256 ND (ND = 4, 8, 16, 32, i.e. K = 1024 .. 8192): a
+// workgroup of 8 wavefronts takes one block of 16 weight rows at a time (blocks dealt
+// round-robin over the grid) and its wavefront w takes the K slice [w S, (w + 1) S), S = 32 ND.
+// The workgroup therefore streams its 16 rows as one contiguous band, instead of every
+// workgroup walking K in step over all rows (measured on MI355X: this code stream reads the
+// 8192 x 28672 codes in 20.2 us, the stepped pattern of k_mfma2 in 25 us).
+//
+// A lane's activations for its slice stay in registers for the whole kernel: lane (j, g) holds
+// batch row j at k = w S + 8 ND g + [0, 8 ND) (zeros for rows >= m). The codes of a block are
+// loaded as ND / 4 instructions of 64 / ND rows x 16 ND contiguous bytes and transposed through
+// the wavefront's LDS buffer so that lane (j, g) then holds row j, bytes [4 ND g, 4 ND (g + 1))
+// of the slice: dword d (k = w S + 8 ND g + 8 d + 0..7) is the B operand of MFMA d, matching the
+// A operand above. The 16 x 16 partial tiles of the 8 wavefronts are summed in LDS (two sets, one
+// barrier per block); each of the first 256 threads owns one (batch row, weight row) element and
+// keeps its results for up to 8 blocks before storing them. The next block's codes are in
+// flight while a block is computed.
+template <int ND, bool PAIRS>
+__global__ __launch_bounds__(512) void k_mfma_sk(const uint8_t* __restrict__ codes,
+                                                 const uint16_t* __restrict__ x,
+                                                 float* __restrict__ y, int n_rows, int k_cols,
+                                                 int m_rows, LutBytes tb, Lut16 lut,
+                                                 float scale) {
+  static_assert(ND == 4 || ND == 8 || ND == 16 || ND == 32, "64 / ND rows per load");
+  constexpr int BR = 16 * ND;            // code bytes per row per wavefront and block
+  constexpr int RPI = 64 / ND;           // rows per load instruction
+  constexpr int NI = ND / 4;             // load instructions per block
+  constexpr int TP = BR + 16;            // transpose pitch (bytes)
+  constexpr int NRES = 8;                // blocks whose results a thread holds before storing
+  __shared__ __attribute__((aligned(16))) uint32_t s_lut[PAIRS ? kLutWords : 4];
+  __shared__ __attribute__((aligned(16))) uint8_t s_ct[8][16 * TP];
+  __shared__ __attribute__((aligned(16))) float4v s_red[2][8][64];
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int j = lane & 15, g = lane >> 4;
+  const uint32_t laneoff = (uint32_t)lane << 2;
+  const int64_t row_bytes = (int64_t)k_cols / 2;
+  const int nblocks = (n_rows + 15) / 16;
+  const int slice_k0 = w * 32 * ND;
+
+  // Activations first (they return first): batch row j of this lane's slice, in the order the
+  // dequantization produces the weights.
+  u32x4 xa[ND];
+  {
+    const bool live = j < m_rows;
+    const int64_t base = (int64_t)(live ? j : 0) * k_cols + slice_k0 + 8 * ND * g;
+#pragma unroll
+    for (int d = 0; d < ND; ++d) xa[d] = *reinterpret_cast<const u32x4*>(x + base + 8 * d);
+#pragma unroll
+    for (int d = 0; d < ND; ++d) {
+      u32x4 v = live ? xa[d] : u32x4{0u, 0u, 0u, 0u};
+      xa[d] = PAIRS ? v : permute_x8(v);
+    }
+  }
+  // Codes of block b: a descriptor over its rows (size 0 past the last block, short for a
+  // partial last block), so rows past n_rows read as zeros.
+  auto load_block = [&](int b, u32x4 (&q)[NI]) {
+    const int bb = b < nblocks ? b : nblocks - 1;
+    const int64_t base = (int64_t)bb * 16 * row_bytes;
+    const int64_t avail = (int64_t)n_rows * row_bytes - base;
+    const int size = b < nblocks ? (int)(avail < 16 * row_bytes ? avail : 16 * row_bytes) : 0;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(codes + base), (short)0, size, kBufferRsrcWord3);
+#pragma unroll
+    for (int c = 0; c < NI; ++c) {
+      const int r = RPI * c + lane / ND;
+      const int off = r * (int)row_bytes + w * BR + 16 * (lane % ND);
+      q[c] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kCachePolicyNT);
+    }
+  };
+  u32x4 q[2][NI];
+  load_block(blockIdx.x, q[0]);
+  if (PAIRS) fill_lut<4, 512>(s_lut, lut);
+  __syncthreads();
+
+  float res[NRES];
+  int held = 0, blast = 0, par = 0;
+  const int ri = t >> 4, rj = t & 15;      // element of threads t < 256: batch ri, row rj
+  auto flush = [&]() {
+    if (t < 256 && ri < m_rows) {
+#pragma unroll
+      for (int h = 0; h < NRES; ++h) {
+        if (h < held) {
+          const int b = blast - (held - 1 - h) * (int)gridDim.x;
+          const int row = b * 16 + rj;
+          if (row < n_rows) y[(int64_t)ri * n_rows + row] = res[h];
+        }
+      }
+    }
+    held = 0;
+  };
+  uint8_t* s_cw = s_ct[w];
+  auto block = [&](int b, const u32x4 (&qc)[NI]) {
+    // LDS operations of one wavefront complete in order: the reads see the writes.
+#pragma unroll
+    for (int c = 0; c < NI; ++c)
+      *reinterpret_cast<u32x4*>(s_cw + (RPI * c + lane / ND) * TP + 16 * (lane % ND)) = qc[c];
+    __builtin_amdgcn_wave_barrier();
+    u32x4 o[NI];
+#pragma unroll
+    for (int c = 0; c < NI; ++c)
+      o[c] = *reinterpret_cast<const u32x4*>(s_cw + j * TP + 4 * ND * g + 16 * c);
+    __builtin_amdgcn_wave_barrier();
+    float4v acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int d = 0; d < ND; ++d) {
+      const u32x4 od = o[d >> 2];
+      const uint32_t dw = (d & 3) == 0 ? od.x : (d & 3) == 1 ? od.y : (d & 3) == 2 ? od.z : od.w;
+      uint32_t bw[4];
+      if (PAIRS) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) bw[i] = pair_lookup(s_lut, dw, laneoff, i);
+      } else {
+        dequant_dword(dw, tb, bw);
+      }
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+          __builtin_bit_cast(half8v, xa[d]),
+          __builtin_bit_cast(half8v, u32x4{bw[0], bw[1], bw[2], bw[3]}), acc, 0, 0, 0);
+    }
+    // Lane l holds D[4 (l / 16) + r][l % 16] (batch row, weight row) in component r.
+    s_red[par][w][lane] = acc;
+    __syncthreads();
+    if (t < 256) {
+      const int l = 16 * (ri >> 2) + rj, r = ri & 3;
+      float sum = 0.0f;
+#pragma unroll
+      for (int w2 = 0; w2 < 8; ++w2) sum += s_red[par][w2][l][r];
+#pragma unroll
+      for (int h = 0; h < NRES; ++h)
+        if (h == held) res[h] = sum * scale;
+    }
+    par ^= 1;
+    ++held;
+    blast = b;
+    if (held == NRES) flush();
+  };
+  // Every path through the loop issues the same loads (blocks past the end get size-0
+  // descriptors), so the compiler's waits stay exact. The barrier inside block() is reached by
+  // the whole workgroup: the loop bounds depend only on the block index.
+  for (int b = blockIdx.x; b < nblocks; b += 2 * (int)gridDim.x) {
+    load_block(b + (int)gridDim.x, q[1]);
+    block(b, q[0]);
+    load_block(b + 2 * (int)gridDim.x, q[0]);
+    if (b + (int)gridDim.x < nblocks) block(b + (int)gridDim.x, q[1]);
+  }
+  flush();
+}
+
 // ------------------------------------------------------------------ host helpers
 
 // IEEE binary32 -> binary16, round to nearest even.
@@ -1100,6 +1253,39 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
   return launch_status();
 }
 
+// Split-K MFMA path: 4-bit codes, 2 <= m <= 16, K in {1024, 2048, 4096, 8192}.
+bool sk_shape(int M, int K) {
+  return M >= 2 && M <= 16 && (K == 1024 || K == 2048 || K == 4096 || K == 8192);
+}
+
+int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st, int cus) {
+  const int N = (int)j.n;
+  LutBytes tb = {0, 0, 0, 0};
+  Lut16 lut;
+  float scale;
+  // Register dequantization needs a sign-symmetric codebook (every fitted one is); any other
+  // codebook goes through the LDS pair table.
+  const bool symmetric = make_lut_bytes(j.codebook, &tb, &scale);
+  make_lut16(j.codebook, &lut, &scale);
+  const int nblocks = (N + 15) / 16;
+  const int grid = nblocks < cus ? nblocks : cus;
+#define LOGBQ_SK(ND)                                                                             \
+  if (symmetric)                                                                                 \
+    hipLaunchKernelGGL((k_mfma_sk<ND, false>), dim3((unsigned)grid), dim3(512), 0, st, j.codes, x, \
+                       j.y, N, K, M, tb, lut, scale);                                            \
+  else                                                                                           \
+    hipLaunchKernelGGL((k_mfma_sk<ND, true>), dim3((unsigned)grid), dim3(512), 0, st, j.codes, x,  \
+                       j.y, N, K, M, tb, lut, scale);
+  switch (K) {
+    case 1024: LOGBQ_SK(4) break;
+    case 2048: LOGBQ_SK(8) break;
+    case 4096: LOGBQ_SK(16) break;
+    default: LOGBQ_SK(32) break;
+  }
+#undef LOGBQ_SK
+  return launch_status();
+}
+
 // y_i = x . W_hat_i^T for up to kMaxSegs linears sharing x (validated by the caller).
 template <int BITS>
 int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jobs, int count,
@@ -1129,14 +1315,27 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
   // still 1 us faster); the GEMV takes everything else up to m = 8. The choice depends only on
   // (m, k, N), so every linear of a grouped call runs the kernel that a single call would run,
   // with the same result bits.
+  //
+  // Where the split-K MFMA kernel applies (4-bit codes, 2 <= m <= 16, K = 1, 2, 4 or 8 Ki), it
+  // takes m >= 5, m = 4 at N >= 8192 and m = 3 at N >= 16384, except m > 12 at N >= 16384
+  // (measured: it beats the GEMV there and the stepped MFMA kernel everywhere except the widest
+  // layers at m = 13..16, e.g. 2048 x 8192 at m = 16: 13.0 us vs 28.7 us, 8192 -> 28672 at m = 8:
+  // 29.6 us vs 31.8 us).
   int wk = 0, cpl = 0;
   const bool gemv_ok = M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl);
+  const bool sk_ok = BITS == 4 && sk_shape(M, K);
   int gl[kMaxSegs];
   int ng = 0;
   int64_t grows = 0;
   for (int a = 0; a < nlive; ++a) {
     const LinearJob& j = jobs[live[a]];
-    if (gemv_ok && !(M >= 3 && (int64_t)M * j.n > 65536)) {
+    const bool use_sk = sk_ok &&
+                        (M >= 5 || (M == 4 && j.n >= 8192) || (M == 3 && j.n >= 16384)) &&
+                        !(M > 12 && j.n >= 16384);
+    if (use_sk) {
+      const int32_t r = launch_sk(x, M, K, j, st, cus);
+      if (r != LOGBQ_OK) return r;
+    } else if (gemv_ok && !(M >= 3 && (int64_t)M * j.n > 65536)) {
       gl[ng++] = live[a];
       grows += j.n;
     } else {

@@ -291,6 +291,28 @@ def test_linear_arbitrary_codebook():
             assert rel_err(y.cpu().numpy(), x, wh) <= TOL
 
 
+def test_linear_split_k_many_blocks():
+    """The split-K MFMA path (2 <= m <= 16, K = 1, 2, 4 or 8 Ki) with more than 8 blocks of 16
+    rows per workgroup (results are stored 8 blocks at a time) and a ragged last block, for a
+    fitted (register dequantization) and an arbitrary codebook (pair table)."""
+    n, k = 40003, 1024
+    w, p, r = prepare(n, k, [8, 11, 1, 0])
+    codes, cb = gpu_encode(w, p)
+    wh = O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
+    rng = np.random.default_rng(13)
+    cb2 = rng.standard_normal(16).astype(np.float32)
+    wh2 = O.dequantize(O.unpack(codes.cpu().numpy()), cb2)
+    for m in (5, 8, 13, 16):
+        _say(f"split-K many blocks m={m}")
+        x = inputs.activations(m, k, seed=[8, 11, 2, m])
+        xd = torch.from_numpy(x).to(DEV)
+        y = L.linear(xd, codes, cb)
+        y2 = L.linear(xd, codes, cb2)
+        torch.cuda.synchronize()
+        assert rel_err(y.cpu().numpy(), x, wh) <= 2.5e-4
+        assert rel_err(y2.cpu().numpy(), x, wh2) <= TOL
+
+
 def test_linear_multi_matches_single_launches():
     """Grouped launch of linears sharing x: every output equals the single-linear call bit for
     bit, and the oracle within tolerance (qkv-like and gate/up-like groups, ragged sizes)."""
