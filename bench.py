@@ -194,8 +194,7 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=Tr
             "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
             "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
             "algo_bytes": algo,
-            # the library's path rule: GEMV for m <= 8 unless m >= 3 and m * N > 65536
-            "path": "gemv" if m <= 8 and not (m >= 3 and m * n > 65536) else "mfma"}
+            "path": L.linear_path(4, m, k, n)}
     return results, {"n": n, "k": k, "packed": packed, "copies": copies, "fit_s": fit_s,
                      "params": {"base": p.base, "shift": p.shift, "wmin": p.wmin,
                                 "wmax": p.wmax}}, codes, cb
@@ -241,7 +240,7 @@ def bench_layer8(torch, L, inputs, dev, stream, ms, steps, warmup):
             "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
             "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
             "algo_bytes": algo, "copies": copies,
-            "path": "gemv" if m <= 8 and not (m >= 3 and m * n > 65536) else "mfma"}
+            "path": L.linear_path(8, m, k, n)}
     del code_list, codes
     return results
 
@@ -282,7 +281,8 @@ def bench_small(torch, L, inputs, dev, stream, name, steps, warmup):
     timed = steps
     t = time_launches(torch, L, stream, [(x, c, cb, y) for c in code_list], steps, warmup)
     return {"ms": t, "us": t * 1e3, "launches_timed": timed, "weight_GB_s": packed / t / 1e6,
-            "hbm_frac": packed / t / 1e6 / HBM_PEAK_GBS, "copies": copies}
+            "hbm_frac": packed / t / 1e6 / HBM_PEAK_GBS, "copies": copies,
+            "path": L.linear_path(4, 1, lin.k, lin.n)}
 
 
 def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):

@@ -123,7 +123,7 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  * n >= 8192 and m = 3 at n >= 16384 (except m > 12 at n >= 16384); otherwise the
  * wavefront-reduced GEMV runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and
  * shapes whose activations do not fit the GEMV's registers) runs the stepped
- * dequantize-into-MFMA skinny GEMM.
+ * dequantize-into-MFMA skinny GEMM. logbq_linear_path reports the choice.
  * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment), HIP.
  */
 int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
@@ -168,6 +168,26 @@ int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const f
  */
 int32_t logbq_linear8(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
                       int64_t n, const float* codebook, float* y_dev, void* stream);
+
+/* Kernel that logbq_linear (bits 4) or logbq_linear8 (bits 8) runs for a call of a shape. */
+typedef enum logbq_path {
+  LOGBQ_PATH_NONE = 0,     /* m or n is 0 (nothing written) or k is 0 (zeros written)        */
+  LOGBQ_PATH_GEMV = 1,     /* wavefront-reduced GEMV with the LDS pair table                  */
+  LOGBQ_PATH_MFMA = 2,     /* stepped dequantize-into-MFMA skinny GEMM                        */
+  LOGBQ_PATH_SPLITK = 3    /* split-K dequantize-into-MFMA kernel (4-bit, 2 <= m <= 16)        */
+} logbq_path;
+
+/*
+ * logbq_linear_path -- the kernel a logbq_linear / logbq_linear8 call of shape (m, k, n)
+ * runs (Sec. 3.3 product; the choice is this library's, not the method's). Host only: needs
+ * no device and touches none. The choice depends on (bits, m, k, n) alone, so it is the same
+ * for every linear of a logbq_linear_multi call.
+ *   bits     : 4 or 8.
+ *   m, k, n  : as logbq_linear; k % 32 == 0.
+ *   path_out : host, one int32, written with a logbq_path on success.
+ * Errors: INVALID_ARG (null path_out, negative size), UNSUPPORTED (bits, k % 32, m too large).
+ */
+int32_t logbq_linear_path(int32_t bits, int64_t m, int64_t k, int64_t n, int32_t* path_out);
 
 /*
  * logbq_dequantize8 -- Dequant (Eq. 2) of 8-bit codes: w[n][k] = codebook[codes[n][k]].

@@ -1286,6 +1286,30 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob& j, hipStream
   return launch_status();
 }
 
+// Path choice per linear (measured on MI355X). The GEMV's time grows with m * N * K (its
+// products are VALU dot2 per weight and batch row); the MFMA kernel's is about flat in m up to
+// 16 but uses only N / 128 workgroups. Measured crossover: the MFMA kernel wins once m >= 3 and
+// m * N > 65536 (N = 28672 from m = 3, N = 14336 from m = 5; at N = 8192, m = 8 the GEMV is
+// still 1 us faster); the GEMV takes everything else up to m = 8. The choice depends only on
+// (m, k, N), so every linear of a grouped call runs the kernel that a single call would run,
+// with the same result bits.
+//
+// Where the split-K MFMA kernel applies (4-bit codes, 2 <= m <= 16, K = 1, 2, 4 or 8 Ki), it
+// takes m >= 5, m = 4 at N >= 8192 and m = 3 at N >= 16384, except m > 12 at N >= 16384
+// (measured: it beats the GEMV there and the stepped MFMA kernel everywhere except the widest
+// layers at m = 13..16, e.g. 2048 x 8192 at m = 16: 13.0 us vs 28.7 us, 8192 -> 28672 at m = 8:
+// 29.6 us vs 31.8 us).
+template <int BITS>
+int choose_path(int M, int K, int64_t N) {
+  int wk = 0, cpl = 0;
+  if (sk_shape(M, K) && BITS == 4 &&
+      (M >= 5 || (M == 4 && N >= 8192) || (M == 3 && N >= 16384)) && !(M > 12 && N >= 16384))
+    return LOGBQ_PATH_SPLITK;
+  if (M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl) && !(M >= 3 && (int64_t)M * N > 65536))
+    return LOGBQ_PATH_GEMV;
+  return LOGBQ_PATH_MFMA;
+}
+
 // y_i = x . W_hat_i^T for up to kMaxSegs linears sharing x (validated by the caller).
 template <int BITS>
 int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jobs, int count,
@@ -1308,34 +1332,17 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
     return LOGBQ_OK;
   }
   const int M = (int)m, K = (int)k;
-  // Path choice per linear (measured on MI355X). The GEMV's time grows with m * N * K (its
-  // products are VALU dot2 per weight and batch row); the MFMA kernel's is about flat in m up to
-  // 16 but uses only N / 128 workgroups. Measured crossover: the MFMA kernel wins once m >= 3 and
-  // m * N > 65536 (N = 28672 from m = 3, N = 14336 from m = 5; at N = 8192, m = 8 the GEMV is
-  // still 1 us faster); the GEMV takes everything else up to m = 8. The choice depends only on
-  // (m, k, N), so every linear of a grouped call runs the kernel that a single call would run,
-  // with the same result bits.
-  //
-  // Where the split-K MFMA kernel applies (4-bit codes, 2 <= m <= 16, K = 1, 2, 4 or 8 Ki), it
-  // takes m >= 5, m = 4 at N >= 8192 and m = 3 at N >= 16384, except m > 12 at N >= 16384
-  // (measured: it beats the GEMV there and the stepped MFMA kernel everywhere except the widest
-  // layers at m = 13..16, e.g. 2048 x 8192 at m = 16: 13.0 us vs 28.7 us, 8192 -> 28672 at m = 8:
-  // 29.6 us vs 31.8 us).
   int wk = 0, cpl = 0;
-  const bool gemv_ok = M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl);
-  const bool sk_ok = BITS == 4 && sk_shape(M, K);
   int gl[kMaxSegs];
   int ng = 0;
   int64_t grows = 0;
   for (int a = 0; a < nlive; ++a) {
     const LinearJob& j = jobs[live[a]];
-    const bool use_sk = sk_ok &&
-                        (M >= 5 || (M == 4 && j.n >= 8192) || (M == 3 && j.n >= 16384)) &&
-                        !(M > 12 && j.n >= 16384);
-    if (use_sk) {
+    const int path = choose_path<BITS>(M, K, j.n);
+    if (path == LOGBQ_PATH_SPLITK) {
       const int32_t r = launch_sk(x, M, K, j, st, cus);
       if (r != LOGBQ_OK) return r;
-    } else if (gemv_ok && !(M >= 3 && (int64_t)M * j.n > 65536)) {
+    } else if (path == LOGBQ_PATH_GEMV) {
       gl[ng++] = live[a];
       grows += j.n;
     } else {
@@ -1344,6 +1351,7 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
     }
   }
   if (ng == 0) return LOGBQ_OK;
+  if (!gemv_config<BITS>(M, K, &wk, &cpl)) return LOGBQ_ERR_UNSUPPORTED;
   const int groups = 8 / wk;
   GemvSegs<BITS> segs;
   std::memset(&segs, 0, sizeof(segs));
@@ -1509,6 +1517,18 @@ int32_t logbq_dequantize8(const uint8_t* codes_dev, int64_t n, int64_t k, const 
                      dim3(256), 0, (hipStream_t)stream, reinterpret_cast<const uint32_t*>(codes_dev),
                      reinterpret_cast<f32x4*>(w_dev), nwords, cb);
   return launch_status();
+}
+
+int32_t logbq_linear_path(int32_t bits, int64_t m, int64_t k, int64_t n, int32_t* path_out) {
+  if (!path_out || m < 0 || k < 0 || n < 0) return LOGBQ_ERR_INVALID_ARG;
+  if (bits != 4 && bits != 8) return LOGBQ_ERR_UNSUPPORTED;
+  if (k % 32 != 0 || m > kMaxBatchRows || k > INT32_MAX) return LOGBQ_ERR_UNSUPPORTED;
+  if (m == 0 || n == 0 || k == 0) {
+    *path_out = LOGBQ_PATH_NONE;
+    return LOGBQ_OK;
+  }
+  *path_out = bits == 4 ? choose_path<4>((int)m, (int)k, n) : choose_path<8>((int)m, (int)k, n);
+  return LOGBQ_OK;
 }
 
 }  // extern "C"

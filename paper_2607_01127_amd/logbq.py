@@ -64,6 +64,7 @@ SIGNATURES = {
                                 c_void_p, c_void_p]),
     "logbq_dequantize8": (c_int32, [c_void_p, c_int64, c_int64, POINTER(c_float), c_void_p,
                                     c_void_p]),
+    "logbq_linear_path": (c_int32, [c_int32, c_int64, c_int64, c_int64, POINTER(c_int32)]),
 }
 
 ABI_VERSION = 2
@@ -237,3 +238,15 @@ def dequantize8(codes, codebook, out=None, stream=None):
     _check(lib().logbq_dequantize8(c_void_p(codes.data_ptr()), n, k, cbp, c_void_p(out.data_ptr()),
                                    _stream(stream)), "logbq_dequantize8")
     return out
+
+
+PATH_NAMES = {0: "none", 1: "gemv", 2: "mfma", 3: "splitk"}
+
+
+def linear_path(bits: int, m: int, k: int, n: int) -> str:
+    """logbq_linear_path: name of the kernel ("none", "gemv", "mfma" or "splitk") that
+    linear (bits 4) or linear8 (bits 8) runs for an [m][k] x [n][k] call. Host only."""
+    out = c_int32(0)
+    _check(lib().logbq_linear_path(int(bits), int(m), int(k), int(n), ctypes.byref(out)),
+           "logbq_linear_path")
+    return PATH_NAMES[out.value]

@@ -230,3 +230,28 @@ def test_8bit_validation_before_hip():
     assert list(out) == list(p.codebook)
     p.bits = 6
     assert h.logbq_encode(a, 1, 64, ctypes.byref(p), a, None, None) == L.ERR_UNSUPPORTED
+
+
+def test_linear_path_rule():
+    """Path choice is host logic: checked here without a device."""
+    lp = L.linear_path
+    assert lp(4, 1, 8192, 28672) == "gemv"
+    assert lp(4, 0, 8192, 28672) == "none" and lp(4, 4, 0, 100) == "none"
+    assert lp(4, 4, 64, 0) == "none"
+    # split-K kernel: 4-bit, 2 <= m <= 16, K in {1, 2, 4, 8} Ki
+    assert lp(4, 8, 8192, 28672) == "splitk"
+    assert lp(4, 16, 2048, 8192) == "splitk"
+    assert lp(4, 16, 8192, 28672) == "mfma"        # m > 12 at N >= 16384
+    assert lp(4, 3, 4096, 16384) == "splitk" and lp(4, 3, 4096, 8192) == "gemv"
+    assert lp(4, 4, 4096, 8192) == "splitk" and lp(4, 4, 4096, 4096) == "gemv"
+    assert lp(4, 8, 8192 + 32, 28672) == "mfma"    # K outside the split-K set
+    assert lp(4, 17, 8192, 2048) == "mfma" and lp(4, 128, 8192, 28672) == "mfma"
+    # 8-bit codes: GEMV unless m >= 3 and m * N > 65536, else the stepped MFMA kernel
+    assert lp(8, 1, 8192, 28672) == "gemv" and lp(8, 2, 8192, 28672) == "gemv"
+    assert lp(8, 8, 8192, 28672) == "mfma" and lp(8, 8, 2048, 8192) == "gemv"
+    for bad in ((4, -1, 64, 1), (4, 1, 64, -1)):
+        with pytest.raises(L.LogbqError):
+            lp(*bad)
+    for bad in ((5, 1, 64, 1), (4, 1, 48, 1), (8, 1 << 40, 64, 1)):
+        with pytest.raises(L.LogbqError):
+            lp(*bad)
