@@ -21,6 +21,7 @@ import argparse
 import concurrent.futures as cf
 import ctypes
 import json
+import math
 import os
 import sys
 import time
@@ -198,6 +199,61 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=Tr
     return results, {"n": n, "k": k, "packed": packed, "copies": copies, "fit_s": fit_s,
                      "params": {"base": p.base, "shift": p.shift, "wmin": p.wmin,
                                 "wmax": p.wmax}}, codes, cb
+
+
+def bench_quality(torch, L, inputs, dev, stream, layer_codes, layer_cb, steps, warmup):
+    """LogbQuant against the asymmetric linear baseline (Sec. 2, Quant(s, z, x); tensor-wise as
+    in Sec. 4) on the single-tensor workloads: reconstruction SQNR, relative error of an M = 4
+    product against the float64 product with the unquantized weights, the share of weights on
+    the zero level, and, on the 8192 x 28672 layer, the time of the baseline's codes through
+    the same linear kernels (their codebook is not sign-symmetric, so every kernel uses its
+    LDS-table form)."""
+    out = {}
+    for name in ("linear_2048x2048", "up_2048x8192_outliers", "layer_8192x28672"):
+        wl = inputs.WORKLOADS[name]
+        lin = wl["layers"][0]
+        log(f"quality {name}")
+        w = inputs.student_t_weights(lin.n, lin.k, wl["nu"], wl["scale"], seed=[wl["cfg"], 0, 0, 0],
+                                     device=dev, outlier_frac=wl.get("outlier_frac", 0.0))
+        w_host = w.cpu().numpy()
+        if name == "layer_8192x28672":
+            codes, cb = layer_codes, layer_cb
+        else:
+            codes, cb = L.encode(w, L.fit(w_host))
+        u = L.fit_uniform(w_host)
+        ucb = u.codebook_array()
+        ucodes = L.encode_uniform(w, u)
+        x = inputs.activations(4, lin.k, seed=[wl["cfg"], 0, 0, 2], device=dev)
+        w64 = w.double()
+        y_ref = x.double() @ w64.T
+        row = {}
+        for scheme, c, book in (("logbquant", codes, cb), ("uniform", ucodes, ucb)):
+            wh = L.dequantize(c, book).double()
+            err = float(((w64 - wh) ** 2).sum())
+            sig = float((w64 ** 2).sum())
+            y = L.linear(x, c, book).double()
+            row[scheme] = {"sqnr_db": 10.0 * math.log10(sig / err),
+                           "gemv_rel_err_m4": float((y - y_ref).norm() / y_ref.norm()),
+                           "zero_level_frac": float((wh == 0).double().mean())}
+            del wh
+        row["uniform"]["params"] = {"scale": u.scale, "zero": u.zero, "wmin": u.wmin, "wmax": u.wmax}
+        if name == "layer_8192x28672":
+            packed = lin.n * lin.k // 2
+            copies = max(2, -(-ROTATE_BYTES // packed))
+            code_list = [ucodes] + [ucodes.clone() for _ in range(copies - 1)]
+            for m in (1, 8, 32):
+                xm = inputs.activations(m, lin.k, seed=[wl["cfg"], 0, 0, 1], device=dev)
+                launches = [(xm, c, ucb, torch.empty((m, lin.n), dtype=torch.float32, device=dev))
+                            for c in code_list]
+                t = time_launches(torch, L, stream, launches, steps if m == 1 else max(64, steps // 4),
+                                  warmup if m == 1 else warmup // 4)
+                row["uniform"][f"linear_m{m}_us"] = t * 1e3
+                row["uniform"][f"linear_m{m}_path"] = L.linear_path(4, m, lin.k, lin.n)
+            del code_list
+        out[name] = row
+        del w, w64, ucodes, y_ref
+        torch.cuda.empty_cache()
+    return out
 
 
 def bench_layer8(torch, L, inputs, dev, stream, ms, steps, warmup):
@@ -514,9 +570,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10000,
                     help="untimed launches before the timed ones (about 0.2 s of GPU work at M = 1)")
     ap.add_argument("--quick", action="store_true", help="main layer only, no extra rows")
-    ap.add_argument("--rows", default="layer,layer8,small,decode1b,decode8b",
+    ap.add_argument("--rows", default="layer,layer8,small,decode1b,decode8b,quality",
                     help="comma list of extra rows: layer (M sweep + encode), layer8 (the same "
-                         "layer at 8 bits), small, decode1b, decode8b")
+                         "layer at 8 bits), small, decode1b, decode8b, quality (LogbQuant "
+                         "against the asymmetric linear baseline)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device-to-device copy (calibrates the HBM byte "
@@ -554,6 +611,9 @@ def main():
     value = packed / t_ms / 1e6
 
     rows = dict(res)
+    if "quality" in want:
+        rows["quality_vs_uniform"] = bench_quality(torch, L, inputs, dev, stream, codes, cb,
+                                                   args.steps, args.warmup)
     log("HBM read ceiling (4 GiB)")
     ceiling = read_ceiling(torch, stream)
     torch.cuda.empty_cache()

@@ -64,6 +64,23 @@ typedef struct logbq_params {
                               k = 0..qmax-1; entries from qmax on are +inf                  */
 } logbq_params;
 
+/* Per-tensor parameters of the comparison baseline: asymmetric linear quantization,
+ * Quant(s, z, x) = round(x / s) - z (Sec. 2), at tensor granularity (Sec. 4). Plain data.
+ * s = (max w - min w) / (2^n - 1) and z = round(min w / s), ties rounded up; code q in
+ * 0 .. 2^n - 1 stands for s (q + z). Only n = 4 is provided. */
+typedef struct logbq_uniform {
+  int32_t bits;            /* 4                                                            */
+  int32_t zero;            /* z                                                            */
+  double wmin;             /* min w (signed)                                               */
+  double wmax;             /* max w (signed)                                               */
+  double scale;            /* s                                                            */
+  float codebook[16];      /* s (q + z) rounded to float32: the codebook logbq_linear and
+                              logbq_dequantize take for these codes                        */
+  float thresholds[15];    /* [j - 1] = smallest float32 x whose code is at least j (+inf
+                              if none), j = 1 .. 15                                          */
+  float reserved;
+} logbq_uniform;
+
 /* ABI version of the loaded library (LOGBQ_ABI_VERSION it was built with). */
 int32_t logbq_abi_version(void);
 
@@ -168,6 +185,31 @@ int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const f
  */
 int32_t logbq_linear8(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
                       int64_t n, const float* codebook, float* y_dev, void* stream);
+
+/*
+ * logbq_fit_uniform -- s, z, codebook and encoding thresholds of the asymmetric linear
+ * baseline (Sec. 2, Quant(s, z, x)) for one tensor, from its full value range. Host only.
+ *   w_host : host, numel float32 weights (any layout).
+ *   bits   : 4.
+ *   out    : host, filled on success.
+ * Codes are decided in float64 as round(x / s) - z (ties up), clamped to 0 .. 15; the
+ * thresholds reproduce that decision exactly with float32 comparisons.
+ * Errors: INVALID_ARG (null, numel < 2), UNSUPPORTED (bits != 4), NONFINITE (NaN / Inf),
+ * DEGENERATE (all weights equal).
+ */
+int32_t logbq_fit_uniform(const float* w_host, int64_t numel, int32_t bits, logbq_uniform* out);
+
+/*
+ * logbq_encode_uniform -- 4-bit asymmetric linear codes of float32 weights on the GPU:
+ * code(x) = number of thresholds at or below x (NaN gives 0). Packing and layout as
+ * logbq_encode ([n][k/2] bytes, low nibble = even k), but a nibble is the unsigned code q.
+ * The codes run through logbq_linear / logbq_dequantize with u->codebook.
+ *   w_dev     : device, [n][k] float32.   codes_dev : device, [n][k/2] bytes, written.
+ *   u         : host, from logbq_fit_uniform (bits 4, thresholds non-decreasing).
+ * Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment, bits), HIP.
+ */
+int32_t logbq_encode_uniform(const float* w_dev, int64_t n, int64_t k, const logbq_uniform* u,
+                             uint8_t* codes_dev, void* stream);
 
 /* Kernel that logbq_linear (bits 4) or logbq_linear8 (bits 8) runs for a call of a shape. */
 typedef enum logbq_path {

@@ -142,9 +142,59 @@ float exact_threshold(double b, int32_t s, int k) {
   return f;
 }
 
+// Code of x under the asymmetric linear quantizer: round(x / s) - z with ties up, clamped.
+int uniform_code(float x, double s, int32_t z) {
+  const double v = (double)x / s;
+  if (std::isnan(v)) return 0;
+  if (std::isinf(v)) return v > 0 ? 15 : 0;
+  const double q = std::floor(v + 0.5) - (double)z;
+  return q < 0.0 ? 0 : (q > 15.0 ? 15 : (int)q);
+}
+
+// Smallest float32 whose code is at least j: start at the real boundary s (j + z - 1/2) and
+// walk neighbouring float32 values (the code is non-decreasing in x).
+float uniform_threshold(double s, int32_t z, int j) {
+  float t = (float)(s * ((double)j + (double)z - 0.5));
+  if (!std::isfinite(t)) return t;
+  while (uniform_code(t, s, z) >= j) t = std::nextafterf(t, -INFINITY);
+  while (uniform_code(t, s, z) < j) {
+    t = std::nextafterf(t, INFINITY);
+    if (!std::isfinite(t)) break;
+  }
+  return t;
+}
+
 }  // namespace
 
 extern "C" {
+
+int32_t logbq_fit_uniform(const float* w_host, int64_t numel, int32_t bits, logbq_uniform* out) {
+  if (!w_host || !out || numel < 2) return LOGBQ_ERR_INVALID_ARG;
+  if (bits != 4) return LOGBQ_ERR_UNSUPPORTED;
+  float lo = INFINITY, hi = -INFINITY;
+  for (int64_t i = 0; i < numel; ++i) {
+    const float v = w_host[i];
+    if (!std::isfinite(v)) return LOGBQ_ERR_NONFINITE;
+    lo = v < lo ? v : lo;
+    hi = v > hi ? v : hi;
+  }
+  if (!(hi > lo)) return LOGBQ_ERR_DEGENERATE;
+  const double s = ((double)hi - (double)lo) / 15.0;
+  const double zf = std::floor((double)lo / s + 0.5);
+  if (!(zf > -1e9 && zf < 1e9)) return LOGBQ_ERR_DEGENERATE;
+  logbq_uniform u;
+  std::memset(&u, 0, sizeof(u));
+  u.bits = bits;
+  u.zero = (int32_t)zf;
+  u.wmin = lo;
+  u.wmax = hi;
+  u.scale = s;
+  for (int q = 0; q < 16; ++q) u.codebook[q] = (float)(s * (double)(q + u.zero));
+  for (int j = 1; j < 16; ++j) u.thresholds[j - 1] = uniform_threshold(s, u.zero, j);
+  *out = u;
+  return LOGBQ_OK;
+}
+
 
 int32_t logbq_abi_version(void) { return LOGBQ_ABI_VERSION; }
 

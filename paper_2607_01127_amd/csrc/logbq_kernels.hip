@@ -83,12 +83,30 @@ __device__ __forceinline__ uint32_t encode4(const f32x4 a, const Thresholds& th)
   return out;
 }
 
-__global__ __launch_bounds__(256) void k_encode(const f32x4* __restrict__ w,
-                                                uint16_t* __restrict__ codes, int64_t nchunk,
-                                                Thresholds th) {
+// Asymmetric linear baseline (Sec. 2): the unsigned 4-bit code of x is the number of the 15
+// non-decreasing thresholds at or below it.
+struct ThresholdsU { float t[15]; };
+
+__device__ __forceinline__ uint32_t encode4(const f32x4 a, const ThresholdsU& th) {
+  const float v[4] = {a.x, a.y, a.z, a.w};
+  uint32_t out = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint32_t q = 0;
+#pragma unroll
+    for (int t = 0; t < 15; ++t) q += (v[j] >= th.t[t]) ? 1u : 0u;
+    out |= q << (4 * j);
+  }
+  return out;
+}
+
+template <typename TH>
+__device__ __forceinline__ void encode_tiles(const f32x4* __restrict__ w,
+                                             uint16_t* __restrict__ codes, int64_t nchunk,
+                                             const TH& th) {
   const int lane = threadIdx.x & 63;
-  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  const int64_t wave = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;   // 256-thread blocks
+  const int64_t nwaves = ((int64_t)gridDim.x * 256) >> 6;
   const int64_t ntiles = (nchunk + 64 * kEncU - 1) / (64 * kEncU);
   for (int64_t t = wave; t < ntiles; t += nwaves) {
     const int64_t base = t * 64 * kEncU + lane;
@@ -104,6 +122,18 @@ __global__ __launch_bounds__(256) void k_encode(const f32x4* __restrict__ w,
       if (idx < nchunk) codes[idx] = (uint16_t)encode4(v[j], th);
     }
   }
+}
+
+__global__ __launch_bounds__(256) void k_encode(const f32x4* __restrict__ w,
+                                                uint16_t* __restrict__ codes, int64_t nchunk,
+                                                Thresholds th) {
+  encode_tiles(w, codes, nchunk, th);
+}
+
+__global__ __launch_bounds__(256) void k_encode_uniform(const f32x4* __restrict__ w,
+                                                        uint16_t* __restrict__ codes,
+                                                        int64_t nchunk, ThresholdsU th) {
+  encode_tiles(w, codes, nchunk, th);
 }
 
 // ------------------------------------------------------------------ dequantize
@@ -1420,6 +1450,33 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
                        reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint32_t*>(codes_dev),
                        nchunk, th);
   }
+  return launch_status();
+}
+
+int32_t logbq_encode_uniform(const float* w_dev, int64_t n, int64_t k, const logbq_uniform* u,
+                             uint8_t* codes_dev, void* stream) {
+  if (!u || n < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
+  if (u->bits != 4) return LOGBQ_ERR_UNSUPPORTED;
+  if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
+  const int64_t numel = n * k;
+  if (n != 0 && numel / n != k) return LOGBQ_ERR_UNSUPPORTED;
+  for (int i = 0; i < 15; ++i) {
+    const float t = u->thresholds[i];
+    if (std::isnan(t)) return LOGBQ_ERR_INVALID_ARG;
+    if (i > 0 && t < u->thresholds[i - 1]) return LOGBQ_ERR_INVALID_ARG;
+  }
+  if (numel == 0) return LOGBQ_OK;
+  if (!w_dev || !codes_dev) return LOGBQ_ERR_INVALID_ARG;
+  if (!aligned16(w_dev) || !aligned16(codes_dev)) return LOGBQ_ERR_UNSUPPORTED;
+  const int cus = device_cus();
+  if (cus <= 0) return LOGBQ_ERR_HIP;
+  ThresholdsU th;
+  for (int i = 0; i < 15; ++i) th.t[i] = u->thresholds[i];
+  const int64_t nchunk = numel / 4;
+  const int64_t grid = grid_for(nchunk, 256 * kEncU, (int64_t)cus * 32);
+  hipLaunchKernelGGL(k_encode_uniform, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream,
+                     reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint16_t*>(codes_dev),
+                     nchunk, th);
   return launch_status();
 }
 

@@ -45,6 +45,19 @@ class Params(ctypes.Structure):
         return np.ctypeslib.as_array(self.thresholds)[: 1 << (self.bits - 1)].copy()
 
 
+class Uniform(ctypes.Structure):
+    """logbq_uniform: parameters of the asymmetric linear baseline (4-bit)."""
+    _fields_ = [("bits", c_int32), ("zero", c_int32), ("wmin", c_double), ("wmax", c_double),
+                ("scale", c_double), ("codebook", c_float * 16), ("thresholds", c_float * 15),
+                ("reserved", c_float)]
+
+    def codebook_array(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self.codebook).copy()
+
+    def thresholds_array(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self.thresholds).copy()
+
+
 _lib = None
 
 SIGNATURES = {
@@ -65,6 +78,9 @@ SIGNATURES = {
     "logbq_dequantize8": (c_int32, [c_void_p, c_int64, c_int64, POINTER(c_float), c_void_p,
                                     c_void_p]),
     "logbq_linear_path": (c_int32, [c_int32, c_int64, c_int64, c_int64, POINTER(c_int32)]),
+    "logbq_fit_uniform": (c_int32, [POINTER(c_float), c_int64, c_int32, POINTER(Uniform)]),
+    "logbq_encode_uniform": (c_int32, [c_void_p, c_int64, c_int64, POINTER(Uniform), c_void_p,
+                                       c_void_p]),
 }
 
 ABI_VERSION = 2
@@ -250,3 +266,28 @@ def linear_path(bits: int, m: int, k: int, n: int) -> str:
     _check(lib().logbq_linear_path(int(bits), int(m), int(k), int(n), ctypes.byref(out)),
            "logbq_linear_path")
     return PATH_NAMES[out.value]
+
+
+def fit_uniform(w, bits: int = 4) -> Uniform:
+    """logbq_fit_uniform on host float32 weights (numpy array or CPU torch tensor)."""
+    if hasattr(w, "detach"):
+        w = w.detach().cpu().numpy()
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    u = Uniform()
+    _check(lib().logbq_fit_uniform(w.ctypes.data_as(POINTER(c_float)), w.size, bits,
+                                   ctypes.byref(u)), "logbq_fit_uniform")
+    return u
+
+
+def encode_uniform(w, u: Uniform, out=None, stream=None):
+    """logbq_encode_uniform: float32 [N][K] device tensor -> packed uint8 [N][K/2] codes."""
+    import torch
+    if w.dtype != torch.float32 or w.dim() != 2 or not w.is_contiguous():
+        raise ValueError("w must be a contiguous 2-D float32 device tensor")
+    n, k = w.shape
+    if out is None:
+        out = torch.empty((n, k // 2), dtype=torch.uint8, device=w.device)
+    _check(lib().logbq_encode_uniform(c_void_p(w.data_ptr()), n, k, ctypes.byref(u),
+                                      c_void_p(out.data_ptr()), _stream(stream)),
+           "logbq_encode_uniform")
+    return out
