@@ -140,7 +140,8 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  * n >= 8192 and m = 3 at n >= 16384 (except m > 12 at n >= 16384); otherwise the
  * wavefront-reduced GEMV runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and
  * shapes whose activations do not fit the GEMV's registers) runs the stepped
- * dequantize-into-MFMA skinny GEMM. logbq_linear_path reports the choice.
+ * dequantize-into-MFMA skinny GEMM, except m > 96 at n >= 4096, which runs a K-quartered
+ * MFMA GEMM for sign-symmetric codebooks. logbq_linear_path reports the choice.
  * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment), HIP.
  */
 int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
@@ -216,7 +217,10 @@ typedef enum logbq_path {
   LOGBQ_PATH_NONE = 0,     /* m or n is 0 (nothing written) or k is 0 (zeros written)        */
   LOGBQ_PATH_GEMV = 1,     /* wavefront-reduced GEMV with the LDS pair table                  */
   LOGBQ_PATH_MFMA = 2,     /* stepped dequantize-into-MFMA skinny GEMM                        */
-  LOGBQ_PATH_SPLITK = 3    /* split-K dequantize-into-MFMA kernel (4-bit, 2 <= m <= 16)        */
+  LOGBQ_PATH_SPLITK = 3,   /* split-K dequantize-into-MFMA kernel (4-bit, 2 <= m <= 16)        */
+  LOGBQ_PATH_MFMA_KQ = 4   /* K-quartered dequantize-into-MFMA GEMM (4-bit, m > 96, n >= 4096);
+                              a codebook that is not sign-symmetric (never a fitted one) runs the
+                              stepped kernel instead                                          */
 } logbq_path;
 
 /*

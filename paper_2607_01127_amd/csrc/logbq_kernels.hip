@@ -909,6 +909,181 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
     }
 }
 
+// ------------------------------------------------------------------ MFMA GEMM, K quarters, m > 96
+//
+// For large batches k_mfma2's wavefronts (16 weight rows, every batch tile) re-read a fresh
+// activation fragment from LDS for every MFMA. Here a workgroup of 8 wavefronts still owns
+// 128 weight rows x 128 batch rows and walks K in steps of 256, but wavefront w takes weight
+// rows 64 (w % 2) .. +64 (four 16-row tiles) and the K quarter [256 step + 64 (w / 2), +64) of
+// every step, for all eight batch tiles: each activation fragment read from LDS feeds four
+// MFMAs and each dequantized weight fragment eight, and no code is loaded or dequantized twice.
+// The activation tile is staged through LDS as in k_mfma2 (same rotated layout); within its
+// quarter, lane (j, g) holds k in [.. + 16 g, +16) of its rows, i.e. MFMA c contracts
+// k = 256 step + 64 kq + 16 g + 8 c + 0..7 (code dword c of the lane's 8 bytes, activation unit
+// 8 kq + 2 g + c). The next batch tile's fragment is read while the current tile's four MFMAs
+// run. At the end the four K quarters are summed through LDS in a fixed order ((q0 + q2) +
+// (q1 + q3)), so results are deterministic. Measured on MI355X (8192 -> 28672): 86.8 us vs
+// 96.4 us for k_mfma2 at m = 128, 164 vs 183 us at m = 256; SQ_VALU_MFMA_BUSY_CYCLES puts the
+// MFMA pipes at about a third of the kernel's cycles, the rest going to the dequantization and
+// staging VALU work, LDS and the per-step barrier.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef const __attribute__((address_space(1))) u32x2* GlobalU32x2;
+
+__global__ __launch_bounds__(512) void k_mfma_kq(const uint8_t* __restrict__ codes,
+                                                 const uint16_t* __restrict__ x,
+                                                 float* __restrict__ y, int n_rows, int k_cols,
+                                                 int m_rows, LutBytes tb, float scale) {
+  constexpr int XV = 8;                  // 16-byte activation vectors per thread per step
+  __shared__ __attribute__((aligned(16))) uint16_t s_x[2][128][kM2Pad];
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int wave = t >> 6;
+  const int j = lane & 15;
+  const int g = lane >> 4;
+  const int wq = wave & 1;               // weight rows 64 wq .. +64 of the workgroup's 128
+  const int kq = wave >> 1;              // k in [256 step + 64 kq, +64) of every step
+  const int nb = blockIdx.x * 128 + 64 * wq;
+  const int mb = blockIdx.y * 128;
+  const int nsteps = (k_cols + kM2Step - 1) / kM2Step;
+  const int64_t row_bytes = (int64_t)k_cols / 2;
+  GlobalU8 crow[4];
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) {
+    const int r = nb + 16 * rt + j;
+    crow[rt] = (GlobalU8)codes + (int64_t)(r < n_rows ? r : n_rows - 1) * row_bytes;
+  }
+  // Activation tile: as k_mfma2 (clamped loads; rows past m_rows and k past k_cols are zeroed
+  // when written to LDS).
+  auto load_x = [&](int step, u32x4 (&v)[XV]) {
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int idx = t + 512 * i;
+      const int m = mb + (idx >> 5);
+      const int kk = step * kM2Step + (idx & 31) * 8;
+      const int mc = m < m_rows ? m : m_rows - 1;
+      const int kc = kk < k_cols ? kk : k_cols - 8;
+      v[i] = *(GlobalU32x4)((const __attribute__((address_space(1))) uint16_t*)x +
+                            (int64_t)mc * k_cols + kc);
+    }
+  };
+  auto store_x = [&](int step, int slot, const u32x4 (&v)[XV]) {
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int idx = t + 512 * i;
+      const uint32_t keep = 0u - (uint32_t)((mb + (idx >> 5) < m_rows) &
+                                            (step * kM2Step + (idx & 31) * 8 < k_cols));
+      u32x4 w = permute_x8(v[i]);
+      w.x &= keep; w.y &= keep; w.z &= keep; w.w &= keep;
+      const int r = idx >> 5;
+      *reinterpret_cast<u32x4*>(&s_x[slot][r][x_unit(r, idx & 31) * 8]) = w;
+    }
+  };
+  // Codes of a step for row tile rt: lane (j, g) takes the 8 bytes of k in
+  // [256 step + 64 kq + 16 g, +16) of row nb + 16 rt + j (clamped into the row; a clamped piece
+  // only meets zero activations).
+  auto load_codes = [&](int step, u32x2 (&q)[4]) {
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      int64_t off = (int64_t)step * 128 + 32 * kq + 8 * g;
+      off = off + 8 <= row_bytes ? off : row_bytes - 8;
+      q[rt] = *(GlobalU32x2)(crow[rt] + off);
+    }
+  };
+  float4v acc[8][4];
+#pragma unroll
+  for (int bt = 0; bt < 8; ++bt)
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[bt][rt][r] = 0.0f;
+
+  // Pipeline: activation tile s is loaded into registers during step s - 2 and written to LDS
+  // slot s & 1 at the end of step s - 1; the codes of step s are loaded during step s - 1.
+  u32x2 q[2][4];
+  u32x4 xr[XV];
+  auto clampstep = [&](int t2) { return t2 < nsteps ? t2 : nsteps - 1; };
+  load_x(0, xr);
+  load_codes(0, q[0]);
+  store_x(0, 0, xr);
+  load_x(clampstep(1), xr);
+  __syncthreads();
+
+  for (int s0 = 0; s0 < nsteps; s0 += 2) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int step = s0 + u;
+      if (step >= nsteps) break;
+      load_codes(clampstep(step + 1), q[u ^ 1]);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        half8v b[4];
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+          uint32_t bw[4];
+          dequant_dword(c == 0 ? q[u][rt].x : q[u][rt].y, tb, bw);
+          b[rt] = __builtin_bit_cast(half8v, u32x4{bw[0], bw[1], bw[2], bw[3]});
+        }
+        const uint16_t* abase = &s_x[u][j][x_unit(j, 8 * kq + 2 * g + c) * 8];
+        half8v a_cur = *reinterpret_cast<const half8v*>(abase);
+#pragma unroll
+        for (int bt = 0; bt < 8; ++bt) {
+          half8v a_nxt = a_cur;
+          if (bt + 1 < 8) a_nxt = *reinterpret_cast<const half8v*>(abase + 16 * (bt + 1) * kM2Pad);
+#pragma unroll
+          for (int rt = 0; rt < 4; ++rt)
+            acc[bt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a_cur, b[rt], acc[bt][rt], 0, 0, 0);
+          a_cur = a_nxt;
+        }
+      }
+      store_x(step + 1, u ^ 1, xr);
+      load_x(clampstep(step + 2), xr);
+      __syncthreads();
+    }
+  }
+
+  // Sum the four K quarters through LDS (the activation slots are free after the last
+  // barrier): quarters 2, 3 are added to 0, 1, then 1 to 0, which stores. Each of the four
+  // slots holds one wavefront's 8 x 4 tiles (8192 floats).
+  float* s_red = reinterpret_cast<float*>(&s_x[0][0][0]);
+  static_assert(sizeof(s_x) >= 4 * 8192 * sizeof(float), "reduction slots fit the tile buffers");
+  auto red_slot = [&](int w_q, int half) { return s_red + (size_t)(w_q * 2 + half) * 8192; };
+  auto put = [&](float* dst) {
+#pragma unroll
+    for (int bt = 0; bt < 8; ++bt)
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+        *reinterpret_cast<float4v*>(dst + ((bt * 4 + rt) * 64 + lane) * 4) = acc[bt][rt];
+  };
+  __syncthreads();
+  auto add = [&](const float* src) {
+#pragma unroll
+    for (int bt = 0; bt < 8; ++bt)
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+        acc[bt][rt] += *reinterpret_cast<const float4v*>(src + ((bt * 4 + rt) * 64 + lane) * 4);
+  };
+  if (kq >= 2) put(red_slot(wq, kq - 2));
+  __syncthreads();
+  if (kq < 2) add(red_slot(wq, kq));
+  __syncthreads();
+  if (kq == 1) put(red_slot(wq, 0));
+  __syncthreads();
+  if (kq == 0) {
+    add(red_slot(wq, 0));
+#pragma unroll
+    for (int bt = 0; bt < 8; ++bt)
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        const int row = nb + 16 * rt + j;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb + 16 * bt + 4 * g + r;
+          if (m < m_rows && row < n_rows) y[(int64_t)m * n_rows + row] = acc[bt][rt][r] * scale;
+        }
+      }
+  }
+}
+
 // ------------------------------------------------------------------ split-K MFMA, m <= 16
 //
 // For one batch tile (m <= 16) and K = 256 ND (ND = 4, 8, 16, 32, i.e. K = 1024 .. 8192): a
@@ -1283,6 +1458,19 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
   return launch_status();
 }
 
+// K-quartered MFMA path (4-bit, sign-symmetric codebooks): m > 96 at N >= 4096.
+bool kq_shape(int M, int64_t N) { return M > 96 && N >= 4096; }
+
+int32_t launch_kq(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st) {
+  const int N = (int)j.n;
+  LutBytes tb = {0, 0, 0, 0};
+  float scale;
+  if (!make_lut_bytes(j.codebook, &tb, &scale)) return launch_mfma<4>(x, M, K, j, st);
+  dim3 grid((unsigned)((N + 127) / 128), (unsigned)((M + 127) / 128));
+  hipLaunchKernelGGL(k_mfma_kq, grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, tb, scale);
+  return launch_status();
+}
+
 // Split-K MFMA path: 4-bit codes, 2 <= m <= 16, K in {1024, 2048, 4096, 8192}.
 bool sk_shape(int M, int K) {
   return M >= 2 && M <= 16 && (K == 1024 || K == 2048 || K == 4096 || K == 8192);
@@ -1324,6 +1512,10 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob& j, hipStream
 // (m, k, N), so every linear of a grouped call runs the kernel that a single call would run,
 // with the same result bits.
 //
+// Above m = 96 at N >= 4096 the K-quartered kernel replaces the stepped one for 4-bit codes with
+// sign-symmetric codebooks (7-11 % faster on the 8192 x 28672 and 4096 x 14336 layers; slower
+// on narrow layers, which have too few 128-row workgroups).
+//
 // Where the split-K MFMA kernel applies (4-bit codes, 2 <= m <= 16, K = 1, 2, 4 or 8 Ki), it
 // takes m >= 5, m = 4 at N >= 8192 and m = 3 at N >= 16384, except m > 12 at N >= 16384
 // (measured: it beats the GEMV there and the stepped MFMA kernel everywhere except the widest
@@ -1337,6 +1529,7 @@ int choose_path(int M, int K, int64_t N) {
     return LOGBQ_PATH_SPLITK;
   if (M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl) && !(M >= 3 && (int64_t)M * N > 65536))
     return LOGBQ_PATH_GEMV;
+  if (BITS == 4 && kq_shape(M, N)) return LOGBQ_PATH_MFMA_KQ;
   return LOGBQ_PATH_MFMA;
 }
 
@@ -1375,6 +1568,9 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
     } else if (path == LOGBQ_PATH_GEMV) {
       gl[ng++] = live[a];
       grows += j.n;
+    } else if (path == LOGBQ_PATH_MFMA_KQ) {
+      const int32_t r = launch_kq(x, M, K, j, st);
+      if (r != LOGBQ_OK) return r;
     } else {
       const int32_t r = launch_mfma<BITS>(x, M, K, j, st);
       if (r != LOGBQ_OK) return r;

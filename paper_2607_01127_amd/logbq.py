@@ -256,11 +256,11 @@ def dequantize8(codes, codebook, out=None, stream=None):
     return out
 
 
-PATH_NAMES = {0: "none", 1: "gemv", 2: "mfma", 3: "splitk"}
+PATH_NAMES = {0: "none", 1: "gemv", 2: "mfma", 3: "splitk", 4: "mfma_kq"}
 
 
 def linear_path(bits: int, m: int, k: int, n: int) -> str:
-    """logbq_linear_path: name of the kernel ("none", "gemv", "mfma" or "splitk") that
+    """logbq_linear_path: name of the kernel ("none", "gemv", "mfma", "splitk" or "mfma_kq") that
     linear (bits 4) or linear8 (bits 8) runs for an [m][k] x [n][k] call. Host only."""
     out = c_int32(0)
     _check(lib().logbq_linear_path(int(bits), int(m), int(k), int(n), ctypes.byref(out)),

@@ -245,7 +245,10 @@ def test_linear_path_rule():
     assert lp(4, 3, 4096, 16384) == "splitk" and lp(4, 3, 4096, 8192) == "gemv"
     assert lp(4, 4, 4096, 8192) == "splitk" and lp(4, 4, 4096, 4096) == "gemv"
     assert lp(4, 8, 8192 + 32, 28672) == "mfma"    # K outside the split-K set
-    assert lp(4, 17, 8192, 2048) == "mfma" and lp(4, 128, 8192, 28672) == "mfma"
+    assert lp(4, 17, 8192, 2048) == "mfma" and lp(4, 96, 8192, 28672) == "mfma"
+    # K-quartered MFMA GEMM: 4-bit, m > 96 at N >= 4096
+    assert lp(4, 128, 8192, 28672) == "mfma_kq" and lp(4, 97, 1024, 4096) == "mfma_kq"
+    assert lp(4, 128, 1024, 4095) == "mfma" and lp(8, 128, 8192, 28672) == "mfma"
     # 8-bit codes: GEMV unless m >= 3 and m * N > 65536, else the stepped MFMA kernel
     assert lp(8, 1, 8192, 28672) == "gemv" and lp(8, 2, 8192, 28672) == "gemv"
     assert lp(8, 8, 8192, 28672) == "mfma" and lp(8, 8, 2048, 8192) == "gemv"

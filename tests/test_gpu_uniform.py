@@ -69,8 +69,11 @@ def test_encode_uniform_boundaries():
     assert np.array_equal(got, O.pack(U.uniform_encode(x, f.scale, f.zero)))
 
 
+# (4096, 1024, 128) has the K-quartered kernel's shape; this codebook is not sign-symmetric, so
+# it falls back to the stepped kernel's LDS-table form.
 @pytest.mark.parametrize("n,k,m", [(2048, 2048, 1), (8192, 2048, 4), (8192, 2048, 8),
-                                   (4096, 4096, 32), (1000, 4128, 77), (2051, 1024, 128)])
+                                   (4096, 4096, 32), (1000, 4128, 77), (2051, 1024, 128),
+                                   (4096, 1024, 128)])
 def test_linear_on_uniform_codes(n, k, m):
     _say(f"uniform linear n={n} k={k} m={m} path={L.linear_path(4, m, k, n)}")
     w = _tensor(n, k, [31, n, k, 0])
