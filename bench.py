@@ -256,6 +256,86 @@ def bench_quality(torch, L, inputs, dev, stream, layer_codes, layer_cb, steps, w
     return out
 
 
+def bench_gptq(torch, L, inputs, dev, stream, with_cpu):
+    """GPTQ calibration (logbq_gptq) of the 2048 x 2048 and 2048 -> 8192 tensors with seeded
+    synthetic calibration inputs (16384 tokens; per-channel scales exp(N(0, 0.25)) plus a shared
+    rank-8 part, so the Hessian is far from diagonal). The factor U of the damped inverse
+    Hessian is the caller's input; it is formed here with torch in float64 (outside the timed
+    region). Reported: GPU time of the calibration and the layer-output error
+    ||(W - W_hat) X^T|| / ||W X^T|| of round-to-nearest and of GPTQ, for LogbQuant and for the
+    asymmetric linear baseline."""
+    out = {}
+    tokens = 16384
+    for name in ("linear_2048x2048", "up_2048x8192_outliers"):
+        wl = inputs.WORKLOADS[name]
+        lin = wl["layers"][0]
+        n, k = lin.n, lin.k
+        log(f"gptq {name}")
+        w = inputs.student_t_weights(n, k, wl["nu"], wl["scale"], seed=[wl["cfg"], 0, 0, 0],
+                                     device=dev, outlier_frac=wl.get("outlier_frac", 0.0))
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(wl["cfg"] * 1000 + 7)
+        scale = torch.exp(0.5 * torch.randn(k, generator=gen, device=dev))
+        x = (torch.randn(tokens, k, generator=gen, device=dev) * scale +
+             torch.randn(tokens, 8, generator=gen, device=dev) @ torch.randn(8, k, generator=gen, device=dev) * 0.5)
+        x64 = x.double()
+        h = 2.0 * (x64.T @ x64) / tokens
+        h += 0.01 * torch.mean(torch.diag(h)) * torch.eye(k, dtype=torch.float64, device=dev)
+        u = torch.linalg.cholesky(torch.cholesky_inverse(torch.linalg.cholesky(h)), upper=True)
+        u = u.float().contiguous()
+        w_host = w.cpu().numpy()
+        y_ref = w.double() @ x64.T
+        ynorm = float(y_ref.norm())
+        row = {"tokens": tokens}
+        for scheme in ("logbquant", "uniform"):
+            if scheme == "logbquant":
+                params = L.fit(w_host)
+                book = params
+                rtn_codes, _ = L.encode(w, params)
+            else:
+                params = L.fit_uniform(w_host)
+                book = params.codebook_array()
+                rtn_codes = L.encode_uniform(w, params)
+            ws = torch.empty((n, L.GPTQ_BLOCK), dtype=torch.float32, device=dev)
+            codes = torch.empty((n, k // 2), dtype=torch.uint8, device=dev)
+            times = []
+            for rep in range(4):
+                wc = w.clone()
+                torch.cuda.synchronize()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                L.gptq(wc, u, params, out_codes=codes, workspace=ws, stream=stream)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                times.append(e0.elapsed_time(e1))
+
+            def err(c):
+                wh = L.dequantize(c, book).double()
+                return float(((w.double() - wh) @ x64.T).norm()) / ynorm
+            row[scheme] = {"gptq_ms": sorted(times)[1], "launches": 2 * (-(-k // L.GPTQ_BLOCK)) - 1,
+                           "out_err_rtn": err(rtn_codes), "out_err_gptq": err(codes)}
+        if with_cpu:
+            from oracle import gptq_oracle as G
+            from oracle import logbq_oracle as O
+            rows_sample = 128
+            r = O.fit(w_host)
+            lut = O.codebook(r.base, r.shift)
+
+            def q(col):
+                c = O.encode(col, r.base, r.shift)
+                return c, lut[c]
+            t0 = time.perf_counter()
+            G.gptq(w_host[:rows_sample], u.cpu().numpy(), q)
+            dt = time.perf_counter() - t0
+            row["cpu_oracle"] = {"rows": rows_sample, "s": dt,
+                                 "s_scaled_to_all_rows": dt * n / rows_sample}
+        out[name] = row
+        del w, x, x64, h, u, y_ref
+        torch.cuda.empty_cache()
+    return out
+
+
 def bench_layer8(torch, L, inputs, dev, stream, ms, steps, warmup):
     """The 8192 x 28672 layer at 8 bits (q_max = 127, eps = 1e-6): one code byte per weight,
     256-entry table. Same weights and activations as the 4-bit layer."""
@@ -570,10 +650,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10000,
                     help="untimed launches before the timed ones (about 0.2 s of GPU work at M = 1)")
     ap.add_argument("--quick", action="store_true", help="main layer only, no extra rows")
-    ap.add_argument("--rows", default="layer,layer8,small,decode1b,decode8b,quality",
+    ap.add_argument("--rows", default="layer,layer8,small,decode1b,decode8b,quality,gptq",
                     help="comma list of extra rows: layer (M sweep + encode), layer8 (the same "
                          "layer at 8 bits), small, decode1b, decode8b, quality (LogbQuant "
-                         "against the asymmetric linear baseline)")
+                         "against the asymmetric linear baseline), gptq (calibration)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device-to-device copy (calibrates the HBM byte "
@@ -614,6 +694,8 @@ def main():
     if "quality" in want:
         rows["quality_vs_uniform"] = bench_quality(torch, L, inputs, dev, stream, codes, cb,
                                                    args.steps, args.warmup)
+    if "gptq" in want:
+        rows["gptq"] = bench_gptq(torch, L, inputs, dev, stream, not args.no_cpu)
     log("HBM read ceiling (4 GiB)")
     ceiling = read_ceiling(torch, stream)
     torch.cuda.empty_cache()

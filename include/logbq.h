@@ -212,6 +212,32 @@ int32_t logbq_fit_uniform(const float* w_host, int64_t numel, int32_t bits, logb
 int32_t logbq_encode_uniform(const float* w_dev, int64_t n, int64_t k, const logbq_uniform* u,
                              uint8_t* codes_dev, void* stream);
 
+/*
+ * logbq_gptq -- GPTQ post-training calibration (the calibration used for every model in Sec. 4)
+ * of one weight matrix with a fixed 4-bit codebook in its inner loop: LogbQuant (Eq. 1-2, from
+ * `p`) or the asymmetric linear baseline (Sec. 2, from `uniform`). Columns are quantized in
+ * order in blocks of 128; after column i, err = (w_i - q_i) / U_ii is subtracted, times U_ij,
+ * from every later column j of its block, and after the block sum_i err_i U_ij from every
+ * later column. All arithmetic is float32 in a fixed order, with no fused multiply-add:
+ * err = (w - q) / U_ii; in the block w_j = w_j - err * U_ij; after it acc = acc + err_i * U_ij
+ * over the block's columns in increasing i from 0, then w_j = w_j - acc.
+ *   w_dev     : device, [n][k] float32, in/out. On return column i holds the value it had
+ *               when it was quantized (the error-compensated weights).
+ *   u_dev     : device, [k][k] float32 row-major: the upper Cholesky factor U of the damped
+ *               inverse Hessian, H^-1 = U^T U (only j >= i is read; U_ii > 0).
+ *   p, uniform: host; exactly one is non-NULL (bits 4). Its codebook is fixed for the whole
+ *               loop (fit it on the original weights).
+ *   err_dev   : device, [n][128] float32 workspace owned by the caller (overwritten).
+ *   codes_dev : device, [n][k/2] packed codes, written (layout as logbq_encode; nibbles are
+ *               sign + magnitude for LogbQuant, the unsigned code for the baseline).
+ * Enqueues 2 * ceil(k / 128) kernels on `stream`. Errors: INVALID_ARG (null pointers, both or
+ * neither of p / uniform, bad thresholds), UNSUPPORTED (bits, k % 32, alignment,
+ * n > 1048560), HIP.
+ */
+int32_t logbq_gptq(float* w_dev, int64_t n, int64_t k, const float* u_dev, const logbq_params* p,
+                   const logbq_uniform* uniform, float* err_dev, uint8_t* codes_dev,
+                   void* stream);
+
 /* Kernel that logbq_linear (bits 4) or logbq_linear8 (bits 8) runs for a call of a shape. */
 typedef enum logbq_path {
   LOGBQ_PATH_NONE = 0,     /* m or n is 0 (nothing written) or k is 0 (zeros written)        */

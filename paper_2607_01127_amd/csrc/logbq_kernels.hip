@@ -660,6 +660,122 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
   }
 }
 
+// ------------------------------------------------------------------ GPTQ calibration
+//
+// Rows of W evolve independently given U, so the column loop runs one wavefront per row: lane
+// l holds columns i1 + l and i1 + 64 + l of the current block. Column i's value is read across
+// the wavefront (v_readlane), quantized to the fixed codebook by threshold counting (the same
+// decision as the encoders), and err = (w - q) / U_ii is subtracted, times U_ij, from the
+// block's later columns held by the lanes; the block's rows of U sit in LDS. After the block a
+// second kernel subtracts sum_i err_i U_ij from every later column (16 rows x 64 columns per
+// workgroup, the block's errors and U rows staged in LDS). Every operation is a separately
+// rounded float32 operation in a fixed order (no contraction), which fixes the result bits.
+constexpr int kGptqBlock = 128;
+
+struct GptqQuant {
+  float cb[16];      // value of each code
+  float th[15];      // LogbQuant: 7 magnitude thresholds on |w|; baseline: 15 on w
+  int uniform;       // 0: sign + magnitude (LogbQuant), 1: unsigned code (baseline)
+};
+
+__device__ __forceinline__ uint32_t gptq_code(float w, const GptqQuant& qz) {
+  uint32_t c = 0;
+  if (qz.uniform) {
+#pragma unroll
+    for (int t = 0; t < 15; ++t) c += (w >= qz.th[t]) ? 1u : 0u;
+  } else {
+    const float a = __builtin_fabsf(w);
+#pragma unroll
+    for (int t = 0; t < 7; ++t) c += (a >= qz.th[t]) ? 1u : 0u;
+    if (w < 0.0f && c != 0u) c |= 8u;
+  }
+  return c;
+}
+
+__global__ __launch_bounds__(512) void k_gptq_panel(float* __restrict__ w, int n_rows, int k_cols,
+                                                    const float* __restrict__ u, int i1, int nb,
+                                                    GptqQuant qz, float* __restrict__ err,
+                                                    uint8_t* __restrict__ codes) {
+#pragma clang fp contract(off)
+  __shared__ float s_u[kGptqBlock * kGptqBlock];
+  for (int idx = threadIdx.x; idx < nb * nb; idx += 512) {
+    const int a = idx / nb, b = idx % nb;
+    s_u[a * kGptqBlock + b] = u[(int64_t)(i1 + a) * k_cols + i1 + b];
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 8 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  float* wr = w + (int64_t)row * k_cols + i1;
+  float p0 = lane < nb ? wr[lane] : 0.0f;
+  float p1 = 64 + lane < nb ? wr[64 + lane] : 0.0f;
+  uint32_t c0 = 0, c1 = 0;
+  for (int i = 0; i < nb; ++i) {
+    const float wi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+        __builtin_bit_cast(int, i < 64 ? p0 : p1), i & 63));
+    const uint32_t c = gptq_code(wi, qz);
+    const float e = __fdiv_rn(wi - qz.cb[c], s_u[i * kGptqBlock + i]);
+    if (lane == (i & 63)) {
+      if (i < 64) c0 = c; else c1 = c;
+    }
+    if (lane == 0) err[(int64_t)row * kGptqBlock + i] = e;
+    const float* ui = s_u + i * kGptqBlock;
+    if (lane > i && lane < nb) p0 = p0 - e * ui[lane];
+    if (64 + lane > i && 64 + lane < nb) p1 = p1 - e * ui[64 + lane];
+  }
+  if (lane < nb) wr[lane] = p0;
+  if (64 + lane < nb) wr[64 + lane] = p1;
+  // Byte b of the block holds columns 2b (low nibble) and 2b + 1.
+  const int src = (2 * lane) & 63;
+  const uint32_t lo0 = __builtin_amdgcn_ds_bpermute(src << 2, (int)c0);
+  const uint32_t hi0 = __builtin_amdgcn_ds_bpermute((src + 1) << 2, (int)c0);
+  const uint32_t lo1 = __builtin_amdgcn_ds_bpermute(src << 2, (int)c1);
+  const uint32_t hi1 = __builtin_amdgcn_ds_bpermute((src + 1) << 2, (int)c1);
+  const uint32_t byte = lane < 32 ? (lo0 | (hi0 << 4)) : (lo1 | (hi1 << 4));
+  if (2 * lane < nb) codes[(int64_t)row * (k_cols / 2) + i1 / 2 + lane] = (uint8_t)byte;
+}
+
+__global__ __launch_bounds__(256) void k_gptq_trail(float* __restrict__ w, int n_rows, int k_cols,
+                                                    const float* __restrict__ u, int i1, int nb,
+                                                    const float* __restrict__ err) {
+#pragma clang fp contract(off)
+  __shared__ float s_e[16][kGptqBlock];
+  __shared__ __attribute__((aligned(16))) float s_u[kGptqBlock][64];
+  const int i2 = i1 + nb;
+  const int r0 = blockIdx.y * 16;
+  const int c0 = i2 + blockIdx.x * 64;
+  for (int idx = threadIdx.x; idx < 16 * kGptqBlock; idx += 256) {
+    const int r = idx / kGptqBlock, i = idx % kGptqBlock;
+    s_e[r][i] = (r0 + r < n_rows && i < nb) ? err[(int64_t)(r0 + r) * kGptqBlock + i] : 0.0f;
+  }
+  for (int idx = threadIdx.x; idx < kGptqBlock * 64; idx += 256) {
+    const int i = idx / 64, c = idx % 64;
+    s_u[i][c] = (i < nb && c0 + c < k_cols) ? u[(int64_t)(i1 + i) * k_cols + c0 + c] : 0.0f;
+  }
+  __syncthreads();
+  const int r = threadIdx.x >> 4;          // 16 rows
+  const int cq = (threadIdx.x & 15) * 4;   // 4 columns each
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int i = 0; i < nb; ++i) {
+    const float e = s_e[r][i];
+    const f32x4 uv = *reinterpret_cast<const f32x4*>(&s_u[i][cq]);
+    acc[0] = acc[0] + e * uv.x;
+    acc[1] = acc[1] + e * uv.y;
+    acc[2] = acc[2] + e * uv.z;
+    acc[3] = acc[3] + e * uv.w;
+  }
+  const int row = r0 + r;
+  if (row >= n_rows) return;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int col = c0 + cq + q;
+    if (col < k_cols) {
+      float* p = w + (int64_t)row * k_cols + col;
+      *p = *p - acc[q];
+    }
+  }
+}
+
 // ------------------------------------------------------------------ MFMA skinny GEMM, register dequant
 //
 // For sign-symmetric codebooks (codebook[8 + k] = -codebook[k], codebook[k] >= 0 for k < 8,
@@ -1674,6 +1790,54 @@ int32_t logbq_encode_uniform(const float* w_dev, int64_t n, int64_t k, const log
                      reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint16_t*>(codes_dev),
                      nchunk, th);
   return launch_status();
+}
+
+int32_t logbq_gptq(float* w_dev, int64_t n, int64_t k, const float* u_dev, const logbq_params* p,
+                   const logbq_uniform* uniform, float* err_dev, uint8_t* codes_dev,
+                   void* stream) {
+  if (n < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
+  if ((p == nullptr) == (uniform == nullptr)) return LOGBQ_ERR_INVALID_ARG;
+  if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
+  if (n > INT32_MAX || k > INT32_MAX || (n != 0 && (n * k) / n != k)) return LOGBQ_ERR_UNSUPPORTED;
+  if (n > 65535LL * 16) return LOGBQ_ERR_UNSUPPORTED;   // rows are the after-block grid's y
+  GptqQuant qz;
+  std::memset(&qz, 0, sizeof(qz));
+  if (p) {
+    if (p->bits != 4 || p->qmax != 7) return LOGBQ_ERR_UNSUPPORTED;
+    for (int i = 0; i < 16; ++i) qz.cb[i] = p->codebook[i];
+    for (int i = 0; i < 7; ++i) qz.th[i] = p->thresholds[i];
+    for (int i = 7; i < 15; ++i) qz.th[i] = INFINITY;
+    qz.uniform = 0;
+  } else {
+    if (uniform->bits != 4) return LOGBQ_ERR_UNSUPPORTED;
+    for (int i = 0; i < 16; ++i) qz.cb[i] = uniform->codebook[i];
+    for (int i = 0; i < 15; ++i) qz.th[i] = uniform->thresholds[i];
+    qz.uniform = 1;
+  }
+  for (int i = 0; i < 16; ++i)
+    if (!std::isfinite(qz.cb[i])) return LOGBQ_ERR_INVALID_ARG;
+  for (int i = 0; i < 15; ++i) {
+    if (std::isnan(qz.th[i])) return LOGBQ_ERR_INVALID_ARG;
+    if (i > 0 && qz.th[i] < qz.th[i - 1]) return LOGBQ_ERR_INVALID_ARG;
+  }
+  if (n == 0 || k == 0) return LOGBQ_OK;
+  if (!w_dev || !u_dev || !err_dev || !codes_dev) return LOGBQ_ERR_INVALID_ARG;
+  if (!aligned16(w_dev) || !aligned16(u_dev) || !aligned16(err_dev) || !aligned16(codes_dev))
+    return LOGBQ_ERR_UNSUPPORTED;
+  const hipStream_t st = (hipStream_t)stream;
+  const int N = (int)n, K = (int)k;
+  for (int i1 = 0; i1 < K; i1 += kGptqBlock) {
+    const int nb = K - i1 < kGptqBlock ? K - i1 : kGptqBlock;
+    hipLaunchKernelGGL(k_gptq_panel, dim3((unsigned)((N + 7) / 8)), dim3(512), 0, st, w_dev, N, K,
+                       u_dev, i1, nb, qz, err_dev, codes_dev);
+    if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
+    if (i1 + nb < K) {
+      hipLaunchKernelGGL(k_gptq_trail, dim3((unsigned)((K - i1 - nb + 63) / 64), (unsigned)((N + 15) / 16)),
+                         dim3(256), 0, st, w_dev, N, K, u_dev, i1, nb, err_dev);
+      if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
+    }
+  }
+  return LOGBQ_OK;
 }
 
 int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const float* codebook,

@@ -81,6 +81,8 @@ SIGNATURES = {
     "logbq_fit_uniform": (c_int32, [POINTER(c_float), c_int64, c_int32, POINTER(Uniform)]),
     "logbq_encode_uniform": (c_int32, [c_void_p, c_int64, c_int64, POINTER(Uniform), c_void_p,
                                        c_void_p]),
+    "logbq_gptq": (c_int32, [c_void_p, c_int64, c_int64, c_void_p, POINTER(Params),
+                             POINTER(Uniform), c_void_p, c_void_p, c_void_p]),
 }
 
 ABI_VERSION = 2
@@ -291,3 +293,32 @@ def encode_uniform(w, u: Uniform, out=None, stream=None):
                                       c_void_p(out.data_ptr()), _stream(stream)),
            "logbq_encode_uniform")
     return out
+
+
+GPTQ_BLOCK = 128
+
+
+def gptq(w, u, params, out_codes=None, workspace=None, stream=None):
+    """logbq_gptq: GPTQ calibration of the float32 [N][K] device tensor `w` (updated in place to
+    the error-compensated weights) with the upper factor `u` ([K][K] float32 device tensor of
+    the damped inverse Hessian) and a fixed codebook: `params` is a Params (LogbQuant, from
+    fit) or a Uniform (the asymmetric linear baseline, from fit_uniform). Returns packed uint8
+    [N][K/2] codes."""
+    import torch
+    if w.dtype != torch.float32 or w.dim() != 2 or not w.is_contiguous():
+        raise ValueError("w must be a contiguous 2-D float32 device tensor")
+    n, k = w.shape
+    if u.dtype != torch.float32 or tuple(u.shape) != (k, k) or not u.is_contiguous():
+        raise ValueError("u must be a contiguous [K][K] float32 device tensor")
+    if out_codes is None:
+        out_codes = torch.empty((n, k // 2), dtype=torch.uint8, device=w.device)
+    if workspace is None:
+        workspace = torch.empty((n, GPTQ_BLOCK), dtype=torch.float32, device=w.device)
+    pp = ctypes.byref(params) if isinstance(params, Params) else None
+    up = ctypes.byref(params) if isinstance(params, Uniform) else None
+    if pp is None and up is None:
+        raise ValueError("params must be a Params or a Uniform")
+    _check(lib().logbq_gptq(c_void_p(w.data_ptr()), n, k, c_void_p(u.data_ptr()), pp, up,
+                            c_void_p(workspace.data_ptr()), c_void_p(out_codes.data_ptr()),
+                            _stream(stream)), "logbq_gptq")
+    return out_codes
