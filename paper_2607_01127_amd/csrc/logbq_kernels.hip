@@ -423,8 +423,10 @@ __device__ __forceinline__ void gemv_row(const u32x4 (&q)[CPL],
 }
 
 template <int BITS, int M, int CPL, bool SPLITK, int NBUF>
-__global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, int k_cols, int wk_arg,
-                                              int stage_x, GemvSegs<BITS> segs) {
+__global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x,
+                                              const uint8_t* codes0, int k_cols, int n_rows0,
+                                              int nseg, int wk_arg, int stage_x,
+                                              GemvSegs<BITS> segs) {
   constexpr int CW = kChunkW<BITS>;   // weights per 16-byte code chunk
   constexpr int CX = kChunkX<BITS>;   // activation dwords per chunk
   const int wk = SPLITK ? wk_arg : 1;
@@ -436,18 +438,30 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x, in
   __shared__ uint32_t s_ticket;
 
   // Segment of this workgroup: a uniform index, so its fields are scalar kernel-argument loads.
+  // The first segment's codes pointer and row count (and the segment count) also come as
+  // leading scalar arguments, which the hardware preloads into SGPRs: a one-segment launch
+  // issues its first code loads without waiting for the segment table.
   const int bid = blockIdx.x;
   int si = 0;
+  const uint8_t* codes = codes0;
+  int n_rows = n_rows0;
+  int wg_begin = 0;
+  int next_begin = (int)gridDim.x;
+  if (nseg > 1) {
+    // A real branch (the empty asm keeps it from being turned into loads and selects that
+    // would make the one-segment path wait for the table as well).
+    asm volatile("" ::: "memory");
 #pragma unroll
-  for (int i = 1; i < kMaxSegs; ++i)
-    if (i < segs.count && bid >= segs.s[i].wg_begin) si = i;
-  const uint8_t* codes = segs.s[si].codes;
+    for (int i = 1; i < kMaxSegs; ++i)
+      if (i < nseg && bid >= segs.s[i].wg_begin) si = i;
+    codes = segs.s[si].codes;
+    n_rows = segs.s[si].n_rows;
+    wg_begin = segs.s[si].wg_begin;
+    next_begin = (si + 1 < nseg) ? segs.s[si + 1].wg_begin : (int)gridDim.x;
+  }
   float* __restrict__ y = segs.s[si].y;
-  const int n_rows = segs.s[si].n_rows;
   const int iters = segs.s[si].iters;
   const float scale = segs.s[si].scale;
-  const int wg_begin = segs.s[si].wg_begin;
-  const int next_begin = (si + 1 < segs.count) ? segs.s[si + 1].wg_begin : (int)gridDim.x;
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
@@ -1436,10 +1450,10 @@ void launch_gemv(int grid, hipStream_t st, const uint16_t* x, int k, int wk, int
   constexpr int NBUF = (CPL <= 2 && M <= 2) ? 3 : 2;
   if (wk == 1)
     hipLaunchKernelGGL((k_gemv<BITS, M, CPL, false, NBUF>), dim3((unsigned)grid), dim3(512), 0,
-                       st, x, k, 1, stage_x, segs);
+                       st, x, segs.s[0].codes, k, segs.s[0].n_rows, segs.count, 1, stage_x, segs);
   else
     hipLaunchKernelGGL((k_gemv<BITS, M, CPL, true, NBUF>), dim3((unsigned)grid), dim3(512), 0,
-                       st, x, k, wk, stage_x, segs);
+                       st, x, segs.s[0].codes, k, segs.s[0].n_rows, segs.count, wk, stage_x, segs);
 }
 
 template <int BITS>
