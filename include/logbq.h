@@ -135,7 +135,7 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  *               so the call is capturable in a HIP graph. Entries are rounded to float16 after
  *               a common power-of-two scaling, exact in the result up to float16 rounding.
  *   y_dev     : device, [m][n] float32, written.
- * Accumulation is float32. Three kernels, chosen from (m, k, n) alone: for 2 <= m <= 16 and
+ * Accumulation is float32. Four kernels, chosen from (m, k, n) alone: for 2 <= m <= 16 and
  * k in {1024, 2048, 4096, 8192}, a split-K dequantize-into-MFMA kernel takes m >= 5, m = 4 at
  * n >= 8192 and m = 3 at n >= 16384 (except m > 12 at n >= 16384); otherwise the
  * wavefront-reduced GEMV runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and

@@ -15,6 +15,13 @@
 //   k_mfma_sk  the same product for 2 <= m <= 16 split over K: the 8 wavefronts of a workgroup
 //              share a block of 16 rows (one K slice each, activations held in registers) and
 //              sum their partial tiles through LDS.
+//   k_mfma_kq  the same product for m > 96: each wavefront takes 64 weight rows and one K
+//              quarter of every step for all 128 batch rows of the workgroup; the quarters'
+//              tiles are summed through LDS at the end.
+//   k_encode8, k_dequant8, k_gemv<8, ...>, k_mfma2<8, ...>  the same on 8-bit codes.
+//   k_encode_uniform  codes of the asymmetric linear baseline (Sec. 2), for comparisons.
+//   k_gptq_panel, k_gptq_trail  GPTQ calibration with a fixed codebook (one wavefront per row
+//              within a block of 128 columns; the block's errors applied to the later columns).
 //
 // The float16 tables hold codebook / 2^e with 2^e chosen so that the largest entry lies in
 // [2^14, 2^15); the result is multiplied back by 2^e (exact). Lookup replaces evaluating
