@@ -1239,12 +1239,28 @@ __global__ __launch_bounds__(512) void k_mfma_kq(const uint8_t* __restrict__ cod
 // barrier per block); each of the first 256 threads owns one (batch row, weight row) element and
 // keeps its results for up to 8 blocks before storing them. The next block's codes are in
 // flight while a block is computed.
+// Up to kMaxSegs linears that share x, in one launch: their 16-row blocks are numbered one
+// after another (segment s holds blocks [blk_begin, blk_begin + ceil(n_rows / 16))), and every
+// block is computed exactly as in a launch of its linear alone. Grouped launches need
+// sign-symmetric codebooks (register dequantization: each block's tables are its segment's
+// kernel arguments); the pair table (PAIRS) serves one segment only.
+struct SkSeg {
+  const uint8_t* codes;
+  float* y;
+  int n_rows;
+  int blk_begin;
+  LutBytes tb;
+  float scale;
+};
+struct SkSegs {
+  SkSeg s[kMaxSegs];
+};
+
 template <int ND, bool PAIRS>
-__global__ __launch_bounds__(512) void k_mfma_sk(const uint8_t* __restrict__ codes,
-                                                 const uint16_t* __restrict__ x,
-                                                 float* __restrict__ y, int n_rows, int k_cols,
-                                                 int m_rows, LutBytes tb, Lut16 lut,
-                                                 float scale) {
+__global__ __launch_bounds__(512) void k_mfma_sk(const uint16_t* __restrict__ x,
+                                                 const uint8_t* codes0, int n_rows0, int nseg,
+                                                 int nblocks, int k_cols, int m_rows,
+                                                 SkSegs segs, Lut16 lut) {
   static_assert(ND == 4 || ND == 8 || ND == 16 || ND == 32, "64 / ND rows per load");
   constexpr int BR = 16 * ND;            // code bytes per row per wavefront and block
   constexpr int RPI = 64 / ND;           // rows per load instruction
@@ -1260,8 +1276,16 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint8_t* __restrict__ cod
   const int j = lane & 15, g = lane >> 4;
   const uint32_t laneoff = (uint32_t)lane << 2;
   const int64_t row_bytes = (int64_t)k_cols / 2;
-  const int nblocks = (n_rows + 15) / 16;
   const int slice_k0 = w * 32 * ND;
+  // Segment of block b (a uniform value); one-segment launches take the first segment's codes
+  // pointer and row count from their leading (preloaded) arguments.
+  auto seg_of = [&](int b) {
+    int si = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxSegs; ++i)
+      if (i < nseg && b >= segs.s[i].blk_begin) si = i;
+    return si;
+  };
 
   // Activations first (they return first): batch row j of this lane's slice, in the order the
   // dequantization produces the weights.
@@ -1281,7 +1305,15 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint8_t* __restrict__ cod
   // partial last block), so rows past n_rows read as zeros.
   auto load_block = [&](int b, u32x4 (&q)[NI]) {
     const int bb = b < nblocks ? b : nblocks - 1;
-    const int64_t base = (int64_t)bb * 16 * row_bytes;
+    const uint8_t* codes = codes0;
+    int n_rows = n_rows0, lb = bb;
+    if (nseg > 1) {
+      const int si = seg_of(bb);
+      codes = segs.s[si].codes;
+      n_rows = segs.s[si].n_rows;
+      lb = bb - segs.s[si].blk_begin;
+    }
+    const int64_t base = (int64_t)lb * 16 * row_bytes;
     const int64_t avail = (int64_t)n_rows * row_bytes - base;
     const int size = b < nblocks ? (int)(avail < 16 * row_bytes ? avail : 16 * row_bytes) : 0;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
@@ -1307,8 +1339,10 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint8_t* __restrict__ cod
       for (int h = 0; h < NRES; ++h) {
         if (h < held) {
           const int b = blast - (held - 1 - h) * (int)gridDim.x;
-          const int row = b * 16 + rj;
-          if (row < n_rows) y[(int64_t)ri * n_rows + row] = res[h];
+          const int si = seg_of(b);
+          const int n_rows = segs.s[si].n_rows;
+          const int row = (b - segs.s[si].blk_begin) * 16 + rj;
+          if (row < n_rows) segs.s[si].y[(int64_t)ri * n_rows + row] = res[h];
         }
       }
     }
@@ -1316,6 +1350,9 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint8_t* __restrict__ cod
   };
   uint8_t* s_cw = s_ct[w];
   auto block = [&](int b, const u32x4 (&qc)[NI]) {
+    const int bsi = seg_of(b);
+    const LutBytes tb = segs.s[bsi].tb;
+    const float scale = segs.s[bsi].scale;
     // LDS operations of one wavefront complete in order: the reads see the writes.
 #pragma unroll
     for (int c = 0; c < NI; ++c)
@@ -1613,32 +1650,58 @@ bool sk_shape(int M, int K) {
   return M >= 2 && M <= 16 && (K == 1024 || K == 2048 || K == 4096 || K == 8192);
 }
 
-int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st, int cus) {
-  const int N = (int)j.n;
-  LutBytes tb = {0, 0, 0, 0};
+// Split-K launches for the linears jobs[idx[0..count)] of one call: one grouped launch when
+// every codebook is sign-symmetric (register dequantization), otherwise one launch per linear.
+int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const int* idx,
+                  int count, hipStream_t st, int cus) {
+  SkSegs segs;
+  std::memset(&segs, 0, sizeof(segs));
   Lut16 lut;
-  float scale;
-  // Register dequantization needs a sign-symmetric codebook (every fitted one is); any other
-  // codebook goes through the LDS pair table.
-  const bool symmetric = make_lut_bytes(j.codebook, &tb, &scale);
-  make_lut16(j.codebook, &lut, &scale);
-  const int nblocks = (N + 15) / 16;
-  const int grid = nblocks < cus ? nblocks : cus;
-#define LOGBQ_SK(ND)                                                                             \
-  if (symmetric)                                                                                 \
-    hipLaunchKernelGGL((k_mfma_sk<ND, false>), dim3((unsigned)grid), dim3(512), 0, st, j.codes, x, \
-                       j.y, N, K, M, tb, lut, scale);                                            \
-  else                                                                                           \
-    hipLaunchKernelGGL((k_mfma_sk<ND, true>), dim3((unsigned)grid), dim3(512), 0, st, j.codes, x,  \
-                       j.y, N, K, M, tb, lut, scale);
-  switch (K) {
-    case 1024: LOGBQ_SK(4) break;
-    case 2048: LOGBQ_SK(8) break;
-    case 4096: LOGBQ_SK(16) break;
-    default: LOGBQ_SK(32) break;
+  bool all_symmetric = true;
+  int total = 0;
+  for (int a = 0; a < count; ++a) {
+    const LinearJob& j = jobs[idx[a]];
+    SkSeg& sg = segs.s[a];
+    sg.codes = j.codes;
+    sg.y = j.y;
+    sg.n_rows = (int)j.n;
+    sg.blk_begin = total;
+    all_symmetric = make_lut_bytes(j.codebook, &sg.tb, &sg.scale) && all_symmetric;
+    total += (int)((j.n + 15) / 16);
   }
+  auto launch = [&](int nseg, const SkSegs& sgs, int nblocks, bool pairs, const Lut16& l) {
+    const int grid = nblocks < cus ? nblocks : cus;
+#define LOGBQ_SK(ND)                                                                             \
+  if (pairs)                                                                                     \
+    hipLaunchKernelGGL((k_mfma_sk<ND, true>), dim3((unsigned)grid), dim3(512), 0, st, x,          \
+                       sgs.s[0].codes, sgs.s[0].n_rows, nseg, nblocks, K, M, sgs, l);            \
+  else                                                                                           \
+    hipLaunchKernelGGL((k_mfma_sk<ND, false>), dim3((unsigned)grid), dim3(512), 0, st, x,         \
+                       sgs.s[0].codes, sgs.s[0].n_rows, nseg, nblocks, K, M, sgs, l);
+    switch (K) {
+      case 1024: LOGBQ_SK(4) break;
+      case 2048: LOGBQ_SK(8) break;
+      case 4096: LOGBQ_SK(16) break;
+      default: LOGBQ_SK(32) break;
+    }
 #undef LOGBQ_SK
-  return launch_status();
+    return launch_status();
+  };
+  if (all_symmetric) return launch(count, segs, total, false, lut);
+  for (int a = 0; a < count; ++a) {
+    const LinearJob& j = jobs[idx[a]];
+    SkSegs one;
+    std::memset(&one, 0, sizeof(one));
+    one.s[0] = segs.s[a];
+    one.s[0].blk_begin = 0;
+    // Register dequantization for a sign-symmetric codebook (every fitted one), the LDS pair
+    // table for any other.
+    const bool symmetric = make_lut_bytes(j.codebook, &one.s[0].tb, &one.s[0].scale);
+    make_lut16(j.codebook, &lut, &one.s[0].scale);
+    const int32_t r = launch(1, one, (int)((j.n + 15) / 16), !symmetric, lut);
+    if (r != LOGBQ_OK) return r;
+  }
+  return LOGBQ_OK;
 }
 
 // Path choice per linear (measured on MI355X). The GEMV's time grows with m * N * K (its
@@ -1696,12 +1759,13 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
   int gl[kMaxSegs];
   int ng = 0;
   int64_t grows = 0;
+  int sl[kMaxSegs];
+  int ns = 0;
   for (int a = 0; a < nlive; ++a) {
     const LinearJob& j = jobs[live[a]];
     const int path = choose_path<BITS>(M, K, j.n);
     if (path == LOGBQ_PATH_SPLITK) {
-      const int32_t r = launch_sk(x, M, K, j, st, cus);
-      if (r != LOGBQ_OK) return r;
+      sl[ns++] = live[a];
     } else if (path == LOGBQ_PATH_GEMV) {
       gl[ng++] = live[a];
       grows += j.n;
@@ -1712,6 +1776,10 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
       const int32_t r = launch_mfma<BITS>(x, M, K, j, st);
       if (r != LOGBQ_OK) return r;
     }
+  }
+  if (ns > 0) {
+    const int32_t r = launch_sk(x, M, K, jobs, sl, ns, st, cus);
+    if (r != LOGBQ_OK) return r;
   }
   if (ng == 0) return LOGBQ_OK;
   if (!gemv_config<BITS>(M, K, &wk, &cpl)) return LOGBQ_ERR_UNSUPPORTED;

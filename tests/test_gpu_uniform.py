@@ -115,3 +115,20 @@ def test_quality_on_gpu_matches_oracle():
     assert U.sqnr_db(w, wl.cpu().numpy()) == U.sqnr_db(w, wl_ref)
     assert U.sqnr_db(w, wu.cpu().numpy()) == U.sqnr_db(w, wu_ref)
     assert U.sqnr_db(w, wl_ref) > U.sqnr_db(w, wu_ref) + 6.0
+
+
+def test_grouped_launch_with_uniform_codebooks():
+    """Grouped calls whose codebooks are not sign-symmetric (the split-K kernel then launches
+    per linear with its LDS table) equal single calls bit for bit."""
+    k = 2048
+    ws = [_tensor(n, k, [33, n, 0, 0]) for n in (4096, 300)]
+    us = [L.fit_uniform(w) for w in ws]
+    codes = [L.encode_uniform(torch.from_numpy(w).to(DEV), u) for w, u in zip(ws, us)]
+    for m in (1, 4, 8, 16):
+        _say(f"grouped uniform m={m}")
+        x = torch.from_numpy(np.asarray(inputs.activations(m, k, seed=[33, m, 0, 1]))).to(DEV)
+        ys = L.linear_multi(x, codes, [u.codebook_array() for u in us])
+        for c, u, y in zip(codes, us, ys):
+            y1 = L.linear(x, c, u.codebook_array())
+            torch.cuda.synchronize()
+            assert torch.equal(y, y1)
