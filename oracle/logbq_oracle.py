@@ -10,6 +10,8 @@ Python ``fractions`` for the few decisions that must be exact:
 
 * ``fit``          -- w_max (Sec. 3.2), w_min by energy-based pruning (Eq. 5), the base b
                       (Eq. 3) and the shift s (Eq. 4).
+* ``fit_exact``    -- the same with the energy sums of Eq. 5 taken exactly (integers in
+                      units of 2^-298, the square of the smallest float32 subnormal).
 * ``codebook``     -- the 2^n-entry table of Dequant values (Eq. 2) for every n-bit code.
 * ``encode``       -- Quant (Eq. 1): round log_b|x| + s to the nearest integer, clamp the
                       magnitude index to [0, q_max], attach the sign.
@@ -29,7 +31,11 @@ Readings of places where the paper is silent or garbled (each also listed in DES
 * Eq. 4 writes floor(log_b w_max); the floor is taken exactly, as the largest integer J with
   b^J <= w_max, so that the top codebook entry never exceeds w_max.
 * Eq. 5: the energy sums are sequential float64 prefix sums over |w| in ascending order,
-  the total is the last prefix sum, and the ratio is a float64 division.
+  the total is the last prefix sum, and the ratio is a float64 division (``fit``). Read
+  with exact sums instead (``fit_exact``): the first sorted position whose exact prefix
+  energy is at least eps times the exact total, compared as rationals with eps taken as its
+  exact double value. The two readings pick the same w_min unless the exact ratio lies within
+  float64 rounding of eps.
 * The sign+magnitude code has two zeros; code 2^(n-1) ("-0") is never produced and decodes
   to +0.0.
 * The codebook is float32: entry k is pow(b, k - s) in double, rounded to float32.
@@ -43,7 +49,7 @@ from fractions import Fraction
 import numpy as np
 
 __all__ = [
-    "OracleError", "FitResult", "qmax", "fit", "codebook", "encode", "magnitude_thresholds",
+    "OracleError", "FitResult", "qmax", "fit", "fit_exact", "codebook", "encode", "magnitude_thresholds",
     "pack", "unpack", "pack_codes", "unpack_codes", "dequantize", "linear", "energy_ratio_exact",
     "log_nearest_code",
 ]
@@ -80,17 +86,7 @@ def fit(w, bits: int = 4, eps: float = 4e-3) -> FitResult:
     w: any array of float32 weights (flattened). eps: the pruned energy fraction
     (Sec. 3.2 gives 4e-3 for 4-bit codebooks).
     """
-    w = np.asarray(w)
-    if w.dtype != np.float32:
-        raise OracleError("invalid_arg", "weights must be float32")
-    if bits < 2 or bits > 8:
-        raise OracleError("invalid_arg", "bits out of range")
-    if not (0.0 < eps < 1.0):
-        raise OracleError("invalid_arg", "eps must lie in (0, 1)")
-    if w.size < 2:
-        raise OracleError("invalid_arg", "need at least two weights")
-    if not np.all(np.isfinite(w)):
-        raise OracleError("nonfinite", "weights contain NaN or Inf")
+    w = _validate(w, bits, eps)
 
     # |w| ascending, in float64 (squares of float32 values are exact in float64).
     a = np.sort(np.abs(w.astype(np.float64)).ravel(), kind="stable")
@@ -108,7 +104,53 @@ def fit(w, bits: int = 4, eps: float = 4e-3) -> FitResult:
     hit = np.nonzero(ratio >= eps)[0]
     i_star = int(hit[0])
     w_min = float(a[i_star])
+    return _base_and_shift(bits, eps, w_min, w_max, i_star)
 
+
+def _validate(w, bits: int, eps: float) -> np.ndarray:
+    w = np.asarray(w)
+    if w.dtype != np.float32:
+        raise OracleError("invalid_arg", "weights must be float32")
+    if bits < 2 or bits > 8:
+        raise OracleError("invalid_arg", "bits out of range")
+    if not (0.0 < eps < 1.0):
+        raise OracleError("invalid_arg", "eps must lie in (0, 1)")
+    if w.size < 2:
+        raise OracleError("invalid_arg", "need at least two weights")
+    if not np.all(np.isfinite(w)):
+        raise OracleError("nonfinite", "weights contain NaN or Inf")
+    return w
+
+
+def fit_exact(w, bits: int = 4, eps: float = 4e-3) -> FitResult:
+    """Per-tensor codebook parameters with the sums of Eq. 5 taken exactly.
+
+    Every float32 |w_i| is an integer multiple n_i of 2^-149, so w_i^2 = n_i^2 2^-298 and
+    both sums of Eq. 5 are integers in units of 2^-298. w_min is |w| at the first position i
+    of |w| sorted ascending where sum_{j <= i} n_j^2 >= eps * sum_j n_j^2, decided on
+    integers with eps as its exact double value. b and s follow as in ``fit``.
+    """
+    w = _validate(w, bits, eps)
+    a = np.sort(np.abs(w.astype(np.float64)).ravel(), kind="stable")
+    w_max = float(a[-1])
+    if w_max == 0.0:
+        raise OracleError("degenerate", "all weights are zero")
+    n = [int(v) for v in np.ldexp(a, 149).tolist()]   # exact: scaling by a power of two
+    energy = [v * v for v in n]
+    total = sum(energy)
+    num, den = float(eps).as_integer_ratio()
+    prefix = 0
+    i_star = len(energy) - 1
+    for i, e in enumerate(energy):
+        prefix += e
+        if prefix * den >= num * total:               # prefix / total >= eps
+            i_star = i
+            break
+    return _base_and_shift(bits, eps, float(a[i_star]), w_max, i_star)
+
+
+def _base_and_shift(bits: int, eps: float, w_min: float, w_max: float, i_star: int) -> FitResult:
+    """Eq. 3 and Eq. 4 from w_min and w_max."""
     q = qmax(bits)
     if not (w_min < w_max):
         raise OracleError("degenerate", "w_min == w_max: base would be 1")
