@@ -106,6 +106,35 @@ const char* logbq_status_str(int32_t status);
 int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
                   logbq_params* out);
 
+/* Bytes of device workspace logbq_fit_device needs. */
+#define LOGBQ_FIT_WORKSPACE_BYTES 49160
+
+/*
+ * logbq_fit_device -- the per-tensor fit on device-resident weights (Sec. 3.1 Eq. 3-4,
+ * Sec. 3.2 Eq. 5), with the energy sums of Eq. 5 taken exactly.
+ *   w_dev        : device, numel float32 weights, 16-byte aligned, read only.
+ *   numel        : 2 <= numel < 2^40.
+ *   bits, eps    : as logbq_fit.
+ *   workspace_dev: device, LOGBQ_FIT_WORKSPACE_BYTES bytes, 8-byte aligned, owned by the
+ *                  caller; overwritten.
+ *   out          : host, filled on success; untouched on error.
+ *   stream       : hipStream_t the passes run on.
+ * w_max = max|w|. w_min = |w| at the smallest position i of |w| sorted ascending (ties in any
+ * order) with sum_{j <= i} w_j^2 >= eps * sum_j w_j^2, both sums exact (squares of float32
+ * values are exact rationals); wmin_index = i. b, s, codebook and thresholds then follow
+ * exactly as in logbq_fit. logbq_fit sums in float64, in sequence; the two agree unless the
+ * exact ratio lies within float64 rounding of eps.
+ * Three radix-selection passes over the weights (bits 30..20, 19..11, 10..0 of the float32
+ * pattern of |w|) accumulate per-bin counts and exact integer energy sums on the device; the
+ * host picks each pass's bin with exact integer arithmetic. Blocks the calling thread until
+ * the stream has run the passes (not capturable in a HIP graph).
+ * Errors: INVALID_ARG (null, numel < 2, eps outside (0,1)), UNSUPPORTED (bits not 4 or 8,
+ * numel too large, misaligned), NONFINITE (NaN/Inf weight), DEGENERATE (w_max == 0 or
+ * w_min == w_max), HIP (a HIP call failed).
+ */
+int32_t logbq_fit_device(const float* w_dev, int64_t numel, int32_t bits, double eps,
+                         void* workspace_dev, logbq_params* out, void* stream);
+
 /*
  * logbq_encode -- Quant (Eq. 1) of a weight matrix into 4-bit or 8-bit codes (Sec. 3.3 packing).
  *   w_dev        : device, [n][k] float32 weights.

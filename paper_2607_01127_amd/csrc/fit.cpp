@@ -13,6 +13,7 @@
 #include <limits>
 #include <vector>
 
+#include "fit_detail.h"
 #include "logbq.h"
 
 namespace {
@@ -74,6 +75,16 @@ struct Big {
     }
     d.swap(r);
     trim();
+  }
+  void add(const Big& o) {
+    if (o.d.size() > d.size()) d.resize(o.d.size(), 0);
+    uint64_t carry = 0;
+    for (size_t i = 0; i < d.size(); ++i) {
+      const uint64_t t = uint64_t(d[i]) + (i < o.d.size() ? o.d[i] : 0u) + carry;
+      d[i] = uint32_t(t);
+      carry = t >> 32;
+    }
+    if (carry) d.push_back(uint32_t(carry));
   }
   void trim() { while (!d.empty() && d.back() == 0) d.pop_back(); }
   static int cmp(const Big& a, const Big& b) {
@@ -164,6 +175,9 @@ float uniform_threshold(double s, int32_t z, int j) {
   return t;
 }
 
+int32_t finish_params(int32_t bits, double eps, double wmin, double wmax, int64_t istar,
+                      logbq_params* out);
+
 }  // namespace
 
 extern "C" {
@@ -215,7 +229,6 @@ int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
   if (!w_host || !out || numel < 2) return LOGBQ_ERR_INVALID_ARG;
   if (!(eps > 0.0 && eps < 1.0)) return LOGBQ_ERR_INVALID_ARG;
   if (bits != 4 && bits != 8) return LOGBQ_ERR_UNSUPPORTED;
-  const int32_t qmax = (1 << (bits - 1)) - 1;
 
   // |w| as float32 bit patterns (sign cleared); reject NaN / Inf.
   std::vector<uint32_t> a((size_t)numel);
@@ -243,6 +256,17 @@ int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
     if (prefix / total >= eps) { istar = i; break; }
   }
   const double wmin = (double)u2f(a[istar]);
+  return finish_params(bits, eps, wmin, wmax, (int64_t)istar, out);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Eq. 3 and Eq. 4 from w_min and w_max, then the codebook (Eq. 2) and the exact thresholds.
+int32_t finish_params(int32_t bits, double eps, double wmin, double wmax, int64_t istar,
+                      logbq_params* out) {
+  const int32_t qmax = (1 << (bits - 1)) - 1;
   if (!(wmin < wmax)) return LOGBQ_ERR_DEGENERATE;
 
   // Eq. 3 and Eq. 4 (floor taken exactly: largest J with b^J <= w_max).
@@ -263,7 +287,7 @@ int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
   p.wmax = wmax;
   p.base = b;
   p.shift = (int32_t)s;
-  p.wmin_index = (int64_t)istar;
+  p.wmin_index = istar;
   const int half = 1 << (bits - 1);
   for (int k = 1; k <= qmax; ++k) {
     const float v = (float)std::pow(b, (double)(k - p.shift));
@@ -280,4 +304,102 @@ int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
   return LOGBQ_OK;
 }
 
-}  // extern "C"
+}  // namespace
+
+// ---- exact selection of the device fit ---------------------------------------------------
+
+namespace {
+
+// Energy of a bin in units of 2^-298 (the square of the smallest float32 subnormal):
+// (hi * 2^24 + lo) * 2^(2 ef + 298), where |w| = m * 2^ef for every weight of the bin.
+Big bin_energy(uint64_t hi, uint64_t lo, uint32_t exp_field) {
+  const int64_t ef = exp_field == 0 ? -149 : int64_t(exp_field) - 150;
+  Big e(hi);
+  e.shl(24);
+  e.add(Big(lo));
+  e.shl(2 * ef + 298);
+  return e;
+}
+
+}  // namespace
+
+namespace logbq_detail {
+
+int32_t fit_from_passes(int32_t bits, double eps, FitPassFn run, void* ctx, logbq_params* out) {
+  FitPassResult r{};
+  int32_t st = run(ctx, 1, 0, &r);
+  if (st != LOGBQ_OK) return st;
+  if (r.nonfinite) return LOGBQ_ERR_NONFINITE;
+  if (r.max_key == 0) return LOGBQ_ERR_DEGENERATE;
+  const double wmax = (double)u2f(r.max_key);
+
+  // eps = N 2^e exactly (e < 0): an energy P reaches eps T iff P 2^-e >= N T.
+  uint64_t N;
+  int64_t e;
+  split_f64(eps, N, e);
+  Big total;
+  for (int b = 0; b < kFitBins1; ++b)
+    if (r.bins[3 * b]) total.add(bin_energy(r.bins[3 * b + 1], r.bins[3 * b + 2], uint32_t(b) >> 3));
+  Big target = total;
+  target.mul_small(N);
+  auto reaches = [&](const Big& p) {
+    Big l = p;
+    l.shl(-e);
+    return Big::cmp(l, target) >= 0;
+  };
+
+  // Energy and count of all weights below the current selection.
+  Big below;
+  uint64_t count_below = 0;
+  // First bin at which the running energy reaches the target; below / count_below then cover
+  // the bins before it.
+  auto pick = [&](const FitPassResult& pr, int nbins, uint32_t exp_field, bool per_bin_exp) {
+    for (int b = 0; b < nbins; ++b) {
+      const uint64_t* w = pr.bins + 3 * b;
+      if (w[0] == 0) continue;
+      Big eb = bin_energy(w[1], w[2], per_bin_exp ? uint32_t(b) >> 3 : exp_field);
+      Big run_e = below;
+      run_e.add(eb);
+      if (reaches(run_e)) return b;
+      below = run_e;
+      count_below += w[0];
+    }
+    return -1;
+  };
+
+  const int b1 = pick(r, kFitBins1, 0, true);
+  if (b1 < 0) return LOGBQ_ERR_HIP;
+  const uint32_t exp_field = uint32_t(b1) >> 3;
+  st = run(ctx, 2, uint32_t(b1), &r);
+  if (st != LOGBQ_OK) return st;
+  const int b2 = pick(r, kFitBins2, exp_field, false);
+  if (b2 < 0) return LOGBQ_ERR_HIP;
+  const uint32_t sel = (uint32_t(b1) << 9) | uint32_t(b2);
+  st = run(ctx, 3, sel, &r);
+  if (st != LOGBQ_OK) return st;
+  const int b3 = pick(r, kFitBins3, exp_field, false);
+  if (b3 < 0) return LOGBQ_ERR_HIP;
+
+  // w_min is the value of the chosen single-value bin; its position is the first of its
+  // copies at which the running energy reaches the target.
+  const uint32_t key = (sel << 11) | uint32_t(b3);
+  const uint64_t copies = r.bins[3 * b3];
+  uint64_t F;
+  int64_t ef;
+  split_f32(u2f(key), F, ef);
+  Big v2(F);
+  v2.mul_small(F);
+  v2.shl(2 * ef + 298);
+  uint64_t lo = 1, hi = copies;   // reaches(below + copies v^2) holds
+  while (lo < hi) {
+    const uint64_t mid = lo + (hi - lo) / 2;
+    Big p = v2;
+    p.mul_small(mid);
+    p.add(below);
+    if (reaches(p)) hi = mid; else lo = mid + 1;
+  }
+  const int64_t istar = (int64_t)(count_below + lo - 1);
+  return finish_params(bits, eps, (double)u2f(key), wmax, istar, out);
+}
+
+}  // namespace logbq_detail

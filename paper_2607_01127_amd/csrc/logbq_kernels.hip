@@ -22,6 +22,8 @@
 //   k_encode_uniform  codes of the asymmetric linear baseline (Sec. 2), for comparisons.
 //   k_gptq_panel, k_gptq_trail  GPTQ calibration with a fixed codebook (one wavefront per row
 //              within a block of 128 columns; the block's errors applied to the later columns).
+//   k_fit_hist  the device fit's radix-selection passes (Eq. 5 with exact sums): per-bin counts
+//              and exact integer energy sums of |w| binned by its float32 bit pattern.
 //
 // The float16 tables hold codebook / 2^e with 2^e chosen so that the largest entry lies in
 // [2^14, 2^15); the result is multiplied back by 2^e (exact). Lookup replaces evaluating
@@ -33,7 +35,9 @@
 #include <cstdint>
 #include <cstring>
 #include <mutex>
+#include <vector>
 
+#include "fit_detail.h"
 #include "logbq.h"
 
 namespace {
@@ -1408,6 +1412,99 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint16_t* __restrict__ x,
   flush();
 }
 
+// ------------------------------------------------------------------ device fit, exact Eq. 5
+//
+// One pass of the radix selection described in fit_detail.h. Workgroup g takes the weights
+// [g C, (g + 1) C), C = kFitChunk, and accumulates per bin, in LDS, the count and the integer
+// sums of (m^2 >> 24) and (m^2 & 0xFFFFFF) of the weights the pass selects (m = integer
+// significand of |w|, m^2 < 2^48). The LDS word a holds count << 44 | sum of (m^2 >> 24): at
+// most C = 2^18 weights per workgroup keep the sum below 2^42 and the count below 2^20, so one
+// 64-bit add updates both. (Measured on the 8192 x 28672 weights: chunks of 2^19 in the
+// selective passes halve their flushed bins but leave half the workgroups to stream, which
+// costs more.) Non-empty bins are then added to the global bins with 64-bit integer
+// atomics, which are exact and independent of order. Pass 1 also takes the largest bit pattern
+// and flags NaN / Inf.
+constexpr int64_t kFitChunk = int64_t(1) << 18;
+constexpr int kFitThreads = 512;
+
+template <int PASS>
+__global__ __launch_bounds__(kFitThreads) void k_fit_hist(const float* __restrict__ w, int64_t n,
+                                                         uint32_t sel,
+                                                         unsigned long long* __restrict__ bins,
+                                                         unsigned int* __restrict__ flags) {
+  constexpr int NB = PASS == 1 ? logbq_detail::kFitBins1
+                     : PASS == 2 ? logbq_detail::kFitBins2 : logbq_detail::kFitBins3;
+  __shared__ unsigned long long s_a[NB];
+  __shared__ unsigned long long s_c[NB];
+  __shared__ unsigned int s_max, s_bad;
+  const int t = threadIdx.x;
+  for (int i = t; i < NB; i += kFitThreads) {
+    s_a[i] = 0;
+    s_c[i] = 0;
+  }
+  if (t == 0) {
+    s_max = 0;
+    s_bad = 0;
+  }
+  __syncthreads();
+  uint32_t kmax = 0, bad = 0;
+  auto add = [&](uint32_t u) {
+    const uint32_t key = u & 0x7FFFFFFFu;
+    bool take;
+    uint32_t bin;
+    if (PASS == 1) {
+      kmax = key > kmax ? key : kmax;
+      bad |= key >= 0x7F800000u ? 1u : 0u;
+      take = true;
+      bin = key >> 20;
+    } else if (PASS == 2) {
+      take = (key >> 20) == sel;
+      bin = (key >> 11) & 0x1FFu;
+    } else {
+      take = (key >> 11) == sel;
+      bin = key & 0x7FFu;
+    }
+    if (take) {
+      const uint64_t m = (key & 0x7FFFFFu) | (key >= 0x800000u ? 0x800000u : 0u);
+      const uint64_t q = m * m;
+      atomicAdd(&s_a[bin], (1ull << 44) | (q >> 24));
+      atomicAdd(&s_c[bin], (unsigned long long)(q & 0xFFFFFFu));
+    }
+  };
+  const int64_t begin = (int64_t)blockIdx.x * kFitChunk;
+  const int64_t end = n - begin < kFitChunk ? n : begin + kFitChunk;
+  const int64_t vend = begin + ((end - begin) & ~int64_t(3));
+  for (int64_t i = begin + 4 * t; i < vend; i += 4 * kFitThreads) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(w + i));
+    add(v.x);
+    add(v.y);
+    add(v.z);
+    add(v.w);
+  }
+  if (vend + t < end) add(__float_as_uint(w[vend + t]));
+  if (PASS == 1) {
+    atomicMax(&s_max, kmax);
+    if (bad) atomicOr(&s_bad, 1u);
+  }
+  __syncthreads();
+  for (int i = t; i < NB; i += kFitThreads) {
+    const unsigned long long a = s_a[i];
+    if (a == 0) continue;
+    atomicAdd(&bins[3 * i], a >> 44);
+    atomicAdd(&bins[3 * i + 1], a & ((1ull << 44) - 1));
+    atomicAdd(&bins[3 * i + 2], s_c[i]);
+  }
+  if (PASS == 1 && t == 0) {
+    atomicMax(&flags[0], s_max);
+    if (s_bad) atomicOr(&flags[1], 1u);
+  }
+}
+
+__global__ void k_fill_u64(unsigned long long* __restrict__ p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
 // ------------------------------------------------------------------ host helpers
 
 // IEEE binary32 -> binary16, round to nearest even.
@@ -1811,6 +1908,49 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
 
 }  // namespace
 
+// One pass of the device fit: clear the workspace, run the pass, copy its bins to the host and
+// wait for them (the next pass's selection depends on them).
+struct FitDeviceCtx {
+  const float* w;
+  int64_t n;
+  unsigned long long* ws;
+  hipStream_t st;
+  std::vector<uint64_t> host;
+};
+
+constexpr int kFitWords = 3 * logbq_detail::kFitBins1 + 1;   // bins, then the pass-1 flags
+static_assert(logbq_detail::kFitBins1 >= logbq_detail::kFitBins2 &&
+              logbq_detail::kFitBins1 >= logbq_detail::kFitBins3, "largest pass");
+static_assert(kFitWords * 8 == LOGBQ_FIT_WORKSPACE_BYTES, "workspace size in the header");
+
+int32_t fit_device_pass(void* vctx, int pass, uint32_t sel, logbq_detail::FitPassResult* res) {
+  FitDeviceCtx& c = *static_cast<FitDeviceCtx*>(vctx);
+  hipLaunchKernelGGL(k_fill_u64, dim3((kFitWords + 255) / 256), dim3(256), 0, c.st, c.ws,
+                     kFitWords);
+  if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
+  const unsigned grid = (unsigned)((c.n + kFitChunk - 1) / kFitChunk);
+  unsigned int* flags = reinterpret_cast<unsigned int*>(c.ws + 3 * logbq_detail::kFitBins1);
+  if (pass == 1)
+    hipLaunchKernelGGL(k_fit_hist<1>, dim3(grid), dim3(kFitThreads), 0, c.st, c.w, c.n, sel, c.ws,
+                       flags);
+  else if (pass == 2)
+    hipLaunchKernelGGL(k_fit_hist<2>, dim3(grid), dim3(kFitThreads), 0, c.st, c.w, c.n, sel, c.ws,
+                       flags);
+  else
+    hipLaunchKernelGGL(k_fit_hist<3>, dim3(grid), dim3(kFitThreads), 0, c.st, c.w, c.n, sel, c.ws,
+                       flags);
+  if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
+  c.host.assign(kFitWords, 0);
+  if (hipMemcpyAsync(c.host.data(), c.ws, (size_t)kFitWords * 8, hipMemcpyDeviceToHost, c.st) !=
+      hipSuccess)
+    return LOGBQ_ERR_HIP;
+  if (hipStreamSynchronize(c.st) != hipSuccess) return LOGBQ_ERR_HIP;
+  res->bins = c.host.data();
+  res->max_key = (uint32_t)c.host[kFitWords - 1];
+  res->nonfinite = (uint32_t)(c.host[kFitWords - 1] >> 32);
+  return LOGBQ_OK;
+}
+
 extern "C" {
 
 int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_params* p,
@@ -1879,6 +2019,18 @@ int32_t logbq_encode_uniform(const float* w_dev, int64_t n, int64_t k, const log
                      reinterpret_cast<const f32x4*>(w_dev), reinterpret_cast<uint16_t*>(codes_dev),
                      nchunk, th);
   return launch_status();
+}
+
+int32_t logbq_fit_device(const float* w_dev, int64_t numel, int32_t bits, double eps,
+                         void* workspace_dev, logbq_params* out, void* stream) {
+  if (!w_dev || !workspace_dev || !out || numel < 2) return LOGBQ_ERR_INVALID_ARG;
+  if (!(eps > 0.0 && eps < 1.0)) return LOGBQ_ERR_INVALID_ARG;
+  if (bits != 4 && bits != 8) return LOGBQ_ERR_UNSUPPORTED;
+  if (numel >= (int64_t(1) << 40)) return LOGBQ_ERR_UNSUPPORTED;
+  if (!aligned16(w_dev) || ((uintptr_t)workspace_dev & 7u) != 0) return LOGBQ_ERR_UNSUPPORTED;
+  FitDeviceCtx c{w_dev, numel, static_cast<unsigned long long*>(workspace_dev),
+                 (hipStream_t)stream, {}};
+  return logbq_detail::fit_from_passes(bits, eps, fit_device_pass, &c, out);
 }
 
 int32_t logbq_gptq(float* w_dev, int64_t n, int64_t k, const float* u_dev, const logbq_params* p,

@@ -83,7 +83,11 @@ SIGNATURES = {
                                        c_void_p]),
     "logbq_gptq": (c_int32, [c_void_p, c_int64, c_int64, c_void_p, POINTER(Params),
                              POINTER(Uniform), c_void_p, c_void_p, c_void_p]),
+    "logbq_fit_device": (c_int32, [c_void_p, c_int64, c_int32, c_double, c_void_p,
+                                   POINTER(Params), c_void_p]),
 }
+
+FIT_WORKSPACE_BYTES = 49160
 
 ABI_VERSION = 2
 
@@ -144,6 +148,23 @@ def fit(w, bits: int = 4, eps: float = 4e-3) -> Params:
     p = Params()
     _check(lib().logbq_fit(w.ctypes.data_as(POINTER(c_float)), w.size, bits, eps,
                            ctypes.byref(p)), "logbq_fit")
+    return p
+
+
+def fit_device(w, bits: int = 4, eps: float = 4e-3, workspace=None, stream=None) -> Params:
+    """logbq_fit_device on a contiguous float32 device tensor (Eq. 5 with exact sums). Blocks
+    until the fit's passes have run on `stream`."""
+    import torch
+    if w.dtype != torch.float32 or not w.is_contiguous() or w.device.type != "cuda":
+        raise ValueError("w must be a contiguous float32 device tensor")
+    if workspace is None:
+        workspace = torch.empty(FIT_WORKSPACE_BYTES, dtype=torch.uint8, device=w.device)
+    elif workspace.numel() * workspace.element_size() < FIT_WORKSPACE_BYTES:
+        raise ValueError(f"workspace must hold {FIT_WORKSPACE_BYTES} bytes")
+    p = Params()
+    _check(lib().logbq_fit_device(c_void_p(w.data_ptr()), w.numel(), bits, eps,
+                                  c_void_p(workspace.data_ptr()), ctypes.byref(p),
+                                  _stream(stream)), "logbq_fit_device")
     return p
 
 

@@ -1,7 +1,9 @@
 """Pins of the exact-sum reading of Eq. 5 (Sec. 3.2) in the oracle (``fit_exact``), which the
-device fit must reproduce bit for bit. The pins come from outside the function: hand-derived results, the
+device fit must reproduce bit for bit, and host-side checks of logbq_fit_device's argument
+validation (no GPU). The pins come from outside the function: hand-derived results, the
 sequential float64 fit where the two readings cannot differ, a rational-arithmetic
 certificate of w_min computed another way, and invariances of the definition."""
+import ctypes
 from fractions import Fraction
 
 import numpy as np
@@ -9,6 +11,7 @@ import pytest
 
 from oracle import logbq_oracle as O
 from paper_2607_01127_amd import inputs
+from paper_2607_01127_amd import logbq as L
 
 
 def test_hand_tie_case():
@@ -115,3 +118,20 @@ def test_errors_match_sequential_fit():
         with pytest.raises(O.OracleError, match=kind):
             O.fit_exact(w)
 
+
+def test_fit_device_validation_before_hip():
+    h = L.lib()
+    p = ctypes.byref(L.Params())
+    a, ws = ctypes.c_void_p(4096), ctypes.c_void_p(8192)   # never dereferenced on these paths
+    assert h.logbq_fit_device(None, 16, 4, 4e-3, ws, p, None) == L.ERR_INVALID_ARG
+    assert h.logbq_fit_device(a, 16, 4, 4e-3, None, p, None) == L.ERR_INVALID_ARG
+    assert h.logbq_fit_device(a, 16, 4, 4e-3, ws, None, None) == L.ERR_INVALID_ARG
+    assert h.logbq_fit_device(a, 1, 4, 4e-3, ws, p, None) == L.ERR_INVALID_ARG
+    for eps in (0.0, 1.0, -1.0, float("nan")):
+        assert h.logbq_fit_device(a, 16, 4, eps, ws, p, None) == L.ERR_INVALID_ARG
+    for bits in (2, 5, 16):
+        assert h.logbq_fit_device(a, 16, bits, 4e-3, ws, p, None) == L.ERR_UNSUPPORTED
+    assert h.logbq_fit_device(a, 2 ** 40, 4, 4e-3, ws, p, None) == L.ERR_UNSUPPORTED
+    assert h.logbq_fit_device(ctypes.c_void_p(4100), 16, 4, 4e-3, ws, p, None) == L.ERR_UNSUPPORTED
+    assert h.logbq_fit_device(a, 16, 4, 4e-3, ctypes.c_void_p(8196), p, None) == L.ERR_UNSUPPORTED
+    assert L.FIT_WORKSPACE_BYTES == 3 * 2048 * 8 + 8
