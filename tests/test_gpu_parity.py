@@ -336,6 +336,28 @@ def test_linear_multi_matches_single_launches():
                 assert rel_err(y.cpu().numpy(), x, wh) <= TOL
 
 
+def test_linear_multi_mixed_gemv_configurations():
+    """At one batch row and k = 8192, linears of up to 4096 rows take two wavefronts per row and
+    wider ones one; a grouped call then launches one GEMV per configuration, and every output
+    still equals the single-linear call bit for bit (and the oracle within tolerance)."""
+    k = 8192
+    ns = [4096, 4160, 2048, 300]
+    tensors = [prepare(n, k, [8, 9, 0, j]) for j, n in enumerate(ns)]
+    codes = [gpu_encode(w, p) for w, p, r in tensors]
+    whs = [O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
+           for w, p, r in tensors]
+    for m in (1, 2):
+        _say(f"linear_multi mixed configurations {ns} m={m}")
+        x = inputs.activations(m, k, seed=[8, 9, 1, m])
+        xd = torch.from_numpy(x).to(DEV)
+        ys = L.linear_multi(xd, [c for c, _ in codes], [cb for _, cb in codes])
+        for (c, cb), y, wh in zip(codes, ys, whs):
+            y1 = L.linear(xd, c, cb)
+            torch.cuda.synchronize()
+            assert torch.equal(y, y1)
+            assert rel_err(y.cpu().numpy(), x, wh) <= 2.5e-4
+
+
 # ---------------------------------------------------------------- full-size, sampled
 
 def test_full_size_layer_8192x28672_sampled():
