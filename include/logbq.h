@@ -107,7 +107,7 @@ int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
                   logbq_params* out);
 
 /* Bytes of device workspace logbq_fit_device needs. */
-#define LOGBQ_FIT_WORKSPACE_BYTES 49160
+#define LOGBQ_FIT_WORKSPACE_BYTES 110600
 
 /*
  * logbq_fit_device -- the per-tensor fit on device-resident weights (Sec. 3.1 Eq. 3-4,

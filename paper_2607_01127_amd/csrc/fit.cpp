@@ -86,6 +86,24 @@ struct Big {
     }
     if (carry) d.push_back(uint32_t(carry));
   }
+  // floor(this / 2^bits), plus one if any discarded bit was set (the ceiling).
+  void shr_ceil(int64_t bits) {
+    if (d.empty() || bits <= 0) return;
+    const size_t limbs = size_t(bits / 32);
+    const int rem = int(bits % 32);
+    bool lost = false;
+    for (size_t i = 0; i < limbs && i < d.size(); ++i) lost |= d[i] != 0;
+    if (limbs < d.size() && rem) lost |= (d[limbs] & ((1u << rem) - 1u)) != 0;
+    std::vector<uint32_t> r(d.size() > limbs ? d.size() - limbs : 0, 0);
+    for (size_t i = 0; i < r.size(); ++i) {
+      uint64_t v = d[i + limbs] >> rem;
+      if (rem && i + limbs + 1 < d.size()) v |= uint64_t(d[i + limbs + 1]) << (32 - rem);
+      r[i] = uint32_t(v);
+    }
+    d.swap(r);
+    trim();
+    if (lost) add(Big(1));
+  }
   void trim() { while (!d.empty() && d.back() == 0) d.pop_back(); }
   static int cmp(const Big& a, const Big& b) {
     if (a.d.size() != b.d.size()) return a.d.size() < b.d.size() ? -1 : 1;
@@ -333,7 +351,8 @@ int32_t fit_from_passes(int32_t bits, double eps, FitPassFn run, void* ctx, logb
   if (r.max_key == 0) return LOGBQ_ERR_DEGENERATE;
   const double wmax = (double)u2f(r.max_key);
 
-  // eps = N 2^e exactly (e < 0): an energy P reaches eps T iff P 2^-e >= N T.
+  // eps = N 2^e exactly (e < 0): an integer energy P reaches eps T iff P 2^-e >= N T, i.e.
+  // iff P >= ceil(N T 2^e).
   uint64_t N;
   int64_t e;
   split_f64(eps, N, e);
@@ -342,11 +361,8 @@ int32_t fit_from_passes(int32_t bits, double eps, FitPassFn run, void* ctx, logb
     if (r.bins[3 * b]) total.add(bin_energy(r.bins[3 * b + 1], r.bins[3 * b + 2], uint32_t(b) >> 3));
   Big target = total;
   target.mul_small(N);
-  auto reaches = [&](const Big& p) {
-    Big l = p;
-    l.shl(-e);
-    return Big::cmp(l, target) >= 0;
-  };
+  target.shr_ceil(-e);
+  auto reaches = [&](const Big& p) { return Big::cmp(p, target) >= 0; };
 
   // Energy and count of all weights below the current selection.
   Big below;
@@ -357,11 +373,10 @@ int32_t fit_from_passes(int32_t bits, double eps, FitPassFn run, void* ctx, logb
     for (int b = 0; b < nbins; ++b) {
       const uint64_t* w = pr.bins + 3 * b;
       if (w[0] == 0) continue;
-      Big eb = bin_energy(w[1], w[2], per_bin_exp ? uint32_t(b) >> 3 : exp_field);
       Big run_e = below;
-      run_e.add(eb);
+      run_e.add(bin_energy(w[1], w[2], per_bin_exp ? uint32_t(b) >> 3 : exp_field));
       if (reaches(run_e)) return b;
-      below = run_e;
+      below.d.swap(run_e.d);
       count_below += w[0];
     }
     return -1;

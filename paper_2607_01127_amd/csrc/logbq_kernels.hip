@@ -1949,8 +1949,9 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
 
 }  // namespace
 
-// One pass of the device fit: clear the workspace, run the pass, copy its bins to the host and
-// wait for them (the next pass's selection depends on them).
+// One pass of the device fit: run the pass into its own region of the workspace (all regions
+// are cleared by one fill before pass 1), copy its bins to the host and wait for them (the next
+// pass's selection depends on them).
 struct FitDeviceCtx {
   const float* w;
   int64_t n;
@@ -1959,36 +1960,54 @@ struct FitDeviceCtx {
   std::vector<uint64_t> host;
 };
 
-constexpr int kFitWords = 3 * logbq_detail::kFitBins1 + 1;   // bins, then the pass-1 flags
-static_assert(logbq_detail::kFitBins1 >= logbq_detail::kFitBins2 &&
-              logbq_detail::kFitBins1 >= logbq_detail::kFitBins3, "largest pass");
+// Workspace words: the pass-1 flags, then the bins of passes 1, 2 and 3.
+constexpr int kFitOff1 = 1;
+constexpr int kFitOff2 = kFitOff1 + 3 * logbq_detail::kFitBins1;
+constexpr int kFitOff3 = kFitOff2 + 3 * logbq_detail::kFitBins2;
+constexpr int kFitWords = kFitOff3 + 3 * logbq_detail::kFitBins3;
 static_assert(kFitWords * 8 == LOGBQ_FIT_WORKSPACE_BYTES, "workspace size in the header");
 
 int32_t fit_device_pass(void* vctx, int pass, uint32_t sel, logbq_detail::FitPassResult* res) {
   FitDeviceCtx& c = *static_cast<FitDeviceCtx*>(vctx);
-  hipLaunchKernelGGL(k_fill_u64, dim3((kFitWords + 255) / 256), dim3(256), 0, c.st, c.ws,
-                     kFitWords);
-  if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
+  if (pass == 1) {
+    hipLaunchKernelGGL(k_fill_u64, dim3((kFitWords + 255) / 256), dim3(256), 0, c.st, c.ws,
+                       kFitWords);
+    if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
+  }
   const unsigned grid = (unsigned)((c.n + kFitChunk - 1) / kFitChunk);
-  unsigned int* flags = reinterpret_cast<unsigned int*>(c.ws + 3 * logbq_detail::kFitBins1);
-  if (pass == 1)
-    hipLaunchKernelGGL(k_fit_hist<1>, dim3(grid), dim3(kFitThreads), 0, c.st, c.w, c.n, sel, c.ws,
-                       flags);
-  else if (pass == 2)
-    hipLaunchKernelGGL(k_fit_hist<2>, dim3(grid), dim3(kFitThreads), 0, c.st, c.w, c.n, sel, c.ws,
-                       flags);
-  else
-    hipLaunchKernelGGL(k_fit_hist<3>, dim3(grid), dim3(kFitThreads), 0, c.st, c.w, c.n, sel, c.ws,
-                       flags);
+  unsigned int* flags = reinterpret_cast<unsigned int*>(c.ws);
+  int off, words;
+  if (pass == 1) {
+    off = 0;   // the flags are copied with pass 1's bins
+    words = kFitOff2;
+    hipLaunchKernelGGL(k_fit_hist<1>, dim3(grid), dim3(kFitThreads), 0, c.st, c.w, c.n, sel,
+                       c.ws + kFitOff1, flags);
+  } else if (pass == 2) {
+    off = kFitOff2;
+    words = kFitOff3 - kFitOff2;
+    hipLaunchKernelGGL(k_fit_hist<2>, dim3(grid), dim3(kFitThreads), 0, c.st, c.w, c.n, sel,
+                       c.ws + kFitOff2, flags);
+  } else {
+    off = kFitOff3;
+    words = kFitWords - kFitOff3;
+    hipLaunchKernelGGL(k_fit_hist<3>, dim3(grid), dim3(kFitThreads), 0, c.st, c.w, c.n, sel,
+                       c.ws + kFitOff3, flags);
+  }
   if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
-  c.host.assign(kFitWords, 0);
-  if (hipMemcpyAsync(c.host.data(), c.ws, (size_t)kFitWords * 8, hipMemcpyDeviceToHost, c.st) !=
-      hipSuccess)
+  c.host.assign((size_t)words, 0);
+  if (hipMemcpyAsync(c.host.data(), c.ws + off, (size_t)words * 8, hipMemcpyDeviceToHost,
+                     c.st) != hipSuccess)
     return LOGBQ_ERR_HIP;
   if (hipStreamSynchronize(c.st) != hipSuccess) return LOGBQ_ERR_HIP;
-  res->bins = c.host.data();
-  res->max_key = (uint32_t)c.host[kFitWords - 1];
-  res->nonfinite = (uint32_t)(c.host[kFitWords - 1] >> 32);
+  if (pass == 1) {
+    res->bins = c.host.data() + kFitOff1;
+    res->max_key = (uint32_t)c.host[0];
+    res->nonfinite = (uint32_t)(c.host[0] >> 32);
+  } else {
+    res->bins = c.host.data();
+    res->max_key = 0;
+    res->nonfinite = 0;
+  }
   return LOGBQ_OK;
 }
 

@@ -87,7 +87,7 @@ SIGNATURES = {
                                    POINTER(Params), c_void_p]),
 }
 
-FIT_WORKSPACE_BYTES = 49160
+FIT_WORKSPACE_BYTES = 110600
 
 ABI_VERSION = 2
 

@@ -134,4 +134,4 @@ def test_fit_device_validation_before_hip():
     assert h.logbq_fit_device(a, 2 ** 40, 4, 4e-3, ws, p, None) == L.ERR_UNSUPPORTED
     assert h.logbq_fit_device(ctypes.c_void_p(4100), 16, 4, 4e-3, ws, p, None) == L.ERR_UNSUPPORTED
     assert h.logbq_fit_device(a, 16, 4, 4e-3, ctypes.c_void_p(8196), p, None) == L.ERR_UNSUPPORTED
-    assert L.FIT_WORKSPACE_BYTES == 3 * 2048 * 8 + 8
+    assert L.FIT_WORKSPACE_BYTES == (1 + 3 * (2048 + 512 + 2048)) * 8
