@@ -14,7 +14,7 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
-CHUNK = 1 << 18          # weights per workgroup of one pass
+CHUNK = 1 << 18          # weights per workgroup of passes 2 and 3 (twice that in pass 1)
 
 
 def _say(msg):
