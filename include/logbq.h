@@ -136,6 +136,16 @@ int32_t logbq_fit_device(const float* w_dev, int64_t numel, int32_t bits, double
                          void* workspace_dev, logbq_params* out, void* stream);
 
 /*
+ * logbq_fit_exact -- logbq_fit_device's fit on host weights: the same three radix-selection
+ * passes, run on the host, and the same exact selection, so the parameters equal
+ * logbq_fit_device's bit for bit (Sec. 3.2 Eq. 5 with exact sums, Sec. 3.1 Eq. 3-4).
+ *   w_host, numel, bits, eps, out: as logbq_fit (2 <= numel < 2^40).
+ * Errors: as logbq_fit. Reentrant; allocates at most 48 KiB of host scratch.
+ */
+int32_t logbq_fit_exact(const float* w_host, int64_t numel, int32_t bits, double eps,
+                        logbq_params* out);
+
+/*
  * logbq_encode -- Quant (Eq. 1) of a weight matrix into 4-bit or 8-bit codes (Sec. 3.3 packing).
  *   w_dev        : device, [n][k] float32 weights.
  *   n, k         : shape; k % 32 == 0.

@@ -418,3 +418,58 @@ int32_t fit_from_passes(int32_t bits, double eps, FitPassFn run, void* ctx, logb
 }
 
 }  // namespace logbq_detail
+
+// ---- the device fit's passes on the host -------------------------------------------------
+
+namespace {
+
+struct HostPassCtx {
+  const float* w;
+  int64_t n;
+  std::vector<uint64_t> bins;
+};
+
+// The three radix-selection passes of fit_detail.h over host weights, one weight at a time.
+int32_t host_pass(void* vctx, int pass, uint32_t sel, logbq_detail::FitPassResult* res) {
+  HostPassCtx& c = *static_cast<HostPassCtx*>(vctx);
+  const int nb = pass == 1 ? logbq_detail::kFitBins1
+               : pass == 2 ? logbq_detail::kFitBins2 : logbq_detail::kFitBins3;
+  c.bins.assign(3 * (size_t)nb, 0);
+  uint32_t kmax = 0, bad = 0;
+  for (int64_t i = 0; i < c.n; ++i) {
+    const uint32_t key = f2u(c.w[i]) & 0x7FFFFFFFu;
+    uint32_t bin;
+    if (pass == 1) {
+      kmax = key > kmax ? key : kmax;
+      bad |= key >= 0x7F800000u ? 1u : 0u;
+      bin = key >> 20;
+    } else if (pass == 2) {
+      if ((key >> 20) != sel) continue;
+      bin = (key >> 11) & 0x1FFu;
+    } else {
+      if ((key >> 11) != sel) continue;
+      bin = key & 0x7FFu;
+    }
+    const uint64_t m = (key & 0x7FFFFFu) | (key >= 0x800000u ? 0x800000u : 0u);
+    const uint64_t q = m * m;
+    c.bins[3 * bin] += 1;
+    c.bins[3 * bin + 1] += q >> 24;
+    c.bins[3 * bin + 2] += q & 0xFFFFFFu;
+  }
+  res->bins = c.bins.data();
+  res->max_key = kmax;
+  res->nonfinite = bad;
+  return LOGBQ_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t logbq_fit_exact(const float* w_host, int64_t numel, int32_t bits, double eps,
+                                   logbq_params* out) {
+  if (!w_host || !out || numel < 2) return LOGBQ_ERR_INVALID_ARG;
+  if (!(eps > 0.0 && eps < 1.0)) return LOGBQ_ERR_INVALID_ARG;
+  if (bits != 4 && bits != 8) return LOGBQ_ERR_UNSUPPORTED;
+  if (numel >= (int64_t(1) << 40)) return LOGBQ_ERR_UNSUPPORTED;
+  HostPassCtx c{w_host, numel, {}};
+  return logbq_detail::fit_from_passes(bits, eps, host_pass, &c, out);
+}

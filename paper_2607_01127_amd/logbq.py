@@ -85,6 +85,7 @@ SIGNATURES = {
                              POINTER(Uniform), c_void_p, c_void_p, c_void_p]),
     "logbq_fit_device": (c_int32, [c_void_p, c_int64, c_int32, c_double, c_void_p,
                                    POINTER(Params), c_void_p]),
+    "logbq_fit_exact": (c_int32, [POINTER(c_float), c_int64, c_int32, c_double, POINTER(Params)]),
 }
 
 FIT_WORKSPACE_BYTES = 110600
@@ -148,6 +149,17 @@ def fit(w, bits: int = 4, eps: float = 4e-3) -> Params:
     p = Params()
     _check(lib().logbq_fit(w.ctypes.data_as(POINTER(c_float)), w.size, bits, eps,
                            ctypes.byref(p)), "logbq_fit")
+    return p
+
+
+def fit_exact(w, bits: int = 4, eps: float = 4e-3) -> Params:
+    """logbq_fit_exact on host float32 weights: the device fit's parameters, computed on the host."""
+    if hasattr(w, "detach"):
+        w = w.detach().cpu().numpy()
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    p = Params()
+    _check(lib().logbq_fit_exact(w.ctypes.data_as(POINTER(c_float)), w.size, bits, eps,
+                                 ctypes.byref(p)), "logbq_fit_exact")
     return p
 
 

@@ -1,6 +1,7 @@
 """Pins of the exact-sum reading of Eq. 5 (Sec. 3.2) in the oracle (``fit_exact``), which the
-device fit must reproduce bit for bit, and host-side checks of logbq_fit_device's argument
-validation (no GPU). The pins come from outside the function: hand-derived results, the
+device fit must reproduce bit for bit; host-side checks of logbq_fit_device's argument
+validation; and the library's host run of the device fit's passes and exact selection
+(logbq_fit_exact) bit for bit against the oracle (no GPU). The pins come from outside the function: hand-derived results, the
 sequential float64 fit where the two readings cannot differ, a rational-arithmetic
 certificate of w_min computed another way, and invariances of the definition."""
 import ctypes
@@ -135,3 +136,78 @@ def test_fit_device_validation_before_hip():
     assert h.logbq_fit_device(ctypes.c_void_p(4100), 16, 4, 4e-3, ws, p, None) == L.ERR_UNSUPPORTED
     assert h.logbq_fit_device(a, 16, 4, 4e-3, ctypes.c_void_p(8196), p, None) == L.ERR_UNSUPPORTED
     assert L.FIT_WORKSPACE_BYTES == (1 + 3 * (2048 + 512 + 2048)) * 8
+
+
+def _assert_exact_params(p, r, bits):
+    q = 2 ** (bits - 1) - 1
+    assert (p.bits, p.qmax) == (bits, q)
+    assert (p.wmin, p.wmax, p.wmin_index) == (r.wmin, r.wmax, r.wmin_index)
+    assert (p.base, p.shift) == (r.base, r.shift)
+    assert p.codebook_array().view(np.uint32).tolist() == \
+        O.codebook(r.base, r.shift, bits).view(np.uint32).tolist()
+    assert p.thresholds_array()[:q].view(np.uint32).tolist() == \
+        O.magnitude_thresholds(r.base, r.shift, bits).view(np.uint32).tolist()
+
+
+@pytest.mark.parametrize("w,eps", [
+    (np.array([1, 1, 1, 1, 2], np.float32), 0.5),
+    (np.array([2.0 ** -30] * 100 + [1.0], np.float32), 50 * 2.0 ** -60),
+    ((np.array([1, 2, 3, 4, 100.]) * 2.0 ** -149).astype(np.float32), 1e-3),
+    (np.array([0.25, -1.0], np.float32), 0.05),
+], ids=["tie", "float64-sums-round", "subnormals", "two-weights"])
+def test_library_exact_fit_hand_cases(w, eps):
+    _assert_exact_params(L.fit_exact(w, 4, eps), O.fit_exact(w, 4, eps), 4)
+
+
+def test_library_exact_fit_random():
+    """The device fit's passes and exact selection, run on the host, against the oracle."""
+    rng = np.random.default_rng(91)
+    for i in range(40):
+        n = int(rng.integers(2, 40000))
+        # 8-bit fits at weight magnitudes near 1 (at 1e-35 or 1e30 the shift s reaches thousands
+        # and the exact thresholds take minutes); 4-bit ones over the whole float32 range
+        lg = rng.uniform(-6, 2) if i % 2 else rng.uniform(-42, 30)
+        w = (rng.standard_t([2.5, 3, 4, 8][i % 4], n) * 10 ** lg).astype(np.float32)
+        if i % 5 == 0:
+            w[rng.integers(0, n, n // 3)] = 0.0
+        if i % 7 == 0:
+            w = (np.round(w / np.abs(w).max() * 50) * 0.01).astype(np.float32)
+        bits, eps = [4, 8][i % 2], [4e-3, 1e-6, 0.1, 0.5][i % 4]
+        try:
+            r = O.fit_exact(w, bits, eps)
+        except O.OracleError as e:
+            with pytest.raises(L.LogbqError) as err:
+                L.fit_exact(w, bits, eps)
+            assert err.value.status == {"nonfinite": L.ERR_NONFINITE,
+                                        "degenerate": L.ERR_DEGENERATE}[e.kind]
+            continue
+        _assert_exact_params(L.fit_exact(w, bits, eps), r, bits)
+
+
+@pytest.mark.parametrize("name", ["up_2048x8192_outliers", "layer_8192x28672"])
+def test_library_exact_fit_workload_slices(name):
+    wl = inputs.WORKLOADS[name]
+    lin = wl["layers"][0]
+    w = np.asarray(inputs.student_t_weights(512, lin.k, wl["nu"], wl["scale"],
+                                            seed=[wl["cfg"], 1, 0, 0],
+                                            outlier_frac=wl.get("outlier_frac", 0.0)))
+    _assert_exact_params(L.fit_exact(w), O.fit_exact(w), 4)
+    _assert_exact_params(L.fit_exact(w, 8, 1e-6), O.fit_exact(w, 8, 1e-6), 8)
+
+
+def test_library_exact_fit_errors():
+    for w, status in [(np.array([1.0, np.nan], np.float32), L.ERR_NONFINITE),
+                      (np.array([1.0, -np.inf], np.float32), L.ERR_NONFINITE),
+                      (np.zeros(8, np.float32), L.ERR_DEGENERATE),
+                      (np.array([0.5, -0.5, 0.5, 0.0], np.float32), L.ERR_DEGENERATE),
+                      (np.array([0.5], np.float32), L.ERR_INVALID_ARG)]:
+        with pytest.raises(L.LogbqError) as e:
+            L.fit_exact(w)
+        assert e.value.status == status
+    for eps in (0.0, 1.0, float("nan")):
+        with pytest.raises(L.LogbqError) as e:
+            L.fit_exact(np.array([0.5, 1.0], np.float32), eps=eps)
+        assert e.value.status == L.ERR_INVALID_ARG
+    with pytest.raises(L.LogbqError) as e:
+        L.fit_exact(np.array([0.5, 1.0], np.float32), bits=5)
+    assert e.value.status == L.ERR_UNSUPPORTED
