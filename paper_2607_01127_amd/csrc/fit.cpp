@@ -86,6 +86,28 @@ struct Big {
     }
     if (carry) d.push_back(uint32_t(carry));
   }
+  Big mul(const Big& o) const {
+    Big r;
+    if (d.empty() || o.d.empty()) return r;
+    r.d.assign(d.size() + o.d.size(), 0);
+    for (size_t i = 0; i < d.size(); ++i) {
+      uint64_t carry = 0;
+      for (size_t j = 0; j < o.d.size(); ++j) {
+        const uint64_t t = uint64_t(d[i]) * o.d[j] + r.d[i + j] + carry;
+        r.d[i + j] = uint32_t(t);
+        carry = t >> 32;
+      }
+      size_t k = i + o.d.size();
+      while (carry) {
+        const uint64_t t = uint64_t(r.d[k]) + carry;
+        r.d[k] = uint32_t(t);
+        carry = t >> 32;
+        ++k;
+      }
+    }
+    r.trim();
+    return r;
+  }
   // floor(this / 2^bits), plus one if any discarded bit was set (the ceiling).
   void shr_ceil(int64_t bits) {
     if (d.empty() || bits <= 0) return;
@@ -129,8 +151,20 @@ void split_f64(double b, uint64_t& B, int64_t& eb) {
   else { B = m | (uint64_t(1) << 52); eb = int64_t(e) - 1075; }
 }
 
-// Exact test f >= b^(n/2) for odd n, i.e. f^2 >= b^n (f >= 0 finite, b > 1 finite).
-bool ge_half_power(float f, double b, int64_t n) {
+// B^e (e >= 0) by repeated squaring.
+Big pow_big(uint64_t B, int64_t e) {
+  Big r(1), x(B);
+  while (e > 0) {
+    if (e & 1) r = r.mul(x);
+    e >>= 1;
+    if (e > 0) x = x.mul(x);
+  }
+  return r;
+}
+
+// Exact test f >= b^(n/2) for odd n, i.e. f^2 >= b^n (f >= 0 finite, b > 1 finite), given
+// pw = B^|n| where b = B 2^eb.
+bool ge_half_power(float f, double b, int64_t n, const Big& pw) {
   uint64_t F, B; int64_t ef, eb;
   split_f32(f, F, ef);
   if (F == 0) return false;
@@ -138,35 +172,37 @@ bool ge_half_power(float f, double b, int64_t n) {
   if (n >= 0) {
     // F^2 2^(2ef) >= B^n 2^(n eb)
     Big lhs(F); lhs.mul_small(F);
-    Big rhs(1); for (int64_t i = 0; i < n; ++i) rhs.mul_small(B);
+    Big rhs = pw;
     const int64_t d = 2 * ef - n * eb;
     if (d >= 0) lhs.shl(d); else rhs.shl(-d);
     return Big::cmp(lhs, rhs) >= 0;
   }
   // F^2 2^(2ef) B^m 2^(m eb) >= 1  with m = -n
   const int64_t m = -n;
-  Big lhs(F); lhs.mul_small(F);
-  for (int64_t i = 0; i < m; ++i) lhs.mul_small(B);
+  Big lhs = pw;
+  lhs.mul_small(F);
+  lhs.mul_small(F);
   const int64_t e = -2 * ef - m * eb;   // need lhs >= 2^e
   if (e <= 0) return true;              // lhs >= 1
   Big rhs(1); rhs.shl(e);
   return Big::cmp(lhs, rhs) >= 0;
 }
 
-// Smallest float32 t with t >= b^(k + 1/2 - s); +inf beyond the float32 range.
-float exact_threshold(double b, int32_t s, int k) {
+// Smallest float32 t with t >= b^(k + 1/2 - s); +inf beyond the float32 range. pw = B^|n| for
+// n = 2k + 1 - 2s, b = B 2^eb.
+float exact_threshold(double b, int32_t s, int k, const Big& pw) {
   const int64_t n = 2 * int64_t(k) + 1 - 2 * int64_t(s);
   const long double approx = powl((long double)b, (long double)k + 0.5L - (long double)s);
   if (!(approx <= (long double)FLT_MAX * 2)) return std::numeric_limits<float>::infinity();
   float f = approx > (long double)FLT_MAX ? FLT_MAX : (float)approx;
   const float inf = std::numeric_limits<float>::infinity();
-  while (!ge_half_power(f, b, n)) {
+  while (!ge_half_power(f, b, n, pw)) {
     f = std::nextafter(f, inf);
     if (std::isinf(f)) return f;
   }
   while (f > 0.0f) {
     const float g = std::nextafter(f, 0.0f);
-    if (ge_half_power(g, b, n)) f = g; else break;
+    if (ge_half_power(g, b, n, pw)) f = g; else break;
   }
   return f;
 }
@@ -315,9 +351,36 @@ int32_t finish_params(int32_t bits, double eps, double wmin, double wmax, int64_
   p.codebook[0] = 0.0f;
   p.codebook[half] = 0.0f;
   const int nthr = (int)(sizeof(p.thresholds) / sizeof(p.thresholds[0]));
-  for (int k = 0; k < nthr; ++k)
-    p.thresholds[k] = k < qmax ? exact_threshold(b, p.shift, k)
-                               : std::numeric_limits<float>::infinity();
+  for (int k = qmax; k < nthr; ++k) p.thresholds[k] = std::numeric_limits<float>::infinity();
+  // B^|n_k| for n_k = 2k + 1 - 2s (odd, never 0). The k with n_k > 0 are taken upward from the
+  // smallest such k, those with n_k < 0 downward from the largest: |n_k| grows by 2 per step
+  // in both sweeps, so each sweep squares once and then multiplies by B^2 per step.
+  uint64_t B;
+  int64_t eb;
+  split_f64(b, B, eb);
+  auto nk = [&](int k) { return 2 * int64_t(k) + 1 - 2 * int64_t(p.shift); };
+  int kpos = 0;
+  while (kpos < qmax && nk(kpos) < 0) ++kpos;
+  if (kpos < qmax) {
+    Big pw = pow_big(B, nk(kpos));
+    for (int k = kpos; k < qmax; ++k) {
+      if (k > kpos) {
+        pw.mul_small(B);
+        pw.mul_small(B);
+      }
+      p.thresholds[k] = exact_threshold(b, p.shift, k, pw);
+    }
+  }
+  if (kpos > 0) {
+    Big pw = pow_big(B, -nk(kpos - 1));
+    for (int k = kpos - 1; k >= 0; --k) {
+      if (k < kpos - 1) {
+        pw.mul_small(B);
+        pw.mul_small(B);
+      }
+      p.thresholds[k] = exact_threshold(b, p.shift, k, pw);
+    }
+  }
   *out = p;
   return LOGBQ_OK;
 }

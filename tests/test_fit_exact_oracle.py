@@ -164,10 +164,9 @@ def test_library_exact_fit_random():
     rng = np.random.default_rng(91)
     for i in range(40):
         n = int(rng.integers(2, 40000))
-        # 8-bit fits at weight magnitudes near 1 (at 1e-35 or 1e30 the shift s reaches thousands
-        # and the exact thresholds take minutes); 4-bit ones over the whole float32 range
-        lg = rng.uniform(-6, 2) if i % 2 else rng.uniform(-42, 30)
-        w = (rng.standard_t([2.5, 3, 4, 8][i % 4], n) * 10 ** lg).astype(np.float32)
+        # magnitudes over the whole float32 range: 8-bit fits at 1e-35 or 1e30 have shifts s in
+        # the thousands, where the exact thresholds need powers b^n with n near 2 s
+        w = (rng.standard_t([2.5, 3, 4, 8][i % 4], n) * 10 ** rng.uniform(-42, 30)).astype(np.float32)
         if i % 5 == 0:
             w[rng.integers(0, n, n // 3)] = 0.0
         if i % 7 == 0:
