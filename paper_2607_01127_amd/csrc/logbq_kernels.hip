@@ -1422,11 +1422,11 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint16_t* __restrict__ x,
 // 64-bit add updates both. Pass 1, which adds every weight, keeps two copies of its bins (even
 // and odd lanes), halving the lanes of one instruction that hit the same LDS word; its 64 KiB
 // then fit two workgroups per CU, so its chunks are twice as long and the grid runs in one
-// round (measured on the 8192 x 28672 weights: the fit 0.868 -> 0.840 ms). (Measured on the 8192 x 28672 weights: chunks of 2^19 in the
-// selective passes halve their flushed bins but leave half the workgroups to stream, which
-// costs more.) Non-empty bins are then added to the global bins with 64-bit integer
-// atomics, which are exact and independent of order. Pass 1 also takes the largest bit pattern
-// and flags NaN / Inf.
+// round (measured on the 8192 x 28672 weights: the fit 0.868 -> 0.840 ms). Passes 2 and 3 keep
+// chunks of 2^18: longer ones halve the bins they flush but leave half the workgroups to
+// stream, which measured slower. Non-empty bins are then added to the global bins with 64-bit
+// integer atomics, which are exact and independent of order. Pass 1 also takes the largest bit
+// pattern and flags NaN / Inf.
 constexpr int64_t kFitChunk = int64_t(1) << 18;
 constexpr int kFitThreads = 512;
 __host__ __device__ constexpr int64_t fit_chunk(int pass) {
