@@ -14,7 +14,7 @@ use it. It shares no code with the HIP library.
                         column j after it.
 * ``output_error``   -- ||(W - W_hat) X^T||_F / ||W X^T||_F, the layer-output error GPTQ reduces.
 
-Readings (also listed in the design doc):
+Readings:
 
 * The paper calibrates with GPTQ but prints no algorithm; the steps are GPTQ's (Algorithm 1 of
   its paper, lazy batch updates with blocks of 128 columns, 1 % damping), in float32 as in its

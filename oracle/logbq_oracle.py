@@ -22,7 +22,7 @@ Python ``fractions`` for the few decisions that must be exact:
 * ``dequantize``   -- Dequant (Eq. 2) by table lookup (Sec. 3.3: LUT instead of b^x).
 * ``linear``       -- y = x . W_hat^T in float64.
 
-Readings of places where the paper is silent or garbled (each also listed in the design doc):
+Readings of places where the paper is silent or garbled:
 
 * Eq. 1 prints the clamp on the signed value; clamping sign(x)*round(...) to [-q_max, q_max]
   would send tiny weights to large values of the opposite sign. The magnitude index is

@@ -15,7 +15,7 @@ and ``bench.py``'s CPU legs may use it. It shares no code with the HIP library.
 * ``sqnr_db``            -- reconstruction signal-to-quantization-noise ratio.
 * ``relative_error``     -- ||y_hat - y|| / ||y|| of a product.
 
-Readings (also listed in the design doc):
+Readings:
 
 * The paper gives Quant(s, z, x) = round(x / s) - z with a scaling factor and a zero-point and
   follows LLM.int8 for the asymmetric baseline; it does not print s and z. Read as min-max
