@@ -258,3 +258,20 @@ def test_linear_path_rule():
     for bad in ((5, 1, 64, 1), (4, 1, 48, 1), (8, 1 << 40, 64, 1)):
         with pytest.raises(L.LogbqError):
             lp(*bad)
+
+
+@pytest.mark.parametrize("scale", [1e-35, 1e30])
+def test_fit8_extreme_shift_thresholds(scale):
+    """An 8-bit codebook (b near 1) on weights far from 1 has a shift s in the thousands; its
+    exact thresholds need b^n for n near 2 s. They equal the oracle's and take well under a
+    second (the fit builds each power once by squaring)."""
+    import time
+    w = (np.random.default_rng(3).standard_t(3, 4000) * scale).astype(np.float32)
+    t0 = time.perf_counter()
+    p = L.fit(w, 8, 0.5)
+    dt = time.perf_counter() - t0
+    r = O.fit(w, 8, 0.5)
+    assert abs(p.shift) > 1000 and p.shift == r.shift and p.base == r.base
+    assert p.thresholds_array()[:127].view(np.uint32).tolist() == \
+        O.magnitude_thresholds(r.base, r.shift, 8).view(np.uint32).tolist()
+    assert dt < 5.0, dt
