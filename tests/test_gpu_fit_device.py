@@ -2,7 +2,7 @@
 C ABI: every field of the parameters bit for bit against the oracle's ``fit_exact`` at sizes
 it finishes in seconds (spanning several workgroups and a ragged tail), the error statuses,
 and at the full 8192 x 28672 size a certificate of w_min in exact integer arithmetic plus
-equality with the host fit."""
+equality with the host run of the same passes (logbq_fit_exact) and with the host fit."""
 import numpy as np
 import pytest
 
@@ -141,6 +141,12 @@ def test_fit_device_full_layer_certificate():
     assert e_below * den < num * total <= (e_below + copies * v * v) * den
     j = -(-(num * total - den * e_below) // (den * v * v))
     assert p.wmin_index == int(np.count_nonzero(keys < vkey)) + j - 1
+    _say("  the same passes on the host")
+    e = L.fit_exact(w, 4, eps)
+    assert (e.wmin, e.wmax, e.wmin_index, e.base, e.shift) == \
+        (p.wmin, p.wmax, p.wmin_index, p.base, p.shift)
+    assert e.thresholds_array().view(np.uint32).tolist() == \
+        p.thresholds_array().view(np.uint32).tolist()
     _say("  host fit of the same tensor")
     h = L.fit(w, 4, eps)
     assert (h.wmin, h.wmax, h.wmin_index, h.base, h.shift) == \
