@@ -11,6 +11,7 @@
 #include <cstdint>
 #include <cstring>
 #include <limits>
+#include <thread>
 #include <vector>
 
 #include "fit_detail.h"
@@ -22,21 +23,50 @@ inline uint32_t f2u(float f) { uint32_t u; std::memcpy(&u, &f, 4); return u; }
 inline float u2f(uint32_t u) { float f; std::memcpy(&f, &u, 4); return f; }
 
 // LSD radix sort of non-negative float32 bit patterns (their integer order is their value
-// order). Three 11-bit passes; passes whose digit is constant over the input are skipped.
+// order). Three 11-bit passes; passes whose digit is constant over the input are skipped. Each
+// pass splits the input into T contiguous ranges: per-range digit counts give every (range,
+// digit) its own output offsets, and each range is scattered in order, so the sort is stable
+// and its result is the same for any T.
 void radix_sort_u32(std::vector<uint32_t>& a) {
   const size_t n = a.size();
+  unsigned nt = std::thread::hardware_concurrency();
+  nt = nt < 1 ? 1 : (nt > 16 ? 16 : nt);
+  if (n < (size_t(1) << 20)) nt = 1;
   std::vector<uint32_t> tmp(n);
   uint32_t* src = a.data();
   uint32_t* dst = tmp.data();
+  std::vector<size_t> cnt((size_t)nt * 2048);
+  auto run = [&](auto&& fn) {
+    if (nt == 1) { fn(0u); return; }
+    std::vector<std::thread> th;
+    for (unsigned t = 0; t < nt; ++t) th.emplace_back(fn, t);
+    for (auto& x : th) x.join();
+  };
+  auto lo = [&](unsigned t) { return n * t / nt; };
   for (int pass = 0; pass < 3; ++pass) {
     const int shift = pass * 11;
-    std::vector<size_t> count(2049, 0);
-    for (size_t i = 0; i < n; ++i) count[((src[i] >> shift) & 2047u) + 1]++;
+    std::fill(cnt.begin(), cnt.end(), size_t(0));
+    run([&](unsigned t) {
+      size_t* c = cnt.data() + (size_t)t * 2048;
+      for (size_t i = lo(t); i < lo(t + 1); ++i) c[(src[i] >> shift) & 2047u]++;
+    });
     bool constant = false;
-    for (int d = 1; d <= 2048; ++d) if (count[d] == n) { constant = true; break; }
+    size_t next = 0;
+    for (int d = 0; d < 2048; ++d) {
+      size_t tot = 0;
+      for (unsigned t = 0; t < nt; ++t) {
+        const size_t c = cnt[(size_t)t * 2048 + d];
+        cnt[(size_t)t * 2048 + d] = next + tot;   // output offset of (range t, digit d)
+        tot += c;
+      }
+      if (tot == n) constant = true;
+      next += tot;
+    }
     if (constant) continue;
-    for (int d = 1; d <= 2048; ++d) count[d] += count[d - 1];
-    for (size_t i = 0; i < n; ++i) dst[count[(src[i] >> shift) & 2047u]++] = src[i];
+    run([&](unsigned t) {
+      size_t* o = cnt.data() + (size_t)t * 2048;
+      for (size_t i = lo(t); i < lo(t + 1); ++i) dst[o[(src[i] >> shift) & 2047u]++] = src[i];
+    });
     std::swap(src, dst);
   }
   if (src != a.data()) std::memcpy(a.data(), src, n * sizeof(uint32_t));
