@@ -11,9 +11,11 @@
  *
  * Conventions shared by every call
  *   - Every call validates all of its arguments before it touches the GPU, and returns a
- *     logbq_status. Nothing is allocated and nothing is synchronised inside a call; device
- *     calls are enqueued on the given stream and return at once, so they can be captured in a
- *     HIP graph. Faults of an enqueued kernel surface at the caller's next synchronisation.
+ *     logbq_status. No device memory is allocated inside a call. Device calls are enqueued on
+ *     the given stream and return at once, so they can be captured in a HIP graph; the one
+ *     exception is logbq_fit_device, which waits for each of its passes because the host
+ *     chooses the next pass's bin. Faults of an enqueued kernel surface at the caller's next
+ *     synchronisation.
  *   - `stream` is a hipStream_t passed as void*; NULL is the default stream.
  *   - The caller owns every buffer. "device" pointers are HIP device memory of the current
  *     device; "host" pointers are ordinary host memory.
@@ -43,7 +45,8 @@ typedef enum logbq_status {
   LOGBQ_ERR_NONFINITE = 2,     /* fit: a weight is NaN or Inf                           */
   LOGBQ_ERR_DEGENERATE = 3,    /* fit: all weights zero, or w_min == w_max (b = 1)      */
   LOGBQ_ERR_UNSUPPORTED = 4,   /* bits not 4 or 8, K % 32 != 0, misaligned, too large    */
-  LOGBQ_ERR_HIP = 5            /* a HIP call failed (no device, launch failure, ...)    */
+  LOGBQ_ERR_HIP = 5,           /* a HIP call failed (no device, launch failure, ...)    */
+  LOGBQ_ERR_HOST_RESOURCE = 6  /* host scratch memory could not be allocated              */
 } logbq_status;
 
 /* Per-tensor codebook parameters (Sec. 3.1, Sec. 3.2). Plain data; copy freely.
@@ -100,8 +103,11 @@ const char* logbq_status_str(int32_t status);
  * k = 1..q_max), codebook[0] = codebook[h] = +0. thresholds[k] is exact: the smallest float32
  * t with t >= b^(k + 1/2 - s).
  * Errors: INVALID_ARG (null, numel < 2, eps outside (0,1)), UNSUPPORTED (bits not 4 or 8),
- * NONFINITE (NaN/Inf weight), DEGENERATE (w_max == 0, or w_min == w_max).
- * Reentrant; allocates host scratch of 4*numel bytes internally for the sort.
+ * NONFINITE (NaN/Inf weight), DEGENERATE (w_max == 0, or w_min == w_max), HOST_RESOURCE (the
+ * host scratch could not be allocated).
+ * Reentrant; allocates host scratch of 8*numel bytes internally for the sort, which runs on up
+ * to 16 threads (LOGBQ_HOST_THREADS = 1..16 in the environment sets the count; the result does
+ * not depend on it; if no thread can be started the sort runs on the calling thread).
  */
 int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
                   logbq_params* out);
@@ -130,7 +136,8 @@ int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
  * the stream has run the passes (not capturable in a HIP graph).
  * Errors: INVALID_ARG (null, numel < 2, eps outside (0,1)), UNSUPPORTED (bits not 4 or 8,
  * numel too large, misaligned), NONFINITE (NaN/Inf weight), DEGENERATE (w_max == 0 or
- * w_min == w_max), HIP (a HIP call failed).
+ * w_min == w_max), HIP (a HIP call failed), HOST_RESOURCE (host copies of the bins could not
+ * be allocated).
  */
 int32_t logbq_fit_device(const float* w_dev, int64_t numel, int32_t bits, double eps,
                          void* workspace_dev, logbq_params* out, void* stream);
@@ -140,7 +147,8 @@ int32_t logbq_fit_device(const float* w_dev, int64_t numel, int32_t bits, double
  * passes, run on the host, and the same exact selection, so the parameters equal
  * logbq_fit_device's bit for bit (Sec. 3.2 Eq. 5 with exact sums, Sec. 3.1 Eq. 3-4).
  *   w_host, numel, bits, eps, out: as logbq_fit (2 <= numel < 2^40).
- * Errors: as logbq_fit. Reentrant; allocates at most 48 KiB of host scratch.
+ * Errors: as logbq_fit (HOST_RESOURCE included). Reentrant; allocates at most 48 KiB of host
+ * scratch.
  */
 int32_t logbq_fit_exact(const float* w_host, int64_t numel, int32_t bits, double eps,
                         logbq_params* out);

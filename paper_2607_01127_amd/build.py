@@ -52,5 +52,35 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+CLANG = os.environ.get("LOGBQ_HOST_CLANG", "/opt/rocm/llvm/bin/clang++")
+
+
+def build_sanitized(sanitize: str, verbose: bool = False) -> str:
+    """A CPU-test build of liblogbq.so with LLVM sanitizers on its host code: `sanitize` is
+    "address,undefined" or "thread". The host fit (fit.cpp) and the host side of the kernel
+    source (argument checks, tables, launches) are instrumented; device code is not. The
+    library lands in _build/san_<kinds>/ and needs the matching runtime preloaded, e.g.
+    LD_PRELOAD=$(clang++ -print-file-name=libclang_rt.asan-x86_64.so) for address; point the
+    binding at it with LOGBQ_LIBRARY=<path>."""
+    tag = sanitize.replace(",", "_")
+    out_dir = os.path.join(BUILD, f"san_{tag}")
+    os.makedirs(out_dir, exist_ok=True)
+    san = [f"-fsanitize={sanitize}", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer",
+           "-g", "-shared-libsan"]
+    fit_o = os.path.join(out_dir, "fit.o")
+    ker_o = os.path.join(out_dir, "logbq_kernels.o")
+    host_flags = [f for f in HOST_FLAGS if f != "-O2"] + ["-O1"]
+    _run([CLANG, *host_flags, *san, "-c", os.path.join(CSRC, "fit.cpp"), "-o", fit_o], verbose)
+    _run([HIPCC, *HIP_FLAGS, *[a for f in san for a in ("-Xarch_host", f)], "-c",
+          os.path.join(CSRC, "logbq_kernels.hip"), "-o", ker_o], verbose)
+    lib = os.path.join(out_dir, "liblogbq.so")
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *san, "-o", lib, fit_o, ker_o],
+         verbose)
+    return lib
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    if "--sanitize" in sys.argv:
+        print(build_sanitized(sys.argv[sys.argv.index("--sanitize") + 1], verbose="-v" in sys.argv))
+    else:
+        print(build(verbose="-v" in sys.argv))

@@ -9,8 +9,11 @@
 #include <cfloat>
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <limits>
+#include <new>
+#include <system_error>
 #include <thread>
 #include <vector>
 
@@ -27,19 +30,38 @@ inline float u2f(uint32_t u) { float f; std::memcpy(&f, &u, 4); return f; }
 // pass splits the input into T contiguous ranges: per-range digit counts give every (range,
 // digit) its own output offsets, and each range is scattered in order, so the sort is stable
 // and its result is the same for any T.
-void radix_sort_u32(std::vector<uint32_t>& a) {
-  const size_t n = a.size();
+// Ranges per pass: LOGBQ_HOST_THREADS (1..16) when set, else the hardware threads (at most
+// 16); one range below 2^20 weights.
+unsigned sort_ranges(size_t n) {
   unsigned nt = std::thread::hardware_concurrency();
+  if (const char* env = std::getenv("LOGBQ_HOST_THREADS")) {
+    const long v = std::strtol(env, nullptr, 10);
+    if (v >= 1) nt = (unsigned)v;
+  }
   nt = nt < 1 ? 1 : (nt > 16 ? 16 : nt);
   if (n < (size_t(1) << 20)) nt = 1;
+  return nt;
+}
+
+void radix_sort_u32(std::vector<uint32_t>& a) {
+  const size_t n = a.size();
+  const unsigned nt = sort_ranges(n);
   std::vector<uint32_t> tmp(n);
   uint32_t* src = a.data();
   uint32_t* dst = tmp.data();
   std::vector<size_t> cnt((size_t)nt * 2048);
+  // Range t runs on a thread of its own, or on the calling thread when no thread can be
+  // started (the ranges are independent, so the result does not depend on where they run).
   auto run = [&](auto&& fn) {
     if (nt == 1) { fn(0u); return; }
     std::vector<std::thread> th;
-    for (unsigned t = 0; t < nt; ++t) th.emplace_back(fn, t);
+    th.reserve(nt);
+    unsigned started = 0;
+    try {
+      for (; started < nt; ++started) th.emplace_back(fn, started);
+    } catch (const std::system_error&) {
+    }
+    for (unsigned t = started; t < nt; ++t) fn(t);
     for (auto& x : th) x.join();
   };
   auto lo = [&](unsigned t) { return n * t / nt; };
@@ -304,15 +326,17 @@ const char* logbq_status_str(int32_t status) {
     case LOGBQ_ERR_DEGENERATE: return "degenerate weight range";
     case LOGBQ_ERR_UNSUPPORTED: return "unsupported shape, alignment or bit width";
     case LOGBQ_ERR_HIP: return "HIP runtime error";
+    case LOGBQ_ERR_HOST_RESOURCE: return "host memory could not be allocated";
     default: return "unknown status";
   }
 }
 
-int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
-                  logbq_params* out) {
-  if (!w_host || !out || numel < 2) return LOGBQ_ERR_INVALID_ARG;
-  if (!(eps > 0.0 && eps < 1.0)) return LOGBQ_ERR_INVALID_ARG;
-  if (bits != 4 && bits != 8) return LOGBQ_ERR_UNSUPPORTED;
+}  // extern "C"
+
+namespace {
+
+int32_t fit_sequential(const float* w_host, int64_t numel, int32_t bits, double eps,
+                       logbq_params* out) {
 
   // |w| as float32 bit patterns (sign cleared); reject NaN / Inf.
   std::vector<uint32_t> a((size_t)numel);
@@ -343,7 +367,19 @@ int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
   return finish_params(bits, eps, wmin, wmax, (int64_t)istar, out);
 }
 
-}  // extern "C"
+}  // namespace
+
+extern "C" int32_t logbq_fit(const float* w_host, int64_t numel, int32_t bits, double eps,
+                             logbq_params* out) {
+  if (!w_host || !out || numel < 2) return LOGBQ_ERR_INVALID_ARG;
+  if (!(eps > 0.0 && eps < 1.0)) return LOGBQ_ERR_INVALID_ARG;
+  if (bits != 4 && bits != 8) return LOGBQ_ERR_UNSUPPORTED;
+  try {
+    return fit_sequential(w_host, numel, bits, eps, out);
+  } catch (...) {   // host scratch (4 numel bytes twice) could not be allocated
+    return LOGBQ_ERR_HOST_RESOURCE;
+  }
+}
 
 namespace {
 
@@ -563,6 +599,10 @@ extern "C" int32_t logbq_fit_exact(const float* w_host, int64_t numel, int32_t b
   if (!(eps > 0.0 && eps < 1.0)) return LOGBQ_ERR_INVALID_ARG;
   if (bits != 4 && bits != 8) return LOGBQ_ERR_UNSUPPORTED;
   if (numel >= (int64_t(1) << 40)) return LOGBQ_ERR_UNSUPPORTED;
-  HostPassCtx c{w_host, numel, {}};
-  return logbq_detail::fit_from_passes(bits, eps, host_pass, &c, out);
+  try {
+    HostPassCtx c{w_host, numel, {}};
+    return logbq_detail::fit_from_passes(bits, eps, host_pass, &c, out);
+  } catch (...) {   // host scratch could not be allocated
+    return LOGBQ_ERR_HOST_RESOURCE;
+  }
 }

@@ -2103,9 +2103,13 @@ int32_t logbq_fit_device(const float* w_dev, int64_t numel, int32_t bits, double
   if (bits != 4 && bits != 8) return LOGBQ_ERR_UNSUPPORTED;
   if (numel >= (int64_t(1) << 40)) return LOGBQ_ERR_UNSUPPORTED;
   if (!aligned16(w_dev) || ((uintptr_t)workspace_dev & 7u) != 0) return LOGBQ_ERR_UNSUPPORTED;
-  FitDeviceCtx c{w_dev, numel, static_cast<unsigned long long*>(workspace_dev),
-                 (hipStream_t)stream, {}};
-  return logbq_detail::fit_from_passes(bits, eps, fit_device_pass, &c, out);
+  try {
+    FitDeviceCtx c{w_dev, numel, static_cast<unsigned long long*>(workspace_dev),
+                   (hipStream_t)stream, {}};
+    return logbq_detail::fit_from_passes(bits, eps, fit_device_pass, &c, out);
+  } catch (...) {   // host copies of the bins could not be allocated
+    return LOGBQ_ERR_HOST_RESOURCE;
+  }
 }
 
 int32_t logbq_gptq(float* w_dev, int64_t n, int64_t k, const float* u_dev, const logbq_params* p,

@@ -13,9 +13,12 @@ from ctypes import POINTER, c_double, c_float, c_int32, c_int64, c_uint8, c_uint
 
 import numpy as np
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblogbq.so")
+# LOGBQ_LIBRARY selects another build of the library (e.g. a sanitizer build for CPU tests).
+LIB_PATH = os.environ.get("LOGBQ_LIBRARY") or \
+    os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblogbq.so")
 
-OK, ERR_INVALID_ARG, ERR_NONFINITE, ERR_DEGENERATE, ERR_UNSUPPORTED, ERR_HIP = range(6)
+OK, ERR_INVALID_ARG, ERR_NONFINITE, ERR_DEGENERATE, ERR_UNSUPPORTED, ERR_HIP, ERR_HOST_RESOURCE = \
+    range(7)
 
 
 class LogbqUnavailable(RuntimeError):

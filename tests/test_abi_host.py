@@ -30,8 +30,9 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(h, n), n
     assert h.logbq_abi_version() == 2
     assert ctypes.sizeof(L.Params) == 4 + 4 + 8 * 4 + 4 + 4 + 8 + 4 * 256 + 4 * 128
-    for s in range(6):
-        assert L.status_str(s)
+    names_seen = {L.status_str(s) for s in range(7)}
+    assert len(names_seen) == 7 and "unknown status" not in names_seen
+    assert L.status_str(L.ERR_HOST_RESOURCE) == "host memory could not be allocated"
     assert L.status_str(99) == "unknown status"
 
 
@@ -275,3 +276,16 @@ def test_fit8_extreme_shift_thresholds(scale):
     assert p.thresholds_array()[:127].view(np.uint32).tolist() == \
         O.magnitude_thresholds(r.base, r.shift, 8).view(np.uint32).tolist()
     assert dt < 5.0, dt
+
+
+@pytest.mark.parametrize("threads", ["1", "3", "16"])
+def test_fit_same_for_any_sort_thread_count(threads, monkeypatch):
+    """The host fit's radix sort splits each pass over LOGBQ_HOST_THREADS ranges (one range
+    runs without starting a thread); the parameters are the same for any count and equal the
+    oracle's (3 * 2^20 + 5 weights, so the threaded path is taken)."""
+    w = inputs.student_t_weights(3 * 2 ** 20 + 5, 1, 4, 0.02, seed=[71, 0, 0, 0]).reshape(-1)
+    monkeypatch.setenv("LOGBQ_HOST_THREADS", threads)
+    p = L.fit(w)
+    r = O.fit(w)
+    assert (p.wmin, p.wmax, p.wmin_index, p.base, p.shift) == \
+        (r.wmin, r.wmax, r.wmin_index, r.base, r.shift)
