@@ -215,7 +215,7 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=Tr
             "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
             "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
             "algo_bytes": algo,
-            "path": L.linear_path(4, m, k, n)}
+            "path": L.linear_path(4, m, k, n), "kernel": L.linear_kernel(4, m, k, n, cb)}
     return results, {"n": n, "k": k, "packed": packed, "copies": copies, "fit_s": fit_s,
                      "params": {"base": p.base, "shift": p.shift, "wmin": p.wmin,
                                 "wmax": p.wmax}}, codes, cb
@@ -396,7 +396,7 @@ def bench_layer8(torch, L, inputs, dev, stream, ms, steps, warmup):
             "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
             "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
             "algo_bytes": algo, "copies": copies,
-            "path": L.linear_path(8, m, k, n)}
+            "path": L.linear_path(8, m, k, n), "kernel": L.linear_kernel(8, m, k, n, cb)}
     del code_list, codes
     return results
 
@@ -757,7 +757,7 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(algo / t_ms / 1e6 / HBM_PEAK_GBS, 4),
                      "traffic": profiled_traffic(),
-                     "kernel": "k_gemv<4, 1, 4, false, 2>", "algo_bytes_per_launch": algo,
+                     "kernel": main_row["kernel"], "algo_bytes_per_launch": algo,
                      "avg_launch_us": t_ms * 1e3,
                      "read_ceiling_GB_s": round(ceiling["GB_s"], 1),
                      "frac_of_read_ceiling": round(algo / t_ms / 1e6 / ceiling["GB_s"], 4)},

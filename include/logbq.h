@@ -312,6 +312,22 @@ typedef enum logbq_path {
 int32_t logbq_linear_path(int32_t bits, int64_t m, int64_t k, int64_t n, int32_t* path_out);
 
 /*
+ * logbq_linear_kernel -- name of the kernel instance (with its template arguments, as a
+ * profiler lists it) that the first launch of a logbq_linear / logbq_linear8 call of shape
+ * (m, k, n) runs, e.g. "k_gemv<4, 1, 4, false, 2>" (Sec. 3.3 product; the choice is this
+ * library's). Host only: needs no device and touches none.
+ *   bits, m, k, n : as logbq_linear_path; n fits in int32.
+ *   codebook      : host, 2^bits floats, or NULL for a fitted (sign-symmetric) codebook; the
+ *                   4-bit MFMA kernels dequantize in registers only for sign-symmetric ones.
+ *   name_out      : host, name_len bytes, receives a NUL-terminated name ("none" for an empty
+ *                   call, "k_fill_zero" for k = 0).
+ * Errors: INVALID_ARG (null name_out, buffer too short, negative size, non-finite codebook
+ * entry), UNSUPPORTED (bits, k % 32, m or n too large).
+ */
+int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const float* codebook,
+                            char* name_out, int64_t name_len);
+
+/*
  * logbq_dequantize8 -- Dequant (Eq. 2) of 8-bit codes: w[n][k] = codebook[codes[n][k]].
  *   codes_dev : device, [n][k]; codebook: host, 256 floats; w_dev: device, [n][k] float32.
  * Bit-exact. Errors: INVALID_ARG, UNSUPPORTED, HIP.

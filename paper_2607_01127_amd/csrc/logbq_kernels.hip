@@ -33,6 +33,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <cstdio>
 #include <cstring>
 #include <mutex>
 #include <vector>
@@ -2026,6 +2027,57 @@ int32_t fit_device_pass(void* vctx, int pass, uint32_t sel, logbq_detail::FitPas
   return LOGBQ_OK;
 }
 
+// Argument checks of the GPTQ entry points (everything but the device pointers) and the
+// quantizer they describe.
+int32_t gptq_validate(int64_t n, int64_t k, const logbq_params* p, const logbq_uniform* uniform,
+                      GptqQuant* qz_out) {
+  if (n < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
+  if ((p == nullptr) == (uniform == nullptr)) return LOGBQ_ERR_INVALID_ARG;
+  if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
+  if (n > INT32_MAX || k > INT32_MAX || (n != 0 && (n * k) / n != k)) return LOGBQ_ERR_UNSUPPORTED;
+  if (n > 65535LL * 16) return LOGBQ_ERR_UNSUPPORTED;   // rows are the after-block grid's y
+  GptqQuant qz;
+  std::memset(&qz, 0, sizeof(qz));
+  if (p) {
+    if (p->bits != 4 || p->qmax != 7) return LOGBQ_ERR_UNSUPPORTED;
+    for (int i = 0; i < 16; ++i) qz.cb[i] = p->codebook[i];
+    for (int i = 0; i < 7; ++i) qz.th[i] = p->thresholds[i];
+    for (int i = 7; i < 15; ++i) qz.th[i] = INFINITY;
+    qz.uniform = 0;
+  } else {
+    if (uniform->bits != 4) return LOGBQ_ERR_UNSUPPORTED;
+    for (int i = 0; i < 16; ++i) qz.cb[i] = uniform->codebook[i];
+    for (int i = 0; i < 15; ++i) qz.th[i] = uniform->thresholds[i];
+    qz.uniform = 1;
+  }
+  for (int i = 0; i < 16; ++i)
+    if (!std::isfinite(qz.cb[i])) return LOGBQ_ERR_INVALID_ARG;
+  for (int i = 0; i < 15; ++i) {
+    if (std::isnan(qz.th[i])) return LOGBQ_ERR_INVALID_ARG;
+    if (i > 0 && qz.th[i] < qz.th[i - 1]) return LOGBQ_ERR_INVALID_ARG;
+  }
+  *qz_out = qz;
+  return LOGBQ_OK;
+}
+
+// The column loop: per block of 128 columns, the panel kernel (quantize, in-block updates,
+// errors into err_dev) and, unless it is the last block, the after-block kernel.
+int32_t gptq_launch(float* w_dev, int N, int K, const float* u_dev, const GptqQuant& qz,
+                    float* err_dev, uint8_t* codes_dev, hipStream_t st) {
+  for (int i1 = 0; i1 < K; i1 += kGptqBlock) {
+    const int nb = K - i1 < kGptqBlock ? K - i1 : kGptqBlock;
+    hipLaunchKernelGGL(k_gptq_panel, dim3((unsigned)((N + 7) / 8)), dim3(512), 0, st, w_dev, N, K,
+                       u_dev, i1, nb, qz, err_dev, codes_dev);
+    if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
+    if (i1 + nb < K) {
+      hipLaunchKernelGGL(k_gptq_trail, dim3((unsigned)((K - i1 - nb + 63) / 64), (unsigned)((N + 15) / 16)),
+                         dim3(256), 0, st, w_dev, N, K, u_dev, i1, nb, err_dev);
+      if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
+    }
+  }
+  return LOGBQ_OK;
+}
+
 extern "C" {
 
 int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_params* p,
@@ -2115,49 +2167,13 @@ int32_t logbq_fit_device(const float* w_dev, int64_t numel, int32_t bits, double
 int32_t logbq_gptq(float* w_dev, int64_t n, int64_t k, const float* u_dev, const logbq_params* p,
                    const logbq_uniform* uniform, float* err_dev, uint8_t* codes_dev,
                    void* stream) {
-  if (n < 0 || k < 0) return LOGBQ_ERR_INVALID_ARG;
-  if ((p == nullptr) == (uniform == nullptr)) return LOGBQ_ERR_INVALID_ARG;
-  if (k % 32 != 0) return LOGBQ_ERR_UNSUPPORTED;
-  if (n > INT32_MAX || k > INT32_MAX || (n != 0 && (n * k) / n != k)) return LOGBQ_ERR_UNSUPPORTED;
-  if (n > 65535LL * 16) return LOGBQ_ERR_UNSUPPORTED;   // rows are the after-block grid's y
   GptqQuant qz;
-  std::memset(&qz, 0, sizeof(qz));
-  if (p) {
-    if (p->bits != 4 || p->qmax != 7) return LOGBQ_ERR_UNSUPPORTED;
-    for (int i = 0; i < 16; ++i) qz.cb[i] = p->codebook[i];
-    for (int i = 0; i < 7; ++i) qz.th[i] = p->thresholds[i];
-    for (int i = 7; i < 15; ++i) qz.th[i] = INFINITY;
-    qz.uniform = 0;
-  } else {
-    if (uniform->bits != 4) return LOGBQ_ERR_UNSUPPORTED;
-    for (int i = 0; i < 16; ++i) qz.cb[i] = uniform->codebook[i];
-    for (int i = 0; i < 15; ++i) qz.th[i] = uniform->thresholds[i];
-    qz.uniform = 1;
-  }
-  for (int i = 0; i < 16; ++i)
-    if (!std::isfinite(qz.cb[i])) return LOGBQ_ERR_INVALID_ARG;
-  for (int i = 0; i < 15; ++i) {
-    if (std::isnan(qz.th[i])) return LOGBQ_ERR_INVALID_ARG;
-    if (i > 0 && qz.th[i] < qz.th[i - 1]) return LOGBQ_ERR_INVALID_ARG;
-  }
-  if (n == 0 || k == 0) return LOGBQ_OK;
+  const int32_t v = gptq_validate(n, k, p, uniform, &qz);
+  if (v != LOGBQ_OK || n == 0 || k == 0) return v;
   if (!w_dev || !u_dev || !err_dev || !codes_dev) return LOGBQ_ERR_INVALID_ARG;
   if (!aligned16(w_dev) || !aligned16(u_dev) || !aligned16(err_dev) || !aligned16(codes_dev))
     return LOGBQ_ERR_UNSUPPORTED;
-  const hipStream_t st = (hipStream_t)stream;
-  const int N = (int)n, K = (int)k;
-  for (int i1 = 0; i1 < K; i1 += kGptqBlock) {
-    const int nb = K - i1 < kGptqBlock ? K - i1 : kGptqBlock;
-    hipLaunchKernelGGL(k_gptq_panel, dim3((unsigned)((N + 7) / 8)), dim3(512), 0, st, w_dev, N, K,
-                       u_dev, i1, nb, qz, err_dev, codes_dev);
-    if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
-    if (i1 + nb < K) {
-      hipLaunchKernelGGL(k_gptq_trail, dim3((unsigned)((K - i1 - nb + 63) / 64), (unsigned)((N + 15) / 16)),
-                         dim3(256), 0, st, w_dev, N, K, u_dev, i1, nb, err_dev);
-      if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
-    }
-  }
-  return LOGBQ_OK;
+  return gptq_launch(w_dev, (int)n, (int)k, u_dev, qz, err_dev, codes_dev, (hipStream_t)stream);
 }
 
 int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const float* codebook,
@@ -2254,6 +2270,56 @@ int32_t logbq_dequantize8(const uint8_t* codes_dev, int64_t n, int64_t k, const 
                      dim3(256), 0, (hipStream_t)stream, reinterpret_cast<const uint32_t*>(codes_dev),
                      reinterpret_cast<f32x4*>(w_dev), nwords, cb);
   return launch_status();
+}
+
+int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const float* codebook,
+                            char* name_out, int64_t name_len) {
+  if (!name_out || name_len < 1 || m < 0 || k < 0 || n < 0) return LOGBQ_ERR_INVALID_ARG;
+  if (bits != 4 && bits != 8) return LOGBQ_ERR_UNSUPPORTED;
+  if (k % 32 != 0 || m > kMaxBatchRows || k > INT32_MAX || n > INT32_MAX)
+    return LOGBQ_ERR_UNSUPPORTED;
+  const int entries = 1 << bits;
+  if (codebook)
+    for (int i = 0; i < entries; ++i)
+      if (!std::isfinite(codebook[i])) return LOGBQ_ERR_INVALID_ARG;
+  char buf[96];
+  if (m == 0 || n == 0) {
+    std::snprintf(buf, sizeof(buf), "none");
+  } else if (k == 0) {
+    std::snprintf(buf, sizeof(buf), "k_fill_zero");
+  } else {
+    const int M = (int)m, K = (int)k;
+    // Register dequantization needs a sign-symmetric codebook; every fitted one is, so a null
+    // codebook stands for a fitted one.
+    LutBytes tb;
+    float scale;
+    const bool symmetric = bits == 4 && (!codebook || make_lut_bytes(codebook, &tb, &scale));
+    const int path = bits == 4 ? choose_path<4>(M, K, n) : choose_path<8>(M, K, n);
+    int wk = 0, cpl = 0;
+    if (path == LOGBQ_PATH_SPLITK) {
+      const int nd = K / 256;
+      std::snprintf(buf, sizeof(buf), "k_mfma_sk<%d, %s>", nd, symmetric ? "false" : "true");
+    } else if (path == LOGBQ_PATH_GEMV) {
+      const bool ok = bits == 4 ? gemv_config_rows<4>(M, K, n, &wk, &cpl)
+                                : gemv_config_rows<8>(M, K, n, &wk, &cpl);
+      if (!ok) return LOGBQ_ERR_UNSUPPORTED;
+      const int nbuf = (cpl <= 2 && M <= 2) ? 3 : 2;
+      std::snprintf(buf, sizeof(buf), "k_gemv<%d, %d, %d, %s, %d>", bits, M, cpl,
+                    wk > 1 ? "true" : "false", nbuf);
+    } else if (path == LOGBQ_PATH_MFMA_KQ && symmetric) {
+      std::snprintf(buf, sizeof(buf), "k_mfma_kq");
+    } else {
+      int mt16 = (M + 15) / 16;
+      const int cap = symmetric ? 8 : 4;
+      if (mt16 > cap) mt16 = cap;
+      std::snprintf(buf, sizeof(buf), "k_mfma2<%d, %d, 4, %s, %s>", bits, mt16,
+                    symmetric ? "false" : "true", mt16 <= 2 ? "true" : "false");
+    }
+  }
+  const size_t need = std::strlen(buf) + 1;
+  if ((int64_t)need > name_len) return LOGBQ_ERR_INVALID_ARG;
+  std::memcpy(name_out, buf, need);
+  return LOGBQ_OK;
 }
 
 int32_t logbq_linear_path(int32_t bits, int64_t m, int64_t k, int64_t n, int32_t* path_out) {

@@ -81,6 +81,8 @@ SIGNATURES = {
     "logbq_dequantize8": (c_int32, [c_void_p, c_int64, c_int64, POINTER(c_float), c_void_p,
                                     c_void_p]),
     "logbq_linear_path": (c_int32, [c_int32, c_int64, c_int64, c_int64, POINTER(c_int32)]),
+    "logbq_linear_kernel": (c_int32, [c_int32, c_int64, c_int64, c_int64, POINTER(c_float),
+                                      ctypes.c_char_p, c_int64]),
     "logbq_fit_uniform": (c_int32, [POINTER(c_float), c_int64, c_int32, POINTER(Uniform)]),
     "logbq_encode_uniform": (c_int32, [c_void_p, c_int64, c_int64, POINTER(Uniform), c_void_p,
                                        c_void_p]),
@@ -304,6 +306,23 @@ def linear_path(bits: int, m: int, k: int, n: int) -> str:
     _check(lib().logbq_linear_path(int(bits), int(m), int(k), int(n), ctypes.byref(out)),
            "logbq_linear_path")
     return PATH_NAMES[out.value]
+
+
+def linear_kernel(bits: int, m: int, k: int, n: int, codebook=None) -> str:
+    """logbq_linear_kernel: the kernel instance (e.g. "k_gemv<4, 1, 4, false, 2>") that the first
+    launch of a linear / linear8 call of that shape runs; codebook None stands for a fitted
+    (sign-symmetric) one. Host only."""
+    buf = ctypes.create_string_buffer(96)
+    cb = None
+    if codebook is not None:
+        arr = np.ascontiguousarray(getattr(codebook, "codebook_array", lambda: codebook)(),
+                                   dtype=np.float32)
+        if arr.size != 1 << bits:
+            raise ValueError(f"codebook of {arr.size} entries for {bits}-bit codes")
+        cb = arr.ctypes.data_as(POINTER(c_float))
+    _check(lib().logbq_linear_kernel(int(bits), int(m), int(k), int(n), cb, buf, len(buf)),
+           "logbq_linear_kernel")
+    return buf.value.decode()
 
 
 def fit_uniform(w, bits: int = 4) -> Uniform:

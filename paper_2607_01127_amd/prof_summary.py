@@ -3,6 +3,7 @@
 kernel-stats: python -m paper_2607_01127_amd.prof_summary stats STATS_CSV CMD > profiles/X.md
 trace:        python -m paper_2607_01127_amd.prof_summary trace TRACE_CSV CMD > profiles/X.md
 counters:     python -m paper_2607_01127_amd.prof_summary counters PMC_CSV KERNEL_SUBSTR CMD > X.md
+mfma:         python -m paper_2607_01127_amd.prof_summary mfma PMC_CSV CUS XCDS CMD KERNEL... > X.md
 traffic:      python -m paper_2607_01127_amd.prof_summary traffic KERNEL_SUBSTR FETCH_CSV WRITE_CSV \
                   COPY_FETCH_CSV COPY_WRITE_CSV COPY_BYTES CMD > profiles/X.md
 
@@ -85,6 +86,35 @@ def counters(path, substr, cmd):
         print(f"- {name}: median {statistics.median(v):.6g} over {len(v)} dispatches")
 
 
+def mfma(path, cus, xcds, cmd, kernels):
+    """MFMA-pipe busy fraction per kernel from SQ_VALU_MFMA_BUSY_CYCLES (summed over every SIMD
+    of the chip; a v_mfma_f32_16x16x32_f16 adds 16 cycles, its issue time at the dense peak
+    rate), GRBM_GUI_ACTIVE (the GPU clock counter summed over the XCDs) and SQ_BUSY_CU_CYCLES.
+    busy = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x CUs x GRBM_GUI_ACTIVE / XCDs)."""
+    cus, xcds = int(cus), int(xcds)
+    print("# MFMA utilisation per dispatch (rocprofv3 --pmc)\n")
+    print(f"Command: `{cmd}`\n")
+    print(f"Normalisation: busy = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x {cus} CUs x "
+          f"GRBM_GUI_ACTIVE / {xcds} XCDs); SQ_VALU_MFMA_BUSY_CYCLES is summed over every SIMD "
+          f"(16 cycles per v_mfma_f32_16x16x32_f16), GRBM_GUI_ACTIVE over the {xcds} XCDs. "
+          f"Medians over the dispatches of each kernel.\n")
+    print("| kernel | dispatches | GRBM_GUI_ACTIVE | SQ_BUSY_CU_CYCLES | SQ_VALU_MFMA_BUSY_CYCLES "
+          "| cycles per XCD | MFMA busy |")
+    print("|---|---|---|---|---|---|---|")
+    for k in kernels:
+        vals = {}
+        for r in csv.DictReader(open(path)):
+            if _short(r["Kernel_Name"]).startswith(k):
+                vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+        g = statistics.median(vals.get("GRBM_GUI_ACTIVE", [float("nan")]))
+        b = statistics.median(vals.get("SQ_BUSY_CU_CYCLES", [float("nan")]))
+        mf = statistics.median(vals.get("SQ_VALU_MFMA_BUSY_CYCLES", [float("nan")]))
+        n = len(vals.get("GRBM_GUI_ACTIVE", []))
+        per_xcd = g / xcds
+        busy = mf / (4 * cus * per_xcd)
+        print(f"| `{k}` | {n} | {g:.6g} | {b:.6g} | {mf:.6g} | {per_xcd:.6g} | {busy:.3f} |")
+
+
 def _counter(path, substr, counter):
     vals = []
     for r in csv.DictReader(open(path)):
@@ -123,3 +153,5 @@ if __name__ == "__main__":
         trace(sys.argv[2], sys.argv[3])
     elif sys.argv[1] == "counters":
         counters(sys.argv[2], sys.argv[3], sys.argv[4])
+    elif sys.argv[1] == "mfma":
+        mfma(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6:])

@@ -261,6 +261,32 @@ def test_linear_path_rule():
             lp(*bad)
 
 
+def test_linear_kernel_names():
+    """The kernel instance a call runs, named as the profiler lists it (host logic)."""
+    lk = L.linear_kernel
+    assert lk(4, 1, 8192, 28672) == "k_gemv<4, 1, 4, false, 2>"
+    assert lk(4, 1, 14336, 4096) == "k_gemv<4, 1, 4, true, 2>"      # two wavefronts per row
+    assert lk(4, 1, 2048, 2048) == "k_gemv<4, 1, 1, false, 3>"
+    assert lk(4, 8, 8192, 28672) == "k_mfma_sk<32, false>"
+    assert lk(4, 32, 8192, 28672) == "k_mfma2<4, 2, 4, false, true>"
+    assert lk(4, 128, 8192, 28672) == "k_mfma_kq"
+    assert lk(8, 1, 8192, 28672) == "k_gemv<8, 1, 8, false, 2>"
+    assert lk(8, 128, 8192, 28672) == "k_mfma2<8, 4, 4, true, false>"
+    assert lk(4, 0, 8192, 28672) == "none" and lk(4, 3, 0, 5) == "k_fill_zero"
+    # a codebook that is not sign-symmetric takes the LDS table
+    cb = np.arange(16, dtype=np.float32)
+    assert lk(4, 8, 8192, 28672, cb) == "k_mfma_sk<32, true>"
+    assert lk(4, 128, 8192, 28672, cb) == "k_mfma2<4, 4, 4, true, false>"
+    sym = np.array([0] + [2.0 ** k for k in range(1, 8)] + [0] + [-(2.0 ** k) for k in range(1, 8)],
+                   dtype=np.float32)
+    assert lk(4, 128, 8192, 28672, sym) == "k_mfma_kq"
+    h = L.lib()
+    small = ctypes.create_string_buffer(4)
+    assert h.logbq_linear_kernel(4, 1, 64, 8, None, small, 4) == L.ERR_INVALID_ARG
+    assert h.logbq_linear_kernel(4, 1, 64, 8, None, None, 96) == L.ERR_INVALID_ARG
+    assert h.logbq_linear_kernel(5, 1, 64, 8, None, small, 4) == L.ERR_UNSUPPORTED
+
+
 @pytest.mark.parametrize("scale", [1e-35, 1e30])
 def test_fit8_extreme_shift_thresholds(scale):
     """An 8-bit codebook (b near 1) on weights far from 1 has a shift s in the thousands; its
