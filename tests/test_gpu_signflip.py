@@ -2,11 +2,16 @@
 symmetric, so flipping every sign bit negates every dequantized weight exactly).
 
 With K = 32 and activations that are zero except at chosen positions, each output of the GEMV
-is one v_dot2_f32_f16 (two products and a zero accumulator), two chained ones, or the full
-chain of one 32-weight chunk; each output of the stepped MFMA kernel at m = 32 is one
-v_mfma_f32_16x16x32_f16 over 2, 8 or 32 nonzero products (the later MFMAs of the step add
-zero products). The tests count the outputs whose negated-code result is not exactly the
-negation."""
+(m = 1) is one v_dot2_f32_f16 with a zero accumulator (k = 0, 1), a second one accumulating
+onto the first (k = 0, 1, 4, 5), or the chains of one 32-weight chunk; each output of the
+stepped MFMA kernel (m = 32) is one v_mfma_f32_16x16x32_f16 with a zero accumulator over 2, 4
+or 8 nonzero products (k < 8), or four MFMAs accumulating onto each other (k < 32). The other
+instructions of the chain add products of zero activations, which leave the accumulator
+unchanged. Measured on MI355X: with a zero accumulator both instructions negate exactly; once
+they add onto a nonzero accumulator, a few per cent of the results differ from the negation in
+the last bit of a partial sum (at most a few units of 2^-24 sum_k |x_k w_k|). So the float32
+accumulation of these instructions is not sign-symmetric, and the general sign-flip test of the
+linear kernels keeps a tolerance instead of bit equality."""
 import numpy as np
 import pytest
 
@@ -48,8 +53,18 @@ def test_sign_flip_single_instruction(m, live):
     torch.cuda.synchronize()
     y, yf = y.cpu().numpy(), yf.cpu().numpy()
     bad = int(np.count_nonzero(yf != -y))
-    kern = L.linear_kernel(4, m, 32, n, book)
-    _say(f"sign flip {kern} m={m} nonzero k={live}: {bad} of {y.size} outputs not exactly negated")
     wh = O.dequantize(O.unpack(codes.cpu().numpy()), book).astype(np.float64)
     absdot = np.abs(x.astype(np.float64)) @ np.abs(wh).T
-    assert np.all(np.abs(yf.astype(np.float64) + y) <= absdot * 2.0 ** -20)
+    absdot[absdot == 0] = 1.0
+    # differences in units of 2^-24 * sum_k |x_k w_k|: one last-bit difference in a partial sum
+    # of that size is at most 2 units
+    units = np.abs(yf.astype(np.float64) + y) / (absdot * 2.0 ** -24)
+    kern = L.linear_kernel(4, m, 32, n, book)
+    _say(f"sign flip {kern} m={m} nonzero k={live}: {bad} of {y.size} outputs not exactly negated, "
+         f"largest difference {float(np.max(units)):.2f} x 2^-24 sum|x w|")
+    one_instruction = max(live) < 2 if m == 1 else max(live) < 8
+    if one_instruction:
+        assert bad == 0        # zero accumulator: the result negates exactly
+    else:
+        assert bad > 0         # accumulating onto a nonzero value: not sign-symmetric
+    assert float(np.max(units)) <= 8.0
