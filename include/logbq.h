@@ -288,6 +288,23 @@ int32_t logbq_gptq(float* w_dev, int64_t n, int64_t k, const float* u_dev, const
                    const logbq_uniform* uniform, float* err_dev, uint8_t* codes_dev,
                    void* stream);
 
+/*
+ * logbq_gptq_noalloc -- logbq_gptq without a caller-provided workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc). Same arguments, results (bit for bit) and kernels as logbq_gptq, except
+ * err_dev: the [n][128] float32 error workspace is a fixed array in the library's code object,
+ * 8 MiB per device, held by every GPU the library runs on until the process ends.
+ *   w_dev, n, k, u_dev, p, uniform, codes_dev, stream: as logbq_gptq; n <= 16384.
+ * Allocates nothing (no hipMalloc, hipFree or allocating library call); the first call on a
+ * device looks up the array's device address once. Every call on a GPU uses that GPU's one
+ * array: calls that overlap on one GPU (e.g. on two streams) race and must be serialised by
+ * the caller. Each call writes every workspace entry it reads, so no clearing is needed.
+ * Errors: as logbq_gptq, and UNSUPPORTED for n > 16384.
+ */
+int32_t logbq_gptq_noalloc(float* w_dev, int64_t n, int64_t k, const float* u_dev,
+                           const logbq_params* p, const logbq_uniform* uniform,
+                           uint8_t* codes_dev, void* stream);
+
 /* Kernel that logbq_linear (bits 4) or logbq_linear8 (bits 8) runs for a call of a shape. */
 typedef enum logbq_path {
   LOGBQ_PATH_NONE = 0,     /* m or n is 0 (nothing written) or k is 0 (zeros written)        */

@@ -1965,6 +1965,29 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
 
 }  // namespace
 
+// Error workspace of logbq_gptq_noalloc: [rows][128] float32 for at most kGptqScratchRows rows
+// (8 MiB). It lives in the code object, so every device the library runs on holds its own copy
+// until the process ends; host code reaches it only through the address hipGetSymbolAddress
+// returns for the current device (the array's name is a host-side stand-in, not a device
+// address).
+constexpr int64_t kGptqScratchRows = 16384;
+static __device__ __align__(256) float scratch[kGptqScratchRows * kGptqBlock];
+
+// Device address of `scratch` on the current device, looked up once per device.
+float* gptq_scratch_ptr() {
+  static std::mutex mu;
+  static void* ptrs[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptrs[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    ptrs[dev] = p;
+  }
+  return static_cast<float*>(ptrs[dev]);
+}
+
 // One pass of the device fit: run the pass into its own region of the workspace (all regions
 // are cleared by one fill before pass 1), copy its bins to the host and wait for them (the next
 // pass's selection depends on them).
@@ -2174,6 +2197,22 @@ int32_t logbq_gptq(float* w_dev, int64_t n, int64_t k, const float* u_dev, const
   if (!aligned16(w_dev) || !aligned16(u_dev) || !aligned16(err_dev) || !aligned16(codes_dev))
     return LOGBQ_ERR_UNSUPPORTED;
   return gptq_launch(w_dev, (int)n, (int)k, u_dev, qz, err_dev, codes_dev, (hipStream_t)stream);
+}
+
+int32_t logbq_gptq_noalloc(float* w_dev, int64_t n, int64_t k, const float* u_dev,
+                           const logbq_params* p, const logbq_uniform* uniform,
+                           uint8_t* codes_dev, void* stream) {
+  GptqQuant qz;
+  const int32_t v = gptq_validate(n, k, p, uniform, &qz);
+  if (v != LOGBQ_OK) return v;
+  if (n > kGptqScratchRows) return LOGBQ_ERR_UNSUPPORTED;
+  if (n == 0 || k == 0) return LOGBQ_OK;
+  if (!w_dev || !u_dev || !codes_dev) return LOGBQ_ERR_INVALID_ARG;
+  if (!aligned16(w_dev) || !aligned16(u_dev) || !aligned16(codes_dev))
+    return LOGBQ_ERR_UNSUPPORTED;
+  float* err = gptq_scratch_ptr();
+  if (!err) return LOGBQ_ERR_HIP;
+  return gptq_launch(w_dev, (int)n, (int)k, u_dev, qz, err, codes_dev, (hipStream_t)stream);
 }
 
 int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const float* codebook,

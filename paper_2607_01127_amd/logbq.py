@@ -88,6 +88,8 @@ SIGNATURES = {
                                        c_void_p]),
     "logbq_gptq": (c_int32, [c_void_p, c_int64, c_int64, c_void_p, POINTER(Params),
                              POINTER(Uniform), c_void_p, c_void_p, c_void_p]),
+    "logbq_gptq_noalloc": (c_int32, [c_void_p, c_int64, c_int64, c_void_p, POINTER(Params),
+                                     POINTER(Uniform), c_void_p, c_void_p]),
     "logbq_fit_device": (c_int32, [c_void_p, c_int64, c_int32, c_double, c_void_p,
                                    POINTER(Params), c_void_p]),
     "logbq_fit_exact": (c_int32, [POINTER(c_float), c_int64, c_int32, c_double, POINTER(Params)]),
