@@ -513,15 +513,17 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x,
   u32x4 q[NBUF][CPL];
   int rq[NBUF];   // row held (or awaited) by buffer b; n_rows when none
 
-  // Start-up, ordered so that the memory system is busy from the first cycle: the staged
-  // activations are requested first (they return first), then the first row of codes; the
-  // pair table is written while both are in flight. With WK = 1 a lane holds at most 8 / M
-  // chunks, so M * K * 2 <= 8 * 64 * 32 * 2 bytes and x is always staged; only split rows may
-  // read x directly (after the pair table is written, which keeps their register use low).
+  // Start-up, ordered so that the memory system is busy from the first cycle: the activations
+  // are requested first (they return first), then the first row of codes; the pair table is
+  // written while both are in flight. x is staged through LDS when it fits (M * K * 2 <= 32 KiB),
+  // except for one batch row of one chunk per lane (K <= 2048), where each lane loads its 64
+  // bytes straight into registers (measured on MI355X: 0.1-0.3 us faster per launch at
+  // K = 2048, slower at K = 4096). Split rows that do not stage read x directly after the pair
+  // table is written, which keeps their register use low.
   constexpr int kXVec = kStageXBytes / 16 / 512;     // 16-byte x vectors per thread
   u32x4 xv[kXVec];
   const int nvec = (M * k_cols) >> 3;                // 16-byte vectors of x
-  const bool staged = !SPLITK || stage_x != 0;
+  const bool staged = stage_x != 0;
   if (staged) {
 #pragma unroll
     for (int v = 0; v < kXVec; ++v) {
@@ -529,6 +531,24 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x,
       xv[v] = *reinterpret_cast<const u32x4*>(x + 8 * (int64_t)(i < nvec ? i : 0));
     }
   }
+  uint32_t xr[M][CPL][CX];
+  // Unstaged activations of one-wavefront rows go out first, straight into registers.
+  auto direct_x = [&]() {
+#pragma unroll
+    for (int s = 0; s < CPL; ++s) {
+      const int c = s * 64 * wk + kw * 64 + lane;
+#pragma unroll
+      for (int m = 0; m < M; ++m)
+#pragma unroll
+        for (int qi = 0; qi < CX / 4; ++qi) {
+          u32x4 v = 0;
+          if (cval[s]) v = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k_cols + (int64_t)c * CW + 8 * qi);
+          xr[m][s][4 * qi] = v.x; xr[m][s][4 * qi + 1] = v.y;
+          xr[m][s][4 * qi + 2] = v.z; xr[m][s][4 * qi + 3] = v.w;
+        }
+    }
+  };
+  if (!SPLITK && !staged) direct_x();
   // The first row goes out at once; the other NBUF - 1 rows right after the pair table is
   // written when the ring is three deep, after the barrier below when it is two deep (measured
   // on MI355X: issuing every ring row at once makes the first row arrive later, so with one or
@@ -548,7 +568,6 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x,
     for (int b = 1; b < NBUF; ++b) load_row(rq[b], q[b]);
   }
 
-  uint32_t xr[M][CPL][CX];
   if (staged) {
 #pragma unroll
     for (int v = 0; v < kXVec; ++v) {
@@ -570,20 +589,8 @@ __global__ __launch_bounds__(512) void k_gemv(const uint16_t* __restrict__ x,
           xr[m][s][4 * qi + 2] = v.z; xr[m][s][4 * qi + 3] = v.w;
         }
     }
-  } else {
-#pragma unroll
-    for (int s = 0; s < CPL; ++s) {
-      const int c = s * 64 * wk + kw * 64 + lane;
-#pragma unroll
-      for (int m = 0; m < M; ++m)
-#pragma unroll
-        for (int qi = 0; qi < CX / 4; ++qi) {
-          u32x4 v = 0;
-          if (cval[s]) v = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k_cols + (int64_t)c * CW + 8 * qi);
-          xr[m][s][4 * qi] = v.x; xr[m][s][4 * qi + 1] = v.y;
-          xr[m][s][4 * qi + 2] = v.z; xr[m][s][4 * qi + 3] = v.w;
-        }
-    }
+  } else if (SPLITK) {
+    direct_x();
   }
 
   float acc[M];
@@ -1955,7 +1962,8 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
       make_lut<BITS>(j.codebook, &sg.lut, &sg.scale);
       begin += (int)share;
     }
-    const int stage_x = ((int64_t)M * K * 2 <= (int64_t)kStageXBytes) ? 1 : 0;
+    const int stage_x = ((int64_t)M * K * 2 <= (int64_t)kStageXBytes) &&
+                        !(M == 1 && cpl == 1 && wk == 1) ? 1 : 0;
     if (!dispatch_gemv<BITS>(M, cpl, begin, st, x, K, wk, stage_x, segs))
       return LOGBQ_ERR_UNSUPPORTED;
     if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
