@@ -18,7 +18,6 @@ And, on the host, the CPU oracle (dequantize + float64 matmul) on a row sample o
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--quick]
 """
 import argparse
-import concurrent.futures as cf
 import ctypes
 import json
 import math
@@ -447,25 +446,28 @@ def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):
     layers = wl["n_layers"]
     log(f"{name}: generating {layers} x {len(wl['layers'])} tensors")
     tensors = []
+    # Quantize at load: every tensor is fitted on the device (logbq_fit_device, exact sums of
+    # Eq. 5) and encoded there; only the parameters travel to the host.
+    ws = torch.empty(L.FIT_WORKSPACE_BYTES, dtype=torch.uint8, device=dev)
     t0 = time.perf_counter()
-    with cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 4)) as pool:
-        for li in range(layers):
-            hosts, devs = [], []
-            for lin in wl["layers"]:
-                wd = inputs.student_t_weights(lin.n, lin.k, wl["nu"], wl["scale"],
-                                              seed=[wl["cfg"], li, inputs.PROJ[lin.name], 0],
-                                              device=dev)
-                devs.append(wd)
-                hosts.append(wd.cpu().numpy())
-            params = list(pool.map(L.fit, hosts))
-            for lin, wd, p in zip(wl["layers"], devs, params):
-                codes, cb = L.encode(wd, p)
-                tensors.append((lin, codes, cb))
+    fit_s = 0.0
+    for li in range(layers):
+        for lin in wl["layers"]:
+            wd = inputs.student_t_weights(lin.n, lin.k, wl["nu"], wl["scale"],
+                                          seed=[wl["cfg"], li, inputs.PROJ[lin.name], 0],
+                                          device=dev)
             torch.cuda.synchronize()
-            del hosts, devs
-            if li % 8 == 7:
-                log(f"{name}: {li + 1} layers ready ({time.perf_counter() - t0:.1f} s)")
+            t1 = time.perf_counter()
+            p = L.fit_device(wd, workspace=ws, stream=stream)
+            codes, cb = L.encode(wd, p, stream=stream)
+            torch.cuda.synchronize()
+            fit_s += time.perf_counter() - t1
+            tensors.append((lin, codes, cb))
+            del wd
+        if li % 8 == 7:
+            log(f"{name}: {li + 1} layers ready ({time.perf_counter() - t0:.1f} s)")
     setup_s = time.perf_counter() - t0
+    del ws
     bytes_pass = sum(lin.n * lin.k // 2 for lin, _, _ in tensors)
     out = {}
     # Launch plan per layer, in dependency order: linears that read the same activations
@@ -543,7 +545,8 @@ def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):
                         "hbm_frac": bytes_pass / t / 1e6 / HBM_PEAK_GBS,
                         "launches": len(plan), "linears": len(tensors)}
         del g
-    return {"bytes_per_pass": bytes_pass, "setup_s": setup_s, **out}
+    return {"bytes_per_pass": bytes_pass, "setup_s": setup_s, "quantize_at_load_s": fit_s,
+            "quantize_at_load": "logbq_fit_device + logbq_encode per tensor", **out}
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "traffic_k_gemv_layer_8192x28672_m1.md")
