@@ -440,8 +440,10 @@ def bench_small(torch, L, inputs, dev, stream, name, steps, warmup):
             "path": L.linear_path(4, 1, lin.k, lin.n)}
 
 
-def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):
-    """A full decode weight pass in dependency order, captured in a HIP graph."""
+def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup, traffic_only=False):
+    """A full decode weight pass in dependency order, captured in a HIP graph. With
+    traffic_only, the pass at the first batch size is only replayed four times (for a
+    rocprofv3 --pmc FETCH_SIZE run) and nothing is timed."""
     wl = inputs.WORKLOADS[name]
     layers = wl["n_layers"]
     log(f"{name}: generating {layers} x {len(wl['layers'])} tensors")
@@ -506,6 +508,11 @@ def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup):
                                     [ys[id(c)] for _, c, _ in grp])
             for i in range(len(plan)):
                 calls.run(i)
+        if traffic_only:
+            for _ in range(4):
+                g.replay()
+            torch.cuda.synchronize()
+            return {"bytes_per_pass": bytes_pass, "launches": len(plan)}
         # check the replay against eager per-linear launches
         g.replay()
         torch.cuda.synchronize()
@@ -678,6 +685,12 @@ def main():
                          "layer at 8 bits), small, decode1b, decode8b, quality (LogbQuant "
                          "against the asymmetric linear baseline), gptq (calibration)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--decode-steps", type=int, default=0,
+                    help="timed (and warmup) passes of each decode row (default 200 for the "
+                         "1B-shaped pass, 100 for the 8B-shaped one)")
+    ap.add_argument("--decode-traffic", action="store_true",
+                    help="only build the 8B-shaped decode pass at M = 1 and replay it four times "
+                         "(for rocprofv3 --pmc FETCH_SIZE per pass) and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device-to-device copy (calibrates the HBM byte "
                          "counters of rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE) and exit")
@@ -702,6 +715,11 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
+    if args.decode_traffic:
+        r = bench_decode(torch, L, inputs, dev, stream, "decode_8b_32x7", [1], 1, 1,
+                         traffic_only=True)
+        print(json.dumps(r))
+        return
 
     want = set() if args.quick else set(args.rows.split(","))
     ms = [1, 8, 32, 128] if "layer" in want else [1]
@@ -733,12 +751,14 @@ def main():
                                  args.steps // 2, args.warmup // 2))
         torch.cuda.empty_cache()
     if "decode1b" in want:
+        n1 = args.decode_steps or 200
         rows["decode_1b_16x7"] = bench_decode(torch, L, inputs, dev, stream, "decode_1b_16x7",
-                                              [1], 200, 200)
+                                              [1], n1, n1)
         torch.cuda.empty_cache()
     if "decode8b" in want:
+        n8 = args.decode_steps or 100
         rows["decode_8b_32x7"] = bench_decode(torch, L, inputs, dev, stream, "decode_8b_32x7",
-                                              [1, 4], 100, 100)
+                                              [1, 4], n8, n8)
         torch.cuda.empty_cache()
 
     cpu = None

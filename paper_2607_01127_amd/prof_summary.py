@@ -4,6 +4,8 @@ kernel-stats: python -m paper_2607_01127_amd.prof_summary stats STATS_CSV CMD > 
 trace:        python -m paper_2607_01127_amd.prof_summary trace TRACE_CSV CMD > profiles/X.md
 counters:     python -m paper_2607_01127_amd.prof_summary counters PMC_CSV KERNEL_SUBSTR CMD > X.md
 mfma:         python -m paper_2607_01127_amd.prof_summary mfma PMC_CSV CUS XCDS CMD KERNEL... > X.md
+pass-traffic: python -m paper_2607_01127_amd.prof_summary pass_traffic FETCH_CSV COPY_FETCH_CSV \
+                  COPY_BYTES LAUNCHES_PER_PASS ALGO_BYTES CMD > profiles/X.md
 traffic:      python -m paper_2607_01127_amd.prof_summary traffic KERNEL_SUBSTR FETCH_CSV WRITE_CSV \
                   COPY_FETCH_CSV COPY_WRITE_CSV COPY_BYTES CMD > profiles/X.md
 
@@ -123,6 +125,30 @@ def _counter(path, substr, counter):
     return vals
 
 
+def pass_traffic(fetch, cfetch, copy_bytes, per_pass, algo, cmd):
+    """HBM bytes fetched per decode pass: FETCH_SIZE of the library's GEMV and split-K launches
+    in dispatch order, in consecutive groups of `per_pass` launches (one pass each), scaled by
+    the copy calibration; reports the median pass."""
+    rows = []
+    for r in csv.DictReader(open(fetch)):
+        name = r["Kernel_Name"]
+        if r["Counter_Name"] == "FETCH_SIZE" and ("k_gemv" in name or "k_mfma" in name):
+            rows.append((int(r.get("Dispatch_Id", 0) or 0), float(r["Counter_Value"])))
+    rows.sort()
+    cf = _counter(cfetch, "copy", "FETCH_SIZE") or _counter(cfetch, "Copy", "FETCH_SIZE")
+    kf = float(copy_bytes) / (statistics.median(cf) * 1024.0)
+    per_pass, algo = int(per_pass), float(algo)
+    passes = [sum(v for _, v in rows[i:i + per_pass]) * 1024.0 * kf
+              for i in range(0, len(rows) - per_pass + 1, per_pass)]
+    print("# HBM bytes per decode pass (rocprofv3 --pmc FETCH_SIZE)\n")
+    print(f"Command: `{cmd}`\n")
+    print(f"- launches per pass: {per_pass}; passes counted: {len(passes)}")
+    print(f"- copy calibration factor {kf:.4f}")
+    print(f"- fetched bytes per pass (median): {statistics.median(passes):.0f}")
+    print(f"- packed code bytes per pass (algorithmic): {algo:.0f}")
+    print(f"- ratio fetched / algorithmic: {statistics.median(passes) / algo:.4f}")
+
+
 def traffic(substr, fetch, write, cfetch, cwrite, copy_bytes, cmd):
     f = _counter(fetch, substr, "FETCH_SIZE")
     w = _counter(write, substr, "WRITE_SIZE")
@@ -153,5 +179,7 @@ if __name__ == "__main__":
         trace(sys.argv[2], sys.argv[3])
     elif sys.argv[1] == "counters":
         counters(sys.argv[2], sys.argv[3], sys.argv[4])
+    elif sys.argv[1] == "pass_traffic":
+        pass_traffic(*sys.argv[2:8])
     elif sys.argv[1] == "mfma":
         mfma(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6:])
