@@ -559,9 +559,10 @@ def bench_decode(torch, L, inputs, dev, stream, name, batches, steps, warmup, tr
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "traffic_k_gemv_layer_8192x28672_m1.md")
 
 
-def profiled_traffic():
+def profiled_traffic(kernel):
     """HBM bytes per launch of the M = 1 layer GEMV from the committed rocprofv3 --pmc summary,
-    or None when there is none or the kernel source changed since it was taken."""
+    or None when there is none, it covers another kernel instance, or the GEMV's device source
+    changed since it was taken."""
     try:
         from paper_2607_01127_amd.prof_summary import source_hash
         text = open(TRAFFIC_PROFILE).read()
@@ -572,7 +573,9 @@ def profiled_traffic():
         if line.startswith("- ") and ":" in line:
             key, val = line[2:].split(":", 1)
             fields[key.strip()] = val.strip()
-    if fields.get("kernel_source_sha256_16") != source_hash():
+    if fields.get("gemv_source_sha256_16") != source_hash():
+        return None
+    if f"kernel: `{kernel}`" not in text:
         return None
     try:
         return float(fields["traffic_bytes"])
@@ -779,7 +782,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(algo / t_ms / 1e6, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(algo / t_ms / 1e6 / HBM_PEAK_GBS, 4),
-                     "traffic": profiled_traffic(),
+                     "traffic": profiled_traffic(main_row["kernel"]),
                      "kernel": main_row["kernel"], "algo_bytes_per_launch": algo,
                      "avg_launch_us": t_ms * 1e3,
                      "read_ceiling_GB_s": round(ceiling["GB_s"], 1),

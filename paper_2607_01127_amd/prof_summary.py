@@ -11,8 +11,8 @@ traffic:      python -m paper_2607_01127_amd.prof_summary traffic KERNEL_SUBSTR 
 
 The traffic summary scales the per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the kernel by
 copy_bytes / (what the same counter reads for a plain device copy of copy_bytes bytes), and
-records the sha256 of the kernel source so that bench.py reports the figure only while the
-kernel is unchanged.
+records the sha256 of the GEMV's device source so that bench.py reports the figure only while
+that source is unchanged (and only for the kernel instance the profile names).
 """
 import csv
 import hashlib
@@ -24,9 +24,16 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCE = os.path.join(HERE, "csrc", "logbq_kernels.hip")
 
 
+GEMV_BEGIN = "// ------------------------------------------------------------------ shared device helpers"
+GEMV_END = "// ------------------------------------------------------------------ GPTQ calibration"
+
+
 def source_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as fh:
-        return hashlib.sha256(fh.read()).hexdigest()[:16]
+    """sha256 (16 hex digits) of the GEMV's device source: the shared device helpers and the
+    GEMV kernel, the part of the kernel file that decides the traffic of a GEMV launch."""
+    text = open(KERNEL_SOURCE, encoding="utf-8").read()
+    i, j = text.index(GEMV_BEGIN), text.index(GEMV_END)
+    return hashlib.sha256(text[i:j].encode("utf-8")).hexdigest()[:16]
 
 
 def _short(name: str) -> str:
@@ -167,7 +174,7 @@ def traffic(substr, fetch, write, cfetch, cwrite, copy_bytes, cmd):
     print(f"- fetch_bytes: {fb:.0f}")
     print(f"- write_bytes: {wb:.0f}")
     print(f"- traffic_bytes: {fb + wb:.0f}")
-    print(f"- kernel_source_sha256_16: {source_hash()}")
+    print(f"- gemv_source_sha256_16: {source_hash()}")
 
 
 if __name__ == "__main__":
