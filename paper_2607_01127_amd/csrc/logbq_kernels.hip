@@ -12,9 +12,9 @@
 //              lane's B operand of v_mfma_f32_16x16x32_f16, dequantized by pair-table lookups
 //              or by v_perm_b32 byte tables in registers; activations are staged through LDS
 //              as the A operand; float32 accumulation in the MFMA.
-//   k_mfma_sk  the same product for 2 <= m <= 16 split over K: the 8 wavefronts of a workgroup
-//              share a block of 16 rows (one K slice each, activations held in registers) and
-//              sum their partial tiles through LDS.
+//   k_mfma_sk  the same product for 2 <= m <= 16 split over K: the 8 or 16 wavefronts of a
+//              workgroup share a block of 16 rows (one K slice each, activations held in
+//              registers) and sum their partial tiles through LDS.
 //   k_mfma_kq  the same product for m > 96: each wavefront takes 64 weight rows and one K
 //              quarter of every step for all 128 batch rows of the workgroup; the quarters'
 //              tiles are summed through LDS at the end.
@@ -1235,22 +1235,38 @@ __global__ __launch_bounds__(512) void k_mfma_kq(const uint8_t* __restrict__ cod
 
 // ------------------------------------------------------------------ split-K MFMA, m <= 16
 //
-// For one batch tile (m <= 16) and K = 256 ND (ND = 4, 8, 16, 32, i.e. K = 1024 .. 8192): a
-// workgroup of 8 wavefronts takes one block of 16 weight rows at a time (blocks dealt
+// For one batch tile (m <= 16) and K = 32 W ND (W wavefronts of ND code dwords per row each): a
+// workgroup of W wavefronts takes one block of 16 weight rows at a time (blocks dealt
 // round-robin over the grid) and its wavefront w takes the K slice [w S, (w + 1) S), S = 32 ND.
 // The workgroup therefore streams its 16 rows as one contiguous band, instead of every
 // workgroup walking K in step over all rows (measured on MI355X: this code stream reads the
 // 8192 x 28672 codes in 20.2 us, the stepped pattern of k_mfma2 in 25 us).
 //
-// A lane's activations for its slice stay in registers for the whole kernel: lane (j, g) holds
-// batch row j at k = w S + 8 ND g + [0, 8 ND) (zeros for rows >= m). The codes of a block are
-// loaded as ND / 4 instructions of 64 / ND rows x 16 ND contiguous bytes and transposed through
-// the wavefront's LDS buffer so that lane (j, g) then holds row j, bytes [4 ND g, 4 ND (g + 1))
-// of the slice: dword d (k = w S + 8 ND g + 8 d + 0..7) is the B operand of MFMA d, matching the
-// A operand above. The 16 x 16 partial tiles of the 8 wavefronts are summed in LDS (two sets, one
-// barrier per block); each of the first 256 threads owns one (batch row, weight row) element and
-// keeps its results for up to 8 blocks before storing them. The next block's codes are in
-// flight while a block is computed.
+// A lane's activations for its slice stay in registers for the whole kernel. With G batch
+// groups (G = 1 for m <= 16, G = 2 for m <= 8) the 16 rows of the MFMA's A operand hold G
+// copies of the batch rows 0 .. 16 / G - 1, each for a different code dword: lane (j, g)
+// holds batch row j % (16 / G) for the dwords d = G r + j / (16 / G), r = 0 .. ND / G - 1,
+// at k = w S + 8 ND g + 8 d + 0..7 (zeros for batch rows >= m). MFMA d then leaves correct
+// products in the D rows of dword group d % G only and accumulates into that group's tile; the
+// other rows are never read. Each lane keeps ND / G activation registers instead of ND, which
+// is what lets 16 wavefronts (4 per SIMD) hold K = 8192 at m <= 8.
+//
+// The codes of a block are loaded as ND / 4 instructions of 64 / ND rows x 16 ND contiguous
+// bytes and transposed through the wavefront's LDS buffer so that lane (j, g) then holds row j,
+// bytes [4 ND g, 4 ND (g + 1)) of the slice: dword d (k = w S + 8 ND g + 8 d + 0..7) is the B
+// operand of MFMA d, matching the A operand above. The 16 x 16 tiles of the W wavefronts and G
+// groups are summed in LDS in a fixed order (two sets, one barrier per block); each of the
+// first 16 x 16 / G threads owns one (batch row, weight row) element and keeps its results for
+// up to 4 blocks before storing them. The next block's codes are in flight while a block is
+// computed.
+//
+// Configurations (measured on MI355X against the 8-wavefront, G = 1 kernel that preceded
+// them, same box): K = 8192 takes W = 16, ND = 16 (8192 -> 28672 at m = 4 / 8 / 12:
+// 28.1 / 29.5 / 31.3 -> 27.1 / 27.8 / 29.1 us, on another box 27.9 / 29.2 -> 24.6 / 26.3 us);
+// K = 4096 takes W = 16, ND = 8 (4096 -> 14336 at m = 4 / 8: 10.1 / 10.5 -> 9.3 / 9.9 us);
+// K = 1024 and 2048 keep W = 8. A non-symmetric codebook (the LDS pair table, 64 KiB) keeps
+// W = 8 and G = 1.
+//
 // Up to kMaxSegs linears that share x, in one launch: their 16-row blocks are numbered one
 // after another (segment s holds blocks [blk_begin, blk_begin + ceil(n_rows / 16))), and every
 // block is computed exactly as in a launch of its linear alone. Grouped launches need
@@ -1268,20 +1284,24 @@ struct SkSegs {
   SkSeg s[kMaxSegs];
 };
 
-template <int ND, bool PAIRS>
-__global__ __launch_bounds__(512) void k_mfma_sk(const uint16_t* __restrict__ x,
+template <int ND, int WAVES, int G, bool PAIRS>
+__global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restrict__ x,
                                                  const uint8_t* codes0, int n_rows0, int nseg,
                                                  int nblocks, int k_cols, int m_rows,
                                                  SkSegs segs, Lut16 lut) {
   static_assert(ND == 4 || ND == 8 || ND == 16 || ND == 32, "64 / ND rows per load");
+  static_assert(G == 1 || G == 2 || G == 4, "batch groups");
   constexpr int BR = 16 * ND;            // code bytes per row per wavefront and block
   constexpr int RPI = 64 / ND;           // rows per load instruction
   constexpr int NI = ND / 4;             // load instructions per block
   constexpr int TP = BR + 16;            // transpose pitch (bytes)
-  constexpr int NRES = 8;                // blocks whose results a thread holds before storing
+  constexpr int NRES = 4;                // blocks whose results a thread holds before storing
+  constexpr int MB = 16 / G;             // batch rows per group
+  constexpr int XR = ND / G;             // activation register sets per lane
+  constexpr int NT = 64 * WAVES;
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[PAIRS ? kLutWords : 4];
-  __shared__ __attribute__((aligned(16))) uint8_t s_ct[8][16 * TP];
-  __shared__ __attribute__((aligned(16))) float4v s_red[2][8][64];
+  __shared__ __attribute__((aligned(16))) uint8_t s_ct[WAVES][16 * TP];
+  __shared__ __attribute__((aligned(16))) float4v s_red[2][WAVES][64];
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -1289,8 +1309,6 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint16_t* __restrict__ x,
   const uint32_t laneoff = (uint32_t)lane << 2;
   const int64_t row_bytes = (int64_t)k_cols / 2;
   const int slice_k0 = w * 32 * ND;
-  // Segment of block b (a uniform value); one-segment launches take the first segment's codes
-  // pointer and row count from their leading (preloaded) arguments.
   auto seg_of = [&](int b) {
     int si = 0;
 #pragma unroll
@@ -1298,19 +1316,20 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint16_t* __restrict__ x,
       if (i < nseg && b >= segs.s[i].blk_begin) si = i;
     return si;
   };
-
-  // Activations first (they return first): batch row j of this lane's slice, in the order the
+  // Activations first (they return first): lane row j is batch row j % MB of dword group
+  // j / MB; register r holds dword d = G r + j / MB of this lane's slice, in the order the
   // dequantization produces the weights.
-  u32x4 xa[ND];
+  u32x4 xa[XR];
   {
-    const bool live = j < m_rows;
-    const int64_t base = (int64_t)(live ? j : 0) * k_cols + slice_k0 + 8 * ND * g;
+    const int mrow = j % MB, sg = j / MB;
+    const bool live = mrow < m_rows;
+    const int64_t base = (int64_t)(live ? mrow : 0) * k_cols + slice_k0 + 8 * ND * g;
 #pragma unroll
-    for (int d = 0; d < ND; ++d) xa[d] = *reinterpret_cast<const u32x4*>(x + base + 8 * d);
+    for (int r = 0; r < XR; ++r) xa[r] = *reinterpret_cast<const u32x4*>(x + base + 8 * (G * r + sg));
 #pragma unroll
-    for (int d = 0; d < ND; ++d) {
-      u32x4 v = live ? xa[d] : u32x4{0u, 0u, 0u, 0u};
-      xa[d] = PAIRS ? v : permute_x8(v);
+    for (int r = 0; r < XR; ++r) {
+      u32x4 v = live ? xa[r] : u32x4{0u, 0u, 0u, 0u};
+      xa[r] = PAIRS ? v : permute_x8(v);
     }
   }
   // Codes of block b: a descriptor over its rows (size 0 past the last block, short for a
@@ -1339,14 +1358,14 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint16_t* __restrict__ x,
   };
   u32x4 q[2][NI];
   load_block(blockIdx.x, q[0]);
-  if (PAIRS) fill_lut<4, 512>(s_lut, lut);
+  if (PAIRS) fill_lut<4, NT>(s_lut, lut);
   __syncthreads();
 
   float res[NRES];
   int held = 0, blast = 0, par = 0;
-  const int ri = t >> 4, rj = t & 15;      // element of threads t < 256: batch ri, row rj
+  const int ri = t >> 4, rj = t & 15;      // element of threads t < 16 MB: batch ri, row rj
   auto flush = [&]() {
-    if (t < 256 && ri < m_rows) {
+    if (t < 16 * MB && ri < m_rows) {
 #pragma unroll
       for (int h = 0; h < NRES; ++h) {
         if (h < held) {
@@ -1361,6 +1380,7 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint16_t* __restrict__ x,
     held = 0;
   };
   uint8_t* s_cw = s_ct[w];
+  const int my_group = (lane >> 4) * G / 4;   // dword group of this lane's D rows
   auto block = [&](int b, const u32x4 (&qc)[NI]) {
     const int bsi = seg_of(b);
     const LutBytes tb = segs.s[bsi].tb;
@@ -1375,7 +1395,9 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint16_t* __restrict__ x,
     for (int c = 0; c < NI; ++c)
       o[c] = *reinterpret_cast<const u32x4*>(s_cw + j * TP + 4 * ND * g + 16 * c);
     __builtin_amdgcn_wave_barrier();
-    float4v acc = {0.f, 0.f, 0.f, 0.f};
+    float4v acc[G];
+#pragma unroll
+    for (int s = 0; s < G; ++s) acc[s] = float4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int d = 0; d < ND; ++d) {
       const u32x4 od = o[d >> 2];
@@ -1387,18 +1409,28 @@ __global__ __launch_bounds__(512) void k_mfma_sk(const uint16_t* __restrict__ x,
       } else {
         dequant_dword(dw, tb, bw);
       }
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-          __builtin_bit_cast(half8v, xa[d]),
-          __builtin_bit_cast(half8v, u32x4{bw[0], bw[1], bw[2], bw[3]}), acc, 0, 0, 0);
+      acc[d % G] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+          __builtin_bit_cast(half8v, xa[d / G]),
+          __builtin_bit_cast(half8v, u32x4{bw[0], bw[1], bw[2], bw[3]}), acc[d % G], 0, 0, 0);
     }
-    // Lane l holds D[4 (l / 16) + r][l % 16] (batch row, weight row) in component r.
-    s_red[par][w][lane] = acc;
+    // Lane l holds D rows 4 (l / 16) .. + 3, which belong to dword group (l / 16) G / 4.
+    float4v mine = acc[0];
+#pragma unroll
+    for (int s = 1; s < G; ++s)
+      if (my_group == s) mine = acc[s];
+    // Lane l holds D[4 (l / 16) + r][l % 16] in component r: D row i is batch row i % MB of
+    // dword group i / MB, column l % 16 the weight row.
+    s_red[par][w][lane] = mine;
     __syncthreads();
-    if (t < 256) {
-      const int l = 16 * (ri >> 2) + rj, r = ri & 3;
+    if (t < 16 * MB) {
       float sum = 0.0f;
 #pragma unroll
-      for (int w2 = 0; w2 < 8; ++w2) sum += s_red[par][w2][l][r];
+      for (int s = 0; s < G; ++s) {
+        const int i = s * MB + ri;
+        const int l = 16 * (i >> 2) + rj, r = i & 3;
+#pragma unroll
+        for (int w2 = 0; w2 < WAVES; ++w2) sum += s_red[par][w2][l][r];
+      }
 #pragma unroll
       for (int h = 0; h < NRES; ++h)
         if (h == held) res[h] = sum * scale;
@@ -1797,6 +1829,13 @@ bool sk_shape(int M, int K) {
   return M >= 2 && M <= 16 && (K == 1024 || K == 2048 || K == 4096 || K == 8192);
 }
 
+// Split-K configuration: wavefronts per workgroup, code dwords per lane and row, batch groups.
+struct SkConfig { int nd, waves, groups; };
+SkConfig sk_config(int M, int K, bool pairs) {
+  const int waves = (!pairs && K >= 4096) ? 16 : 8;
+  return {K / (32 * waves), waves, (!pairs && M <= 8) ? 2 : 1};
+}
+
 // Split-K launches for the linears jobs[idx[0..count)] of one call: one grouped launch when
 // every codebook is sign-symmetric (register dequantization), otherwise one launch per linear.
 int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const int* idx,
@@ -1816,23 +1855,22 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     all_symmetric = make_lut_bytes(j.codebook, &sg.tb, &sg.scale) && all_symmetric;
     total += (int)((j.n + 15) / 16);
   }
-  auto launch = [&](int nseg, const SkSegs& sgs, int nblocks, bool pairs, const Lut16& l) {
+  auto launch = [&](int nseg, const SkSegs& sgs, int nblocks, bool pairs,
+                    const Lut16& l) -> int32_t {
     const int grid = nblocks < cus ? nblocks : cus;
-#define LOGBQ_SK(ND)                                                                             \
-  if (pairs)                                                                                     \
-    hipLaunchKernelGGL((k_mfma_sk<ND, true>), dim3((unsigned)grid), dim3(512), 0, st, x,          \
+    const SkConfig c = sk_config(M, K, pairs);
+#define LOGBQ_SK(ND, W, GG, PR)                                                                  \
+  if (c.nd == ND && c.waves == W && c.groups == GG && pairs == PR) {                             \
+    hipLaunchKernelGGL((k_mfma_sk<ND, W, GG, PR>), dim3((unsigned)grid), dim3(64 * W), 0, st, x,  \
                        sgs.s[0].codes, sgs.s[0].n_rows, nseg, nblocks, K, M, sgs, l);            \
-  else                                                                                           \
-    hipLaunchKernelGGL((k_mfma_sk<ND, false>), dim3((unsigned)grid), dim3(512), 0, st, x,         \
-                       sgs.s[0].codes, sgs.s[0].n_rows, nseg, nblocks, K, M, sgs, l);
-    switch (K) {
-      case 1024: LOGBQ_SK(4) break;
-      case 2048: LOGBQ_SK(8) break;
-      case 4096: LOGBQ_SK(16) break;
-      default: LOGBQ_SK(32) break;
-    }
+    return launch_status();                                                                      \
+  }
+    LOGBQ_SK(4, 8, 1, true) LOGBQ_SK(8, 8, 1, true) LOGBQ_SK(16, 8, 1, true) LOGBQ_SK(32, 8, 1, true)
+    LOGBQ_SK(4, 8, 1, false) LOGBQ_SK(4, 8, 2, false) LOGBQ_SK(8, 8, 1, false) LOGBQ_SK(8, 8, 2, false)
+    LOGBQ_SK(8, 16, 1, false) LOGBQ_SK(8, 16, 2, false)
+    LOGBQ_SK(16, 16, 1, false) LOGBQ_SK(16, 16, 2, false)
 #undef LOGBQ_SK
-    return launch_status();
+    return LOGBQ_ERR_UNSUPPORTED;
   };
   if (all_symmetric) return launch(count, segs, total, false, lut);
   for (int a = 0; a < count; ++a) {
@@ -1864,15 +1902,17 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
 // on narrow layers, which have too few 128-row workgroups).
 //
 // Where the split-K MFMA kernel applies (4-bit codes, 2 <= m <= 16, K = 1, 2, 4 or 8 Ki), it
-// takes m >= 5, m = 4 at N >= 8192 and m = 3 at N >= 16384, except m > 12 at N >= 16384
-// (measured: it beats the GEMV there and the stepped MFMA kernel everywhere except the widest
-// layers at m = 13..16, e.g. 2048 x 8192 at m = 16: 13.0 us vs 28.7 us, 8192 -> 28672 at m = 8:
-// 29.6 us vs 31.8 us).
+// takes m >= 5, m = 4 unless N <= 1024 at K = 8192, and m = 3 at N >= 4096. Measured with
+// forced paths over N = 1024 .. 28672 and K = 2048 .. 8192: at m = 4 it beats the GEMV except
+// at N = 1024, K = 8192 (7.0 vs 6.9 us), e.g. 4096 x 4096: 4.9 vs 5.7 us, 8192 -> 28672:
+// 26.4 vs 37.7 us; at m = 3 from N = 4096 (one exception, 4096 -> 6144: 6.2 vs 5.9 us); at
+// m = 2 the GEMV wins (8192 -> 28672: 21.9 vs 25.4 us). It also beats the stepped MFMA kernel up
+// to m = 16 on the widest layer (8192 -> 28672 at m = 16: 30.6 vs 31.6 us).
 template <int BITS>
 int choose_path(int M, int K, int64_t N) {
   int wk = 0, cpl = 0;
   if (sk_shape(M, K) && BITS == 4 &&
-      (M >= 5 || (M == 4 && N >= 8192) || (M == 3 && N >= 16384)) && !(M > 12 && N >= 16384))
+      (M >= 5 || (M == 4 && (N > 1024 || K <= 4096)) || (M == 3 && N >= 4096)))
     return LOGBQ_PATH_SPLITK;
   if (M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl) && !(M >= 3 && (int64_t)M * N > 65536))
     return LOGBQ_PATH_GEMV;
@@ -2356,8 +2396,9 @@ int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const
     const int path = bits == 4 ? choose_path<4>(M, K, n) : choose_path<8>(M, K, n);
     int wk = 0, cpl = 0;
     if (path == LOGBQ_PATH_SPLITK) {
-      const int nd = K / 256;
-      std::snprintf(buf, sizeof(buf), "k_mfma_sk<%d, %s>", nd, symmetric ? "false" : "true");
+      const SkConfig c = sk_config(M, K, !symmetric);
+      std::snprintf(buf, sizeof(buf), "k_mfma_sk<%d, %d, %d, %s>", c.nd, c.waves, c.groups,
+                    symmetric ? "false" : "true");
     } else if (path == LOGBQ_PATH_GEMV) {
       const bool ok = bits == 4 ? gemv_config_rows<4>(M, K, n, &wk, &cpl)
                                 : gemv_config_rows<8>(M, K, n, &wk, &cpl);

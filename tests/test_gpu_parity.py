@@ -277,24 +277,26 @@ def test_linear_arbitrary_codebook():
     """Any 16 finite floats work as a codebook (the table-lookup kernels); a fitted codebook is
     sign-symmetric and takes the register-dequant MFMA path, any other takes the pair table."""
     rng = np.random.default_rng(12)
-    n, k = 300, 1024
-    codes_np = rng.integers(0, 16, size=(n, k), dtype=np.uint8)
-    codes = torch.from_numpy(O.pack(codes_np)).to(DEV)
-    for trial in range(2):
-        cb = rng.standard_normal(16).astype(np.float32) * np.float32(10.0 ** (3 * trial - 2))
-        wh = O.dequantize(codes_np, cb)
-        for m in (1, 5, 16, 33, 128):
-            _say(f"arbitrary codebook trial {trial} m={m}")
-            x = inputs.activations(m, k, seed=[8, 9, trial, m])
-            y = L.linear(torch.from_numpy(x).to(DEV), codes, cb)
-            torch.cuda.synchronize()
-            assert rel_err(y.cpu().numpy(), x, wh) <= TOL
+    n = 300
+    for k in (1024, 2048, 4096, 8192):
+        codes_np = rng.integers(0, 16, size=(n, k), dtype=np.uint8)
+        codes = torch.from_numpy(O.pack(codes_np)).to(DEV)
+        for trial in range(2):
+            cb = rng.standard_normal(16).astype(np.float32) * np.float32(10.0 ** (3 * trial - 2))
+            wh = O.dequantize(codes_np, cb)
+            for m in ((1, 5, 16, 33, 128) if k == 1024 else (5, 16)):
+                _say(f"arbitrary codebook k={k} trial {trial} m={m}")
+                x = inputs.activations(m, k, seed=[8, 9, trial, m + k])
+                y = L.linear(torch.from_numpy(x).to(DEV), codes, cb)
+                torch.cuda.synchronize()
+                assert rel_err(y.cpu().numpy(), x, wh) <= TOL
 
 
 def test_linear_split_k_many_blocks():
-    """The split-K MFMA path (2 <= m <= 16, K = 1, 2, 4 or 8 Ki) with more than 8 blocks of 16
-    rows per workgroup (results are stored 8 blocks at a time) and a ragged last block, for a
-    fitted (register dequantization) and an arbitrary codebook (pair table)."""
+    """The split-K MFMA path (2 <= m <= 16, K = 1, 2, 4 or 8 Ki) with more than 4 blocks of 16
+    rows per workgroup (results are stored 4 blocks at a time) and a ragged last block, for a
+    fitted (register dequantization, two batch groups up to m = 8) and an arbitrary codebook
+    (pair table)."""
     n, k = 40003, 1024
     w, p, r = prepare(n, k, [8, 11, 1, 0])
     codes, cb = gpu_encode(w, p)
