@@ -182,14 +182,17 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  *               so the call is capturable in a HIP graph. Entries are rounded to float16 after
  *               a common power-of-two scaling, exact in the result up to float16 rounding.
  *   y_dev     : device, [m][n] float32, written.
- * Accumulation is float32. Four kernels, chosen from (m, k, n) alone: for 2 <= m <= 16 and
- * k in {1024, 2048, 4096, 8192}, a split-K dequantize-into-MFMA kernel takes m >= 5, m = 4 at
- * n >= 8192 and m = 3 at n >= 16384 (except m > 12 at n >= 16384); otherwise the
+ * Accumulation is float32. Four kernels, chosen from (m, k, n) alone: for 2 <= m <= 32 and
+ * k in {1024, 2048, 4096, 8192}, a split-K dequantize-into-MFMA kernel takes 5 <= m <= 16,
+ * m = 4 unless n <= 1024 at k = 8192, m = 3 at n >= 4096, and 17 <= m <= 32 unless m > 20 at
+ * k = 8192 and n > 16384 (above m = 16 only for sign-symmetric codebooks; at k = 8192 it first
+ * zeroes y and two workgroups add their halves of K into each output); otherwise the
  * wavefront-reduced GEMV runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and
  * shapes whose activations do not fit the GEMV's registers) runs the stepped
  * dequantize-into-MFMA skinny GEMM, except m > 96 at n >= 4096, which runs a K-quartered
- * MFMA GEMM for sign-symmetric codebooks. logbq_linear_path reports the choice.
- * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment), HIP.
+ * MFMA GEMM for sign-symmetric codebooks. logbq_linear_path reports the choice. Results are
+ * deterministic for every path. k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED
+ * (k % 32, alignment), HIP.
  */
 int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
                      int64_t n, const float* codebook, float* y_dev, void* stream);
@@ -310,7 +313,9 @@ typedef enum logbq_path {
   LOGBQ_PATH_NONE = 0,     /* m or n is 0 (nothing written) or k is 0 (zeros written)        */
   LOGBQ_PATH_GEMV = 1,     /* wavefront-reduced GEMV with the LDS pair table                  */
   LOGBQ_PATH_MFMA = 2,     /* stepped dequantize-into-MFMA skinny GEMM                        */
-  LOGBQ_PATH_SPLITK = 3,   /* split-K dequantize-into-MFMA kernel (4-bit, 2 <= m <= 16)        */
+  LOGBQ_PATH_SPLITK = 3,   /* split-K dequantize-into-MFMA kernel (4-bit, 2 <= m <= 32); above
+                              m = 16 a codebook that is not sign-symmetric runs the stepped
+                              kernel instead                                                  */
   LOGBQ_PATH_MFMA_KQ = 4   /* K-quartered dequantize-into-MFMA GEMM (4-bit, m > 96, n >= 4096);
                               a codebook that is not sign-symmetric (never a fitted one) runs the
                               stepped kernel instead                                          */
@@ -330,9 +335,10 @@ int32_t logbq_linear_path(int32_t bits, int64_t m, int64_t k, int64_t n, int32_t
 
 /*
  * logbq_linear_kernel -- name of the kernel instance (with its template arguments, as a
- * profiler lists it) that the first launch of a logbq_linear / logbq_linear8 call of shape
- * (m, k, n) runs, e.g. "k_gemv<4, 1, 4, false, 2>" (Sec. 3.3 product; the choice is this
- * library's). Host only: needs no device and touches none.
+ * profiler lists it) that reads the codes in a logbq_linear / logbq_linear8 call of shape
+ * (m, k, n), e.g. "k_gemv<4, 1, 4, false, 2>" (Sec. 3.3 product; the choice is this
+ * library's); a split-K call over workgroup pairs launches k_fill_zero before it. Host only:
+ * needs no device and touches none.
  *   bits, m, k, n : as logbq_linear_path; n fits in int32.
  *   codebook      : host, 2^bits floats, or NULL for a fitted (sign-symmetric) codebook; the
  *                   4-bit MFMA kernels dequantize in registers only for sign-symmetric ones.

@@ -12,9 +12,10 @@
 //              lane's B operand of v_mfma_f32_16x16x32_f16, dequantized by pair-table lookups
 //              or by v_perm_b32 byte tables in registers; activations are staged through LDS
 //              as the A operand; float32 accumulation in the MFMA.
-//   k_mfma_sk  the same product for 2 <= m <= 16 split over K: the 8 or 16 wavefronts of a
+//   k_mfma_sk  the same product for 2 <= m <= 32 split over K: the 8 or 16 wavefronts of a
 //              workgroup share a block of 16 rows (one K slice each, activations held in
-//              registers) and sum their partial tiles through LDS.
+//              registers) and sum their partial tiles through LDS; at K = 8192 and m > 16 two
+//              workgroups share a block (one K half each) and add into a zeroed y.
 //   k_mfma_kq  the same product for m > 96: each wavefront takes 64 weight rows and one K
 //              quarter of every step for all 128 batch rows of the workgroup; the quarters'
 //              tiles are summed through LDS at the end.
@@ -1235,9 +1236,10 @@ __global__ __launch_bounds__(512) void k_mfma_kq(const uint8_t* __restrict__ cod
 
 // ------------------------------------------------------------------ split-K MFMA, m <= 16
 //
-// For one batch tile (m <= 16) and K = 32 W ND (W wavefronts of ND code dwords per row each): a
-// workgroup of W wavefronts takes one block of 16 weight rows at a time (blocks dealt
-// round-robin over the grid) and its wavefront w takes the K slice [w S, (w + 1) S), S = 32 ND.
+// For T batch tiles of 16 rows (T = 1 for m <= 16, T = 2 for m <= 32) and K = 32 W ND KS (W
+// wavefronts of ND code dwords per row each, KS workgroups per block): a workgroup of W
+// wavefronts takes one block of 16 weight rows at a time (blocks dealt round-robin over the
+// grid) and its wavefront w takes the K slice [w S, (w + 1) S), S = 32 ND, of its K part.
 // The workgroup therefore streams its 16 rows as one contiguous band, instead of every
 // workgroup walking K in step over all rows (measured on MI355X: this code stream reads the
 // 8192 x 28672 codes in 20.2 us, the stepped pattern of k_mfma2 in 25 us).
@@ -1265,7 +1267,12 @@ __global__ __launch_bounds__(512) void k_mfma_kq(const uint8_t* __restrict__ cod
 // 28.1 / 29.5 / 31.3 -> 27.1 / 27.8 / 29.1 us, on another box 27.9 / 29.2 -> 24.6 / 26.3 us);
 // K = 4096 takes W = 16, ND = 8 (4096 -> 14336 at m = 4 / 8: 10.1 / 10.5 -> 9.3 / 9.9 us);
 // K = 1024 and 2048 keep W = 8. A non-symmetric codebook (the LDS pair table, 64 KiB) keeps
-// W = 8 and G = 1.
+// W = 8 and G = 1. Two batch tiles (17 <= m <= 32, register tables only) hold 2 ND activation
+// registers per lane: W = 16 with ND = 4 and 8 at K = 2048 and 4096, W = 8 at K = 1024, and at
+// K = 8192 two K parts (KS = 2) of ND = 8: workgroups 2 i and 2 i + 1 take the two K halves of
+// the same blocks and add their results into y with float atomics after y is zeroed (two terms
+// onto zero: the same sum in either order, so results stay deterministic). The alternative
+// of two launches (the second adding into y) measured 7-8 us slower at 8192 -> 28672.
 //
 // Up to kMaxSegs linears that share x, in one launch: their 16-row blocks are numbered one
 // after another (segment s holds blocks [blk_begin, blk_begin + ceil(n_rows / 16))), and every
@@ -1284,31 +1291,40 @@ struct SkSegs {
   SkSeg s[kMaxSegs];
 };
 
-template <int ND, int WAVES, int G, bool PAIRS>
+template <int ND, int WAVES, int G, int T, int KS, bool PAIRS>
 __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restrict__ x,
                                                  const uint8_t* codes0, int n_rows0, int nseg,
                                                  int nblocks, int k_cols, int m_rows,
                                                  SkSegs segs, Lut16 lut) {
   static_assert(ND == 4 || ND == 8 || ND == 16 || ND == 32, "64 / ND rows per load");
   static_assert(G == 1 || G == 2 || G == 4, "batch groups");
+  static_assert((T == 1 || (T == 2 && G == 1 && !PAIRS)) && (KS == 1 || (KS == 2 && T == 2)),
+                "two batch tiles (and the K split) only with one group and register tables");
   constexpr int BR = 16 * ND;            // code bytes per row per wavefront and block
   constexpr int RPI = 64 / ND;           // rows per load instruction
   constexpr int NI = ND / 4;             // load instructions per block
   constexpr int TP = BR + 16;            // transpose pitch (bytes)
   constexpr int NRES = 4;                // blocks whose results a thread holds before storing
   constexpr int MB = 16 / G;             // batch rows per group
-  constexpr int XR = ND / G;             // activation register sets per lane
+  constexpr int XR = ND / G;             // activation registers per lane and tile
   constexpr int NT = 64 * WAVES;
+  constexpr int NOUT = 16 * MB * T;      // outputs per block: batch rows x 16 weight rows
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[PAIRS ? kLutWords : 4];
   __shared__ __attribute__((aligned(16))) uint8_t s_ct[WAVES][16 * TP];
-  __shared__ __attribute__((aligned(16))) float4v s_red[2][WAVES][64];
+  __shared__ __attribute__((aligned(16))) float4v s_red[2][WAVES][T][64];
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   const int j = lane & 15, g = lane >> 4;
   const uint32_t laneoff = (uint32_t)lane << 2;
   const int64_t row_bytes = (int64_t)k_cols / 2;
-  const int slice_k0 = w * 32 * ND;
+  // K part of this workgroup (KS = 2: workgroups 2 i and 2 i + 1 take the two halves of the
+  // same blocks) and its first block.
+  const int part = KS == 2 ? (int)(blockIdx.x & 1) : 0;
+  const int gb = (int)gridDim.x / KS;
+  const int b0 = (int)blockIdx.x / KS;
+  const int slice_k0 = part * (k_cols / KS) + w * 32 * ND;
+  const int slice_b0 = part * (int)(row_bytes / KS) + w * BR;
   auto seg_of = [&](int b) {
     int si = 0;
 #pragma unroll
@@ -1316,20 +1332,22 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
       if (i < nseg && b >= segs.s[i].blk_begin) si = i;
     return si;
   };
-  // Activations first (they return first): lane row j is batch row j % MB of dword group
-  // j / MB; register r holds dword d = G r + j / MB of this lane's slice, in the order the
-  // dequantization produces the weights.
-  u32x4 xa[XR];
-  {
-    const int mrow = j % MB, sg = j / MB;
+  // Activations first (they return first): in tile tt, lane row j is batch row
+  // 16 tt + j % MB of dword group j / MB; register r holds dword d = G r + j / MB of this
+  // lane's slice, in the order the dequantization produces the weights.
+  u32x4 xa[T][XR];
+#pragma unroll
+  for (int tt = 0; tt < T; ++tt) {
+    const int mrow = 16 * tt + j % MB, sg = j / MB;
     const bool live = mrow < m_rows;
     const int64_t base = (int64_t)(live ? mrow : 0) * k_cols + slice_k0 + 8 * ND * g;
 #pragma unroll
-    for (int r = 0; r < XR; ++r) xa[r] = *reinterpret_cast<const u32x4*>(x + base + 8 * (G * r + sg));
+    for (int r = 0; r < XR; ++r)
+      xa[tt][r] = *reinterpret_cast<const u32x4*>(x + base + 8 * (G * r + sg));
 #pragma unroll
     for (int r = 0; r < XR; ++r) {
-      u32x4 v = live ? xa[r] : u32x4{0u, 0u, 0u, 0u};
-      xa[r] = PAIRS ? v : permute_x8(v);
+      u32x4 v = live ? xa[tt][r] : u32x4{0u, 0u, 0u, 0u};
+      xa[tt][r] = PAIRS ? v : permute_x8(v);
     }
   }
   // Codes of block b: a descriptor over its rows (size 0 past the last block, short for a
@@ -1352,28 +1370,34 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
 #pragma unroll
     for (int c = 0; c < NI; ++c) {
       const int r = RPI * c + lane / ND;
-      const int off = r * (int)row_bytes + w * BR + 16 * (lane % ND);
+      const int off = r * (int)row_bytes + slice_b0 + 16 * (lane % ND);
       q[c] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kCachePolicyNT);
     }
   };
   u32x4 q[2][NI];
-  load_block(blockIdx.x, q[0]);
+  load_block(b0, q[0]);
   if (PAIRS) fill_lut<4, NT>(s_lut, lut);
   __syncthreads();
 
   float res[NRES];
   int held = 0, blast = 0, par = 0;
-  const int ri = t >> 4, rj = t & 15;      // element of threads t < 16 MB: batch ri, row rj
+  const int ri = t >> 4, rj = t & 15;      // element of threads t < NOUT: batch ri, row rj
+  // KS = 2: each output receives exactly two float atomic adds onto zero (the caller zeroes
+  // y first), and a + b = b + a, so the result does not depend on their order.
   auto flush = [&]() {
-    if (t < 16 * MB && ri < m_rows) {
+    if (t < NOUT && ri < m_rows) {
 #pragma unroll
       for (int h = 0; h < NRES; ++h) {
         if (h < held) {
-          const int b = blast - (held - 1 - h) * (int)gridDim.x;
+          const int b = blast - (held - 1 - h) * gb;
           const int si = seg_of(b);
           const int n_rows = segs.s[si].n_rows;
           const int row = (b - segs.s[si].blk_begin) * 16 + rj;
-          if (row < n_rows) segs.s[si].y[(int64_t)ri * n_rows + row] = res[h];
+          if (row < n_rows) {
+            float* yp = segs.s[si].y + (int64_t)ri * n_rows + row;
+            if (KS == 2) unsafeAtomicAdd(yp, res[h]);
+            else *yp = res[h];
+          }
         }
       }
     }
@@ -1395,9 +1419,11 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
     for (int c = 0; c < NI; ++c)
       o[c] = *reinterpret_cast<const u32x4*>(s_cw + j * TP + 4 * ND * g + 16 * c);
     __builtin_amdgcn_wave_barrier();
-    float4v acc[G];
+    float4v acc[T][G];
 #pragma unroll
-    for (int s = 0; s < G; ++s) acc[s] = float4v{0.f, 0.f, 0.f, 0.f};
+    for (int tt = 0; tt < T; ++tt)
+#pragma unroll
+      for (int s = 0; s < G; ++s) acc[tt][s] = float4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int d = 0; d < ND; ++d) {
       const u32x4 od = o[d >> 2];
@@ -1409,27 +1435,34 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
       } else {
         dequant_dword(dw, tb, bw);
       }
-      acc[d % G] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-          __builtin_bit_cast(half8v, xa[d / G]),
-          __builtin_bit_cast(half8v, u32x4{bw[0], bw[1], bw[2], bw[3]}), acc[d % G], 0, 0, 0);
-    }
-    // Lane l holds D rows 4 (l / 16) .. + 3, which belong to dword group (l / 16) G / 4.
-    float4v mine = acc[0];
 #pragma unroll
-    for (int s = 1; s < G; ++s)
-      if (my_group == s) mine = acc[s];
+      for (int tt = 0; tt < T; ++tt)
+        acc[tt][d % G] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+            __builtin_bit_cast(half8v, xa[tt][d / G]),
+            __builtin_bit_cast(half8v, u32x4{bw[0], bw[1], bw[2], bw[3]}), acc[tt][d % G], 0, 0,
+            0);
+    }
     // Lane l holds D[4 (l / 16) + r][l % 16] in component r: D row i is batch row i % MB of
-    // dword group i / MB, column l % 16 the weight row.
-    s_red[par][w][lane] = mine;
+    // dword group i / MB (so lane l's rows belong to group (l / 16) G / 4), column l % 16 the
+    // weight row.
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+      float4v mine = acc[tt][0];
+#pragma unroll
+      for (int s = 1; s < G; ++s)
+        if (my_group == s) mine = acc[tt][s];
+      s_red[par][w][tt][lane] = mine;
+    }
     __syncthreads();
-    if (t < 16 * MB) {
+    if (t < NOUT) {
+      const int tt = ri / MB, mrow = ri % MB;
       float sum = 0.0f;
 #pragma unroll
       for (int s = 0; s < G; ++s) {
-        const int i = s * MB + ri;
+        const int i = s * MB + mrow;
         const int l = 16 * (i >> 2) + rj, r = i & 3;
 #pragma unroll
-        for (int w2 = 0; w2 < WAVES; ++w2) sum += s_red[par][w2][l][r];
+        for (int w2 = 0; w2 < WAVES; ++w2) sum += s_red[par][w2][tt][l][r];
       }
 #pragma unroll
       for (int h = 0; h < NRES; ++h)
@@ -1443,11 +1476,11 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
   // Every path through the loop issues the same loads (blocks past the end get size-0
   // descriptors), so the compiler's waits stay exact. The barrier inside block() is reached by
   // the whole workgroup: the loop bounds depend only on the block index.
-  for (int b = blockIdx.x; b < nblocks; b += 2 * (int)gridDim.x) {
-    load_block(b + (int)gridDim.x, q[1]);
+  for (int b = b0; b < nblocks; b += 2 * gb) {
+    load_block(b + gb, q[1]);
     block(b, q[0]);
-    load_block(b + 2 * (int)gridDim.x, q[0]);
-    if (b + (int)gridDim.x < nblocks) block(b + (int)gridDim.x, q[1]);
+    load_block(b + 2 * gb, q[0]);
+    if (b + gb < nblocks) block(b + gb, q[1]);
   }
   flush();
 }
@@ -1824,20 +1857,27 @@ int32_t launch_kq(const uint16_t* x, int M, int K, const LinearJob& j, hipStream
   return launch_status();
 }
 
-// Split-K MFMA path: 4-bit codes, 2 <= m <= 16, K in {1024, 2048, 4096, 8192}.
+// Split-K MFMA path: 4-bit codes, 2 <= m <= 32, K in {1024, 2048, 4096, 8192}.
 bool sk_shape(int M, int K) {
-  return M >= 2 && M <= 16 && (K == 1024 || K == 2048 || K == 4096 || K == 8192);
+  return M >= 2 && M <= 32 && (K == 1024 || K == 2048 || K == 4096 || K == 8192);
 }
 
-// Split-K configuration: wavefronts per workgroup, code dwords per lane and row, batch groups.
-struct SkConfig { int nd, waves, groups; };
+// Split-K configuration: code dwords per lane and row, wavefronts per workgroup, batch groups,
+// batch tiles and K parts (workgroups per block).
+struct SkConfig { int nd, waves, groups, tiles, kparts; };
 SkConfig sk_config(int M, int K, bool pairs) {
+  if (M > 16) {   // two batch tiles (register tables only); K = 8192 over workgroup pairs
+    const int waves = K >= 2048 ? 16 : 8;
+    const int kparts = K == 8192 ? 2 : 1;
+    return {K / (32 * waves * kparts), waves, 1, 2, kparts};
+  }
   const int waves = (!pairs && K >= 4096) ? 16 : 8;
-  return {K / (32 * waves), waves, (!pairs && M <= 8) ? 2 : 1};
+  return {K / (32 * waves), waves, (!pairs && M <= 8) ? 2 : 1, 1, 1};
 }
 
 // Split-K launches for the linears jobs[idx[0..count)] of one call: one grouped launch when
-// every codebook is sign-symmetric (register dequantization), otherwise one launch per linear.
+// every codebook is sign-symmetric (register dequantization), otherwise one launch per linear
+// (above m = 16 a codebook that is not sign-symmetric takes the stepped MFMA kernel).
 int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const int* idx,
                   int count, hipStream_t st, int cus) {
   SkSegs segs;
@@ -1857,18 +1897,32 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
   }
   auto launch = [&](int nseg, const SkSegs& sgs, int nblocks, bool pairs,
                     const Lut16& l) -> int32_t {
-    const int grid = nblocks < cus ? nblocks : cus;
     const SkConfig c = sk_config(M, K, pairs);
-#define LOGBQ_SK(ND, W, GG, PR)                                                                  \
-  if (c.nd == ND && c.waves == W && c.groups == GG && pairs == PR) {                             \
-    hipLaunchKernelGGL((k_mfma_sk<ND, W, GG, PR>), dim3((unsigned)grid), dim3(64 * W), 0, st, x,  \
-                       sgs.s[0].codes, sgs.s[0].n_rows, nseg, nblocks, K, M, sgs, l);            \
+    // One workgroup per CU (the grid walks the blocks); with two K parts an even grid of
+    // workgroup pairs, after zeroing every output the atomic adds will land on.
+    int grid = nblocks * c.kparts < cus ? nblocks * c.kparts : cus;
+    grid -= grid % c.kparts;
+    if (c.kparts == 2)
+      for (int a = 0; a < nseg; ++a) {
+        const int64_t cnt = (int64_t)M * sgs.s[a].n_rows;
+        hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)grid_for(cnt, 256, (int64_t)cus * 16)),
+                           dim3(256), 0, st, sgs.s[a].y, cnt);
+      }
+#define LOGBQ_SK(ND, W, GG, TT, KP, PR)                                                          \
+  if (c.nd == ND && c.waves == W && c.groups == GG && c.tiles == TT && c.kparts == KP &&         \
+      pairs == PR) {                                                                             \
+    hipLaunchKernelGGL((k_mfma_sk<ND, W, GG, TT, KP, PR>), dim3((unsigned)grid), dim3(64 * W), 0, \
+                       st, x, sgs.s[0].codes, sgs.s[0].n_rows, nseg, nblocks, K, M, sgs, l);     \
     return launch_status();                                                                      \
   }
-    LOGBQ_SK(4, 8, 1, true) LOGBQ_SK(8, 8, 1, true) LOGBQ_SK(16, 8, 1, true) LOGBQ_SK(32, 8, 1, true)
-    LOGBQ_SK(4, 8, 1, false) LOGBQ_SK(4, 8, 2, false) LOGBQ_SK(8, 8, 1, false) LOGBQ_SK(8, 8, 2, false)
-    LOGBQ_SK(8, 16, 1, false) LOGBQ_SK(8, 16, 2, false)
-    LOGBQ_SK(16, 16, 1, false) LOGBQ_SK(16, 16, 2, false)
+    LOGBQ_SK(4, 8, 1, 1, 1, true) LOGBQ_SK(8, 8, 1, 1, 1, true)
+    LOGBQ_SK(16, 8, 1, 1, 1, true) LOGBQ_SK(32, 8, 1, 1, 1, true)
+    LOGBQ_SK(4, 8, 1, 1, 1, false) LOGBQ_SK(4, 8, 2, 1, 1, false)
+    LOGBQ_SK(8, 8, 1, 1, 1, false) LOGBQ_SK(8, 8, 2, 1, 1, false)
+    LOGBQ_SK(8, 16, 1, 1, 1, false) LOGBQ_SK(8, 16, 2, 1, 1, false)
+    LOGBQ_SK(16, 16, 1, 1, 1, false) LOGBQ_SK(16, 16, 2, 1, 1, false)
+    LOGBQ_SK(4, 8, 1, 2, 1, false) LOGBQ_SK(4, 16, 1, 2, 1, false)
+    LOGBQ_SK(8, 16, 1, 2, 1, false) LOGBQ_SK(8, 16, 1, 2, 2, false)
 #undef LOGBQ_SK
     return LOGBQ_ERR_UNSUPPORTED;
   };
@@ -1883,7 +1937,8 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     // table for any other.
     const bool symmetric = make_lut_bytes(j.codebook, &one.s[0].tb, &one.s[0].scale);
     make_lut16(j.codebook, &lut, &one.s[0].scale);
-    const int32_t r = launch(1, one, (int)((j.n + 15) / 16), !symmetric, lut);
+    const int32_t r = (M > 16 && !symmetric) ? launch_mfma<4>(x, M, K, j, st)
+                                              : launch(1, one, (int)((j.n + 15) / 16), !symmetric, lut);
     if (r != LOGBQ_OK) return r;
   }
   return LOGBQ_OK;
@@ -1901,18 +1956,23 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
 // sign-symmetric codebooks (7-11 % faster on the 8192 x 28672 and 4096 x 14336 layers; slower
 // on narrow layers, which have too few 128-row workgroups).
 //
-// Where the split-K MFMA kernel applies (4-bit codes, 2 <= m <= 16, K = 1, 2, 4 or 8 Ki), it
-// takes m >= 5, m = 4 unless N <= 1024 at K = 8192, and m = 3 at N >= 4096. Measured with
-// forced paths over N = 1024 .. 28672 and K = 2048 .. 8192: at m = 4 it beats the GEMV except
-// at N = 1024, K = 8192 (7.0 vs 6.9 us), e.g. 4096 x 4096: 4.9 vs 5.7 us, 8192 -> 28672:
-// 26.4 vs 37.7 us; at m = 3 from N = 4096 (one exception, 4096 -> 6144: 6.2 vs 5.9 us); at
-// m = 2 the GEMV wins (8192 -> 28672: 21.9 vs 25.4 us). It also beats the stepped MFMA kernel up
-// to m = 16 on the widest layer (8192 -> 28672 at m = 16: 30.6 vs 31.6 us).
+// Where the split-K MFMA kernel applies (4-bit codes, 2 <= m <= 32, K = 1, 2, 4 or 8 Ki), it
+// takes 5 <= m <= 16, m = 4 unless N <= 1024 at K = 8192, m = 3 at N >= 4096, and
+// 17 <= m <= 32 except m > 20 at K = 8192 and N > 16384. Measured with forced paths over
+// N = 1024 .. 28672 and K = 2048 .. 8192: at m = 4 it beats the GEMV except at N = 1024,
+// K = 8192 (7.0 vs 6.9 us), e.g. 4096 x 4096: 4.9 vs 5.7 us, 8192 -> 28672: 26.4 vs 37.7 us; at
+// m = 3 from N = 4096 (one exception, 4096 -> 6144: 6.2 vs 5.9 us); at m = 2 the GEMV wins
+// (8192 -> 28672: 21.9 vs 25.4 us). Up to m = 16 it beats the stepped MFMA kernel on every
+// layer (8192 -> 28672 at m = 16: 30.6 vs 31.6 us); at m = 32 on every layer but the widest:
+// 4096 x 4096 11.1 vs 20.4 us, 4096 -> 14336 16.7 vs 21.1 us, 8192 -> 2048 13.2 vs 37.5 us,
+// 8192 -> 14336 28.6 vs 39.1 us, but 8192 -> 28672 44.4 vs 41.3 us (there it wins to m = 20:
+// 38.6 vs 41.0 us).
 template <int BITS>
 int choose_path(int M, int K, int64_t N) {
   int wk = 0, cpl = 0;
   if (sk_shape(M, K) && BITS == 4 &&
-      (M >= 5 || (M == 4 && (N > 1024 || K <= 4096)) || (M == 3 && N >= 4096)))
+      ((M >= 5 && M <= 16) || (M == 4 && (N > 1024 || K <= 4096)) || (M == 3 && N >= 4096) ||
+       (M > 16 && (K <= 4096 || N <= 16384 || M <= 20))))
     return LOGBQ_PATH_SPLITK;
   if (M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl) && !(M >= 3 && (int64_t)M * N > 65536))
     return LOGBQ_PATH_GEMV;
@@ -2395,10 +2455,10 @@ int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const
     const bool symmetric = bits == 4 && (!codebook || make_lut_bytes(codebook, &tb, &scale));
     const int path = bits == 4 ? choose_path<4>(M, K, n) : choose_path<8>(M, K, n);
     int wk = 0, cpl = 0;
-    if (path == LOGBQ_PATH_SPLITK) {
+    if (path == LOGBQ_PATH_SPLITK && (M <= 16 || symmetric)) {
       const SkConfig c = sk_config(M, K, !symmetric);
-      std::snprintf(buf, sizeof(buf), "k_mfma_sk<%d, %d, %d, %s>", c.nd, c.waves, c.groups,
-                    symmetric ? "false" : "true");
+      std::snprintf(buf, sizeof(buf), "k_mfma_sk<%d, %d, %d, %d, %d, %s>", c.nd, c.waves,
+                    c.groups, c.tiles, c.kparts, symmetric ? "false" : "true");
     } else if (path == LOGBQ_PATH_GEMV) {
       const bool ok = bits == 4 ? gemv_config_rows<4>(M, K, n, &wk, &cpl)
                                 : gemv_config_rows<8>(M, K, n, &wk, &cpl);

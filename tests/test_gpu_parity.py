@@ -315,6 +315,37 @@ def test_linear_split_k_many_blocks():
         assert rel_err(y2.cpu().numpy(), x, wh2) <= TOL
 
 
+def test_linear_split_k_two_tiles():
+    """Split-K with two batch tiles (17 <= m <= 32) at every supported K, on ragged row counts:
+    at K = 8192 two workgroups add their K halves into y with float atomics after zeroing it,
+    so y is prefilled with NaN (every output must be overwritten) and each call is repeated
+    to check that the result is the same bit for bit. A grouped call equals single calls."""
+    for k in (1024, 2048, 4096, 8192):
+        ns = (300, 4099)
+        tensors = [prepare(n, k, [8, 21, k % 1000, j]) for j, n in enumerate(ns)]
+        codes = [gpu_encode(w, p) for w, p, r in tensors]
+        whs = [O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
+               for w, p, r in tensors]
+        for m in (17, 24, 32):
+            assert all(L.linear_path(4, m, k, n) == "splitk" for n in ns)
+            _say(f"split-K two tiles k={k} m={m}")
+            x = inputs.activations(m, k, seed=[8, 21, k % 1000, m])
+            xd = torch.from_numpy(x).to(DEV)
+            for (c, cb), wh, n in zip(codes, whs, ns):
+                y = torch.full((m, n), float("nan"), dtype=torch.float32, device=DEV)
+                L.linear(xd, c, cb, out=y)
+                y2 = L.linear(xd, c, cb)
+                torch.cuda.synchronize()
+                assert torch.isfinite(y).all()
+                assert torch.equal(y, y2)
+                assert rel_err(y.cpu().numpy(), x, wh) <= 2.5e-4
+            ys = L.linear_multi(xd, [c for c, _ in codes], [cb for _, cb in codes])
+            for (c, cb), yg in zip(codes, ys):
+                y1 = L.linear(xd, c, cb)
+                torch.cuda.synchronize()
+                assert torch.equal(yg, y1)
+
+
 def test_linear_multi_matches_single_launches():
     """Grouped launch of linears sharing x: every output equals the single-linear call bit for
     bit, and the oracle within tolerance (qkv-like and gate/up-like groups, ragged sizes)."""
