@@ -168,6 +168,34 @@ def test_encode8_every_float32(params):
     assert mism == 0
 
 
+def test_encode8_estimate_fallbacks():
+    """The 8-bit encode estimates each magnitude index from log2|x| and corrects it against the
+    thresholds; parameters whose thresholds do not sit where the estimate puts them (a base
+    that disagrees with the thresholds) or whose base is too close to 1 for a float estimate
+    take the binary search. Codes must equal the count of thresholds <= |x| either way."""
+    rng = np.random.default_rng(31)
+    for name, base, shift, claimed in (("consistent", 1.1, 100, None),
+                                        ("base disagrees", 1.1, 100, 1.5),
+                                        ("base near 1", 1.0001, 60000, None)):
+        _say(f"encode8 estimate: {name}")
+        thr = O.magnitude_thresholds(base, shift, 8)
+        p = L.Params()
+        p.bits, p.qmax, p.base, p.shift = 8, 127, claimed or base, shift
+        for i in range(127):
+            p.thresholds[i] = float(thr[i])
+        p.thresholds[127] = float("inf")
+        lo, hi = np.log2(float(thr[0])) - 2, np.log2(float(thr[126])) + 2
+        mags = np.exp2(rng.uniform(lo, hi, size=64 * 4096)).astype(np.float32)
+        x = (mags * rng.choice([-1.0, 1.0], size=mags.size)).astype(np.float32)
+        x[:254] = np.repeat(thr, 2) * np.tile([1.0, -1.0], 127)          # thresholds themselves
+        w = x.reshape(64, 4096)
+        codes, _ = L.encode(torch.from_numpy(w).to(DEV), p)
+        torch.cuda.synchronize()
+        mag = np.searchsorted(thr, np.abs(w), side="right").astype(np.int64)
+        exp = (mag + 128 * ((w < 0) & (mag > 0))).astype(np.uint8)
+        assert np.array_equal(codes.cpu().numpy(), exp), name
+
+
 # ---------------------------------------------------------------- linear
 
 SHAPES = [(2048, 2048), (1000, 352), (37, 32), (512, 14336), (4096, 4096), (64, 8192),
