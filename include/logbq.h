@@ -234,8 +234,11 @@ int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const f
  *   codebook  : host, 256 floats (logbq_params.codebook of an 8-bit fit); rounded to float16
  *               after a common power-of-two scaling, as for logbq_linear.
  *   y_dev     : device, [m][n] float32, written.
- * Float32 accumulation. The GEMV runs for m <= 8 unless m >= 3 and m * n > 65536; the
- * dequantize-into-MFMA skinny GEMM runs otherwise. Errors: as logbq_linear.
+ * Float32 accumulation. For k in {2048, 4096, 8192} a split-K dequantize-into-MFMA kernel
+ * takes 5 <= m <= 8 unless n <= 1024 at k >= 4096, m = 3, 4 at n >= 8192, and 9 <= m <= 16
+ * unless n > 16384 at k = 8192; otherwise the GEMV runs for m <= 8 unless m >= 5 and
+ * m * n > 65536, and the stepped dequantize-into-MFMA skinny GEMM runs for the rest.
+ * Errors: as logbq_linear.
  */
 int32_t logbq_linear8(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
                       int64_t n, const float* codebook, float* y_dev, void* stream);
@@ -313,9 +316,9 @@ typedef enum logbq_path {
   LOGBQ_PATH_NONE = 0,     /* m or n is 0 (nothing written) or k is 0 (zeros written)        */
   LOGBQ_PATH_GEMV = 1,     /* wavefront-reduced GEMV with the LDS pair table                  */
   LOGBQ_PATH_MFMA = 2,     /* stepped dequantize-into-MFMA skinny GEMM                        */
-  LOGBQ_PATH_SPLITK = 3,   /* split-K dequantize-into-MFMA kernel (4-bit, 2 <= m <= 32); above
-                              m = 16 a codebook that is not sign-symmetric runs the stepped
-                              kernel instead                                                  */
+  LOGBQ_PATH_SPLITK = 3,   /* split-K dequantize-into-MFMA kernel (4-bit, 2 <= m <= 32; 8-bit,
+                              3 <= m <= 16); above m = 16 a 4-bit codebook that is not
+                              sign-symmetric runs the stepped kernel instead                  */
   LOGBQ_PATH_MFMA_KQ = 4   /* K-quartered dequantize-into-MFMA GEMM (4-bit, m > 96, n >= 4096);
                               a codebook that is not sign-symmetric (never a fitted one) runs the
                               stepped kernel instead                                          */

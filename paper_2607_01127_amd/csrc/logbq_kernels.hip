@@ -19,7 +19,7 @@
 //   k_mfma_kq  the same product for m > 96: each wavefront takes 64 weight rows and one K
 //              quarter of every step for all 128 batch rows of the workgroup; the quarters'
 //              tiles are summed through LDS at the end.
-//   k_encode8, k_dequant8, k_gemv<8, ...>, k_mfma2<8, ...>  the same on 8-bit codes.
+//   k_encode8, k_dequant8, k_gemv<8, ...>, k_mfma_sk8, k_mfma2<8, ...>  the same on 8-bit codes.
 //   k_encode_uniform  codes of the asymmetric linear baseline (Sec. 2), for comparisons.
 //   k_gptq_panel, k_gptq_trail  GPTQ calibration with a fixed codebook (one wavefront per row
 //              within a block of 128 columns; the block's errors applied to the later columns).
@@ -1504,6 +1504,151 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
   flush();
 }
 
+// ------------------------------------------------------------------ split-K MFMA, 8-bit codes
+//
+// The split-K scheme of k_mfma_sk on one code byte per weight: 16 wavefronts, m <= 16,
+// K = 512 ND (ND = 4, 8, 16 MFMAs per lane and block), batch groups G as in k_mfma_sk. Each
+// weight is looked up in the LDS table of float16 images (one private copy per lane, 64 KiB,
+// two lookups per float16 pair), so the 16 wavefronts' transpose buffers must be small: they
+// run in phases of 128 code bytes per row (4 MFMAs) through 2.3 KiB per wavefront. Phase p of a
+// block is loaded as two instructions of 8 rows x 128 B, written to the buffer, and the same
+// registers are refilled at once with phase p of the workgroup's next block (one block of
+// look-ahead in 2 ND / 4 registers). Lane (j, g) then reads row j, bytes [32 g, 32 g + 32) of
+// the phase: MFMA d = 4 p + m contracts k = w S + 128 p + 32 g + 8 m + 0..7 (natural order),
+// S = 32 ND. One launch serves one linear (its table fills LDS). Measured on MI355X against the
+// stepped MFMA kernel (8-bit): 8192 -> 28672 at m = 5 / 8: 57.4 / 57.6 -> 42.1 / 42.5 us,
+// 4096 -> 14336 at m = 8: 28.1 -> 14.2 us, 8192 -> 2048 at m = 16: 48.8 -> 17.1 us; but
+// 8192 -> 28672 at m = 16: 57.9 -> 60.4 us, so m > 8 at K = 8192 and N > 16384 stays on the
+// stepped kernel.
+template <int ND, int G>
+__global__ __launch_bounds__(1024) void k_mfma_sk8(const uint16_t* __restrict__ x,
+                                                   const uint8_t* __restrict__ codes, int n_rows,
+                                                   int nblocks, int k_cols, int m_rows,
+                                                   float* __restrict__ y, float scale, Lut256 lut) {
+  static_assert(ND == 4 || ND == 8 || ND == 16, "K = 512 ND");
+  static_assert(G == 1 || G == 2, "batch groups");
+  constexpr int W = 16;
+  constexpr int NP = ND / 4;             // phases per block
+  constexpr int TP = 128 + 16;           // transpose pitch (bytes)
+  constexpr int NRES = 4;
+  constexpr int MB = 16 / G;
+  constexpr int XR = ND / G;
+  __shared__ __attribute__((aligned(16))) uint32_t s_lut[kLutWords];
+  __shared__ __attribute__((aligned(16))) uint8_t s_ct[W][16 * TP];
+  __shared__ __attribute__((aligned(16))) float4v s_red[2][W][64];
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int j = lane & 15, g = lane >> 4;
+  const uint32_t laneoff = (uint32_t)lane << 2;
+  const int slice0 = w * 32 * ND;        // first weight (and code byte) of this wavefront's slice
+  u32x4 xa[XR];
+  {
+    const int mrow = j % MB, sg = j / MB;
+    const bool live = mrow < m_rows;
+    const int64_t base = (int64_t)(live ? mrow : 0) * k_cols + slice0 + 32 * g;
+#pragma unroll
+    for (int r = 0; r < XR; ++r) {
+      const int d = G * r + sg;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(x + base + 128 * (d >> 2) + 8 * (d & 3));
+      xa[r] = live ? v : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  auto load_phase = [&](int b, int p, u32x4 (&q)[2]) {
+    const int bb = b < nblocks ? b : nblocks - 1;
+    const int64_t base = (int64_t)bb * 16 * k_cols;
+    const int64_t avail = (int64_t)n_rows * k_cols - base;
+    const int size = b < nblocks ? (int)(avail < 16 * (int64_t)k_cols ? avail : 16 * (int64_t)k_cols) : 0;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(codes + base), (short)0, size, kBufferRsrcWord3);
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int off = (8 * c + (lane >> 3)) * k_cols + slice0 + 128 * p + 16 * (lane & 7);
+      q[c] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kCachePolicyNT);
+    }
+  };
+  const int gb = (int)gridDim.x;
+  u32x4 q[NP][2];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) load_phase(blockIdx.x, p, q[p]);
+  fill_single_lut<1024>(s_lut, lut);
+  __syncthreads();
+
+  float res[NRES];
+  int held = 0, blast = 0, par = 0;
+  const int ri = t >> 4, rj = t & 15;
+  auto flush = [&]() {
+    if (t < 16 * MB && ri < m_rows) {
+#pragma unroll
+      for (int h = 0; h < NRES; ++h) {
+        if (h < held) {
+          const int b = blast - (held - 1 - h) * gb;
+          const int row = b * 16 + rj;
+          if (row < n_rows) y[(int64_t)ri * n_rows + row] = res[h];
+        }
+      }
+    }
+    held = 0;
+  };
+  uint8_t* s_cw = s_ct[w];
+  const int my_group = (lane >> 4) * G / 4;
+  for (int b = blockIdx.x; b < nblocks; b += gb) {
+    float4v acc[G];
+#pragma unroll
+    for (int s = 0; s < G; ++s) acc[s] = float4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      // LDS operations of one wavefront complete in order: the reads see the writes.
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        *reinterpret_cast<u32x4*>(s_cw + (8 * c + (lane >> 3)) * TP + 16 * (lane & 7)) = q[p][c];
+      load_phase(b + gb, p, q[p]);
+      __builtin_amdgcn_wave_barrier();
+      u32x4 o[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        o[i] = *reinterpret_cast<const u32x4*>(s_cw + j * TP + 32 * g + 16 * i);
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int d = 4 * p + m;
+        const u32x4 od = o[m >> 1];
+        const uint32_t d0 = (m & 1) ? od.z : od.x;
+        const uint32_t d1 = (m & 1) ? od.w : od.y;
+        const u32x4 bw{single_pair(s_lut, d0, laneoff, 0), single_pair(s_lut, d0, laneoff, 1),
+                       single_pair(s_lut, d1, laneoff, 0), single_pair(s_lut, d1, laneoff, 1)};
+        acc[d % G] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+            __builtin_bit_cast(half8v, xa[d / G]), __builtin_bit_cast(half8v, bw), acc[d % G],
+            0, 0, 0);
+      }
+    }
+    float4v mine = acc[0];
+#pragma unroll
+    for (int s = 1; s < G; ++s)
+      if (my_group == s) mine = acc[s];
+    s_red[par][w][lane] = mine;
+    __syncthreads();
+    if (t < 16 * MB) {
+      float sum = 0.0f;
+#pragma unroll
+      for (int s = 0; s < G; ++s) {
+        const int i = s * MB + ri;
+        const int l = 16 * (i >> 2) + rj, r = i & 3;
+#pragma unroll
+        for (int w2 = 0; w2 < W; ++w2) sum += s_red[par][w2][l][r];
+      }
+#pragma unroll
+      for (int h = 0; h < NRES; ++h)
+        if (h == held) res[h] = sum * scale;
+    }
+    par ^= 1;
+    ++held;
+    blast = b;
+    if (held == NRES) flush();
+  }
+  flush();
+}
+
 // ------------------------------------------------------------------ device fit, exact Eq. 5
 //
 // One pass of the radix selection described in fit_detail.h. Workgroup g takes the weights
@@ -1863,6 +2008,28 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
   return launch_status();
 }
 
+// Split-K launch on 8-bit codes (one linear per launch).
+bool sk8_shape(int M, int K) { return M >= 2 && M <= 16 && (K == 2048 || K == 4096 || K == 8192); }
+
+int32_t launch_sk8(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st, int cus) {
+  Lut256 lut;
+  float scale;
+  make_lut<8>(j.codebook, &lut, &scale);
+  const int nblocks = (int)((j.n + 15) / 16);
+  const int grid = nblocks < cus ? nblocks : cus;
+  const bool g2 = M <= 8;
+#define LOGBQ_SK8(ND, GG)                                                                        \
+  hipLaunchKernelGGL((k_mfma_sk8<ND, GG>), dim3((unsigned)grid), dim3(1024), 0, st, x, j.codes, \
+                     (int)j.n, nblocks, K, M, j.y, scale, lut)
+  switch (K) {
+    case 2048: if (g2) LOGBQ_SK8(4, 2); else LOGBQ_SK8(4, 1); break;
+    case 4096: if (g2) LOGBQ_SK8(8, 2); else LOGBQ_SK8(8, 1); break;
+    default: if (g2) LOGBQ_SK8(16, 2); else LOGBQ_SK8(16, 1); break;
+  }
+#undef LOGBQ_SK8
+  return launch_status();
+}
+
 // K-quartered MFMA path (4-bit, sign-symmetric codebooks): m > 96 at N >= 4096.
 bool kq_shape(int M, int64_t N) { return M > 96 && N >= 4096; }
 
@@ -1967,7 +2134,9 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
 // products are VALU dot2 per weight and batch row); the MFMA kernel's is about flat in m up to
 // 16 but uses only N / 128 workgroups. Measured crossover: the MFMA kernel wins once m >= 3 and
 // m * N > 65536 (N = 28672 from m = 3, N = 14336 from m = 5; at N = 8192, m = 8 the GEMV is
-// still 1 us faster); the GEMV takes everything else up to m = 8. The choice depends only on
+// still 1 us faster); the GEMV takes everything else up to m = 8. At 8 bits the stepped MFMA
+// kernel looks up every weight in its LDS table and the GEMV stays ahead to m = 4 on every
+// layer (8192 -> 28672 at m = 3 / 4: 48.0 / 56.1 us vs 57.2 / 57.3 us; at m = 6: 103 vs 57 us). The choice depends only on
 // (m, k, N), so every linear of a grouped call runs the kernel that a single call would run,
 // with the same result bits.
 //
@@ -1986,14 +2155,24 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
 // 4096 x 4096 11.1 vs 20.4 us, 4096 -> 14336 16.7 vs 21.1 us, 8192 -> 2048 13.2 vs 37.5 us,
 // 8192 -> 14336 28.6 vs 39.1 us, but 8192 -> 28672 44.4 vs 41.3 us (there it wins to m = 20:
 // 38.6 vs 41.0 us).
+//
+// 8-bit codes take their split-K kernel for 5 <= m <= 8 unless N <= 1024 at K >= 4096, for
+// m = 3, 4 at N >= 8192 and for 9 <= m <= 16 unless N > 16384 at K = 8192 (forced-path builds
+// over N = 1024 .. 28672, K = 2048 .. 8192: e.g. 4096 x 4096 at m = 8: 7.3 us vs 12.9 us for the
+// GEMV; 8192 -> 28672 at m = 5: 40.9 vs 90.7 us; N = 1024, K = 8192 at m = 8: 9.9 vs 8.4 us).
 template <int BITS>
 int choose_path(int M, int K, int64_t N) {
   int wk = 0, cpl = 0;
+  if (BITS == 8 && sk8_shape(M, K) &&
+      ((M >= 5 && M <= 8 && !(N <= 1024 && K >= 4096)) || (M <= 4 && M >= 3 && N >= 8192) ||
+       (M >= 9 && !(K == 8192 && N > 16384))))
+    return LOGBQ_PATH_SPLITK;
   if (sk_shape(M, K) && BITS == 4 &&
       ((M >= 5 && M <= 16) || (M == 4 && (N > 1024 || K <= 4096)) || (M == 3 && N >= 4096) ||
        (M > 16 && (K <= 4096 || N <= 16384 || M <= 20))))
     return LOGBQ_PATH_SPLITK;
-  if (M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl) && !(M >= 3 && (int64_t)M * N > 65536))
+  if (M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl) &&
+      !(M >= (BITS == 8 ? 5 : 3) && (int64_t)M * N > 65536))
     return LOGBQ_PATH_GEMV;
   if (BITS == 4 && kq_shape(M, N)) return LOGBQ_PATH_MFMA_KQ;
   return LOGBQ_PATH_MFMA;
@@ -2030,7 +2209,10 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
   for (int a = 0; a < nlive; ++a) {
     const LinearJob& j = jobs[live[a]];
     const int path = choose_path<BITS>(M, K, j.n);
-    if (path == LOGBQ_PATH_SPLITK) {
+    if (path == LOGBQ_PATH_SPLITK && BITS == 8) {
+      const int32_t r = launch_sk8(x, M, K, j, st, cus);
+      if (r != LOGBQ_OK) return r;
+    } else if (path == LOGBQ_PATH_SPLITK) {
       sl[ns++] = live[a];
     } else if (path == LOGBQ_PATH_GEMV) {
       gl[ng++] = live[a];
@@ -2492,7 +2674,9 @@ int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const
     const bool symmetric = bits == 4 && (!codebook || make_lut_bytes(codebook, &tb, &scale));
     const int path = bits == 4 ? choose_path<4>(M, K, n) : choose_path<8>(M, K, n);
     int wk = 0, cpl = 0;
-    if (path == LOGBQ_PATH_SPLITK && (M <= 16 || symmetric)) {
+    if (path == LOGBQ_PATH_SPLITK && bits == 8) {
+      std::snprintf(buf, sizeof(buf), "k_mfma_sk8<%d, %d>", K / 512, M <= 8 ? 2 : 1);
+    } else if (path == LOGBQ_PATH_SPLITK && (M <= 16 || symmetric)) {
       const SkConfig c = sk_config(M, K, !symmetric);
       std::snprintf(buf, sizeof(buf), "k_mfma_sk<%d, %d, %d, %d, %d, %s>", c.nd, c.waves,
                     c.groups, c.tiles, c.kparts, symmetric ? "false" : "true");

@@ -254,9 +254,15 @@ def test_linear_path_rule():
     # K-quartered MFMA GEMM: 4-bit, m > 96 at N >= 4096
     assert lp(4, 128, 8192, 28672) == "mfma_kq" and lp(4, 97, 1024, 4096) == "mfma_kq"
     assert lp(4, 128, 1024, 4095) == "mfma" and lp(8, 128, 8192, 28672) == "mfma"
-    # 8-bit codes: GEMV unless m >= 3 and m * N > 65536, else the stepped MFMA kernel
+    # 8-bit codes: split-K for K in {2, 4, 8} Ki at 5 <= m <= 8 (not N <= 1024 at K >= 4096),
+    # m = 3, 4 from N = 8192, 9 <= m <= 16 (not N > 16384 at K = 8192); else GEMV unless m >= 5
+    # and m * N > 65536, else the stepped MFMA kernel
     assert lp(8, 1, 8192, 28672) == "gemv" and lp(8, 2, 8192, 28672) == "gemv"
-    assert lp(8, 8, 8192, 28672) == "mfma" and lp(8, 8, 2048, 8192) == "gemv"
+    assert lp(8, 3, 8192, 28672) == "splitk" and lp(8, 4, 4096, 4096) == "gemv"
+    assert lp(8, 5, 8192, 28672) == "splitk" and lp(8, 8, 2048, 8192) == "splitk"
+    assert lp(8, 8, 8192, 1024) == "gemv" and lp(8, 8, 2048, 1024) == "splitk"
+    assert lp(8, 16, 8192, 16384) == "splitk" and lp(8, 16, 8192, 28672) == "mfma"
+    assert lp(8, 8, 6144, 28672) == "mfma" and lp(8, 17, 4096, 4096) == "mfma"
     for bad in ((4, -1, 64, 1), (4, 1, 64, -1)):
         with pytest.raises(L.LogbqError):
             lp(*bad)
@@ -282,6 +288,7 @@ def test_linear_kernel_names():
     assert lk(4, 128, 8192, 28672) == "k_mfma_kq"
     assert lk(8, 1, 8192, 28672) == "k_gemv<8, 1, 8, false, 2>"
     assert lk(8, 128, 8192, 28672) == "k_mfma2<8, 4, 4, true, false>"
+    assert lk(8, 8, 8192, 28672) == "k_mfma_sk8<16, 2>" and lk(8, 12, 4096, 4096) == "k_mfma_sk8<8, 1>"
     assert lk(4, 0, 8192, 28672) == "none" and lk(4, 3, 0, 5) == "k_fill_zero"
     # a codebook that is not sign-symmetric takes the LDS table
     cb = np.arange(16, dtype=np.float32)

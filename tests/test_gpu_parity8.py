@@ -310,6 +310,35 @@ def test_linear8_arbitrary_codebook():
             assert rel_err(y.cpu().numpy(), x, wh) <= TOL
 
 
+def test_linear8_split_k():
+    """The 8-bit split-K kernel at every K it serves, batch groups of two (m <= 8) and one, row
+    counts that leave a partial last block, more blocks per workgroup than results held, a
+    fitted and an arbitrary codebook; y prefilled with NaN so that every output must be
+    written, and two calls bit-equal."""
+    rng = np.random.default_rng(41)
+    for n, k in ((3001, 8192), (6007, 4096), (20001, 2048)):
+        w, p, r = prepare(n, k, [18, 41, k % 1000, 0])
+        codes, cb = gpu_encode(w, p)
+        wh = oracle_w_hat(w, r)
+        cb2 = rng.standard_normal(256).astype(np.float32)
+        wh2 = O.dequantize(codes.cpu().numpy(), cb2)
+        for m in (3, 5, 8, 9, 16):
+            if L.linear_path(8, m, k, n) != "splitk":
+                continue
+            _say(f"linear8 split-K n={n} k={k} m={m}")
+            x = inputs.activations(m, k, seed=[18, 41, k % 1000, m])
+            xd = torch.from_numpy(x).to(DEV)
+            for book, ref, bar in ((cb, wh, 2.5e-4), (cb2, wh2, TOL)):
+                y = torch.full((m, n), float("nan"), dtype=torch.float32, device=DEV)
+                L.linear8(xd, codes, book, out=y)
+                y2 = L.linear8(xd, codes, book)
+                torch.cuda.synchronize()
+                assert torch.isfinite(y).all()
+                assert torch.equal(y, y2)
+                assert rel_err(y.cpu().numpy(), x, ref) <= bar, (n, k, m)
+    assert L.linear_path(8, 8, 8192, 3001) == "splitk" and L.linear_path(8, 16, 2048, 20001) == "splitk"
+
+
 # ---------------------------------------------------------------- full-size, sampled
 
 def test_full_size_layer8_8192x28672_sampled():
