@@ -1292,6 +1292,10 @@ __global__ __launch_bounds__(512) void k_mfma_kq(const uint8_t* __restrict__ cod
 // the same blocks and add their results into y with float atomics after y is zeroed (two terms
 // onto zero: the same sum in either order, so results stay deterministic). The alternative
 // of two launches (the second adding into y) measured 7-8 us slower at 8192 -> 28672.
+// K = 14336 (m <= 8, G = 2) takes the same K split over workgroup pairs of W = 14 wavefronts,
+// ND = 16: 14336 -> 4096 at m = 4 / 8: 14.5 / 26.7 -> 11.5 / 12.6 us against the split-row
+// GEMV and the stepped kernel (one 16-wavefront workgroup per block, ND = 28, measured
+// 14.8 / 17.2 us: 256 blocks leave each workgroup one block, with nothing to overlap).
 //
 // Up to kMaxSegs linears that share x, in one launch: their 16-row blocks are numbered one
 // after another (segment s holds blocks [blk_begin, blk_begin + ceil(n_rows / 16))), and every
@@ -1317,8 +1321,8 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
                                                  SkSegs segs, Lut16 lut) {
   static_assert(ND == 4 || ND == 8 || ND == 16 || ND == 32, "64 / ND rows per load");
   static_assert(G == 1 || G == 2 || G == 4, "batch groups");
-  static_assert((T == 1 || (T == 2 && G == 1 && !PAIRS)) && (KS == 1 || (KS == 2 && T == 2)),
-                "two batch tiles (and the K split) only with one group and register tables");
+  static_assert((T == 1 || (T == 2 && G == 1 && !PAIRS)) && (KS == 1 || (KS == 2 && !PAIRS)),
+                "two batch tiles and the K split only with register tables");
   constexpr int BR = 16 * ND;            // code bytes per row per wavefront and block
   constexpr int RPI = 64 / ND;           // rows per load instruction
   constexpr int NI = ND / 4;             // load instructions per block
@@ -1395,7 +1399,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
   };
   u32x4 q[2][NI];
   load_block(b0, q[0]);
-  if (PAIRS) fill_lut<4, NT>(s_lut, lut);
+  if constexpr (PAIRS) fill_lut<4, NT>(s_lut, lut);
   __syncthreads();
 
   float res[NRES];
@@ -2043,15 +2047,19 @@ int32_t launch_kq(const uint16_t* x, int M, int K, const LinearJob& j, hipStream
   return launch_status();
 }
 
-// Split-K MFMA path: 4-bit codes, 2 <= m <= 32, K in {1024, 2048, 4096, 8192}.
+// Split-K MFMA path: 4-bit codes, 2 <= m <= 32 at K in {1024, 2048, 4096, 8192}, and
+// 2 <= m <= 8 at K = 14336 (the down projection of the 8B-shaped decoder).
 bool sk_shape(int M, int K) {
-  return M >= 2 && M <= 32 && (K == 1024 || K == 2048 || K == 4096 || K == 8192);
+  return M >= 2 && ((M <= 32 && (K == 1024 || K == 2048 || K == 4096 || K == 8192)) ||
+                    (M <= 8 && K == 14336));
 }
 
 // Split-K configuration: code dwords per lane and row, wavefronts per workgroup, batch groups,
 // batch tiles and K parts (workgroups per block).
 struct SkConfig { int nd, waves, groups, tiles, kparts; };
 SkConfig sk_config(int M, int K, bool pairs) {
+  // K = 14336 = 2 x 14 x 512: workgroup pairs of 14 wavefronts, one K half each.
+  if (K == 14336) return {16, 14, 2, 1, 2};
   if (M > 16) {   // two batch tiles (register tables only); K = 8192 over workgroup pairs
     const int waves = K >= 2048 ? 16 : 8;
     const int kparts = K == 8192 ? 2 : 1;
@@ -2063,7 +2071,8 @@ SkConfig sk_config(int M, int K, bool pairs) {
 
 // Split-K launches for the linears jobs[idx[0..count)] of one call: one grouped launch when
 // every codebook is sign-symmetric (register dequantization), otherwise one launch per linear
-// (above m = 16 a codebook that is not sign-symmetric takes the stepped MFMA kernel).
+// (above m = 16, and at K = 14336, a codebook that is not sign-symmetric takes the stepped MFMA
+// kernel).
 int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const int* idx,
                   int count, hipStream_t st, int cus) {
   SkSegs segs;
@@ -2109,6 +2118,7 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     LOGBQ_SK(16, 16, 1, 1, 1, false) LOGBQ_SK(16, 16, 2, 1, 1, false)
     LOGBQ_SK(4, 8, 1, 2, 1, false) LOGBQ_SK(4, 16, 1, 2, 1, false)
     LOGBQ_SK(8, 16, 1, 2, 1, false) LOGBQ_SK(8, 16, 1, 2, 2, false)
+    LOGBQ_SK(16, 14, 2, 1, 2, false)
 #undef LOGBQ_SK
     return LOGBQ_ERR_UNSUPPORTED;
   };
@@ -2123,8 +2133,9 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     // table for any other.
     const bool symmetric = make_lut_bytes(j.codebook, &one.s[0].tb, &one.s[0].scale);
     make_lut16(j.codebook, &lut, &one.s[0].scale);
-    const int32_t r = (M > 16 && !symmetric) ? launch_mfma<4>(x, M, K, j, st)
-                                              : launch(1, one, (int)((j.n + 15) / 16), !symmetric, lut);
+    const int32_t r = ((M > 16 || K == 14336) && !symmetric)
+                          ? launch_mfma<4>(x, M, K, j, st)
+                          : launch(1, one, (int)((j.n + 15) / 16), !symmetric, lut);
     if (r != LOGBQ_OK) return r;
   }
   return LOGBQ_OK;
@@ -2676,7 +2687,7 @@ int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const
     int wk = 0, cpl = 0;
     if (path == LOGBQ_PATH_SPLITK && bits == 8) {
       std::snprintf(buf, sizeof(buf), "k_mfma_sk8<%d, %d>", K / 512, M <= 8 ? 2 : 1);
-    } else if (path == LOGBQ_PATH_SPLITK && (M <= 16 || symmetric)) {
+    } else if (path == LOGBQ_PATH_SPLITK && ((M <= 16 && K != 14336) || symmetric)) {
       const SkConfig c = sk_config(M, K, !symmetric);
       std::snprintf(buf, sizeof(buf), "k_mfma_sk<%d, %d, %d, %d, %d, %s>", c.nd, c.waves,
                     c.groups, c.tiles, c.kparts, symmetric ? "false" : "true");

@@ -250,6 +250,7 @@ def test_linear_path_rule():
     assert lp(4, 17, 8192, 2048) == "splitk" and lp(4, 32, 8192, 16384) == "splitk"
     assert lp(4, 20, 8192, 28672) == "splitk" and lp(4, 21, 8192, 28672) == "mfma"
     assert lp(4, 32, 4096, 28672) == "splitk" and lp(4, 33, 4096, 4096) == "mfma"
+    assert lp(4, 4, 14336, 4096) == "splitk" and lp(4, 9, 14336, 4096) == "mfma"
     assert lp(4, 96, 8192, 28672) == "mfma"
     # K-quartered MFMA GEMM: 4-bit, m > 96 at N >= 4096
     assert lp(4, 128, 8192, 28672) == "mfma_kq" and lp(4, 97, 1024, 4096) == "mfma_kq"
@@ -284,6 +285,7 @@ def test_linear_kernel_names():
     assert lk(4, 32, 4096, 14336) == "k_mfma_sk<8, 16, 1, 2, 1, false>"   # two batch tiles
     assert lk(4, 32, 8192, 2048) == "k_mfma_sk<8, 16, 1, 2, 2, false>"    # K over 2 workgroups
     assert lk(4, 32, 1024, 4096) == "k_mfma_sk<4, 8, 1, 2, 1, false>"
+    assert lk(4, 4, 14336, 4096) == "k_mfma_sk<16, 14, 2, 1, 2, false>"   # K over 2 workgroups
     assert lk(4, 32, 8192, 28672) == "k_mfma2<4, 2, 4, false, true>"
     assert lk(4, 128, 8192, 28672) == "k_mfma_kq"
     assert lk(8, 1, 8192, 28672) == "k_gemv<8, 1, 8, false, 2>"
@@ -294,6 +296,7 @@ def test_linear_kernel_names():
     cb = np.arange(16, dtype=np.float32)
     assert lk(4, 8, 8192, 28672, cb) == "k_mfma_sk<32, 8, 1, 1, 1, true>"
     assert lk(4, 32, 4096, 14336, cb) == "k_mfma2<4, 2, 4, true, true>"   # above m = 16
+    assert lk(4, 4, 14336, 4096, cb) == "k_mfma2<4, 1, 4, true, true>"    # and at K = 14336
     assert lk(4, 128, 8192, 28672, cb) == "k_mfma2<4, 4, 4, true, false>"
     sym = np.array([0] + [2.0 ** k for k in range(1, 8)] + [0] + [-(2.0 ** k) for k in range(1, 8)],
                    dtype=np.float32)

@@ -278,7 +278,7 @@ def test_linear_arbitrary_codebook():
     sign-symmetric and takes the register-dequant MFMA path, any other takes the pair table."""
     rng = np.random.default_rng(12)
     n = 300
-    for k in (1024, 2048, 4096, 8192):
+    for k in (1024, 2048, 4096, 8192, 14336):
         codes_np = rng.integers(0, 16, size=(n, k), dtype=np.uint8)
         codes = torch.from_numpy(O.pack(codes_np)).to(DEV)
         for trial in range(2):
