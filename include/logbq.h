@@ -238,7 +238,8 @@ int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const f
  * Float32 accumulation. For k in {2048, 4096, 8192} a split-K dequantize-into-MFMA kernel
  * takes 5 <= m <= 8 unless n <= 1024 at k >= 4096, m = 3, 4 at n >= 8192, and 9 <= m <= 16
  * unless n > 16384 at k = 8192; otherwise the GEMV runs for m <= 8 unless m >= 5 and
- * m * n > 65536, and the stepped dequantize-into-MFMA skinny GEMM runs for the rest.
+ * m * n > 65536, a K-quartered MFMA GEMM for m > 64 at n >= 16384, and the stepped
+ * dequantize-into-MFMA skinny GEMM for the rest.
  * Errors: as logbq_linear.
  */
 int32_t logbq_linear8(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
@@ -320,9 +321,9 @@ typedef enum logbq_path {
   LOGBQ_PATH_SPLITK = 3,   /* split-K dequantize-into-MFMA kernel (4-bit, 2 <= m <= 32; 8-bit,
                               3 <= m <= 16); above m = 16 a 4-bit codebook that is not
                               sign-symmetric runs the stepped kernel instead                  */
-  LOGBQ_PATH_MFMA_KQ = 4   /* K-quartered dequantize-into-MFMA GEMM (4-bit, m > 96, n >= 4096);
-                              a codebook that is not sign-symmetric (never a fitted one) runs the
-                              stepped kernel instead                                          */
+  LOGBQ_PATH_MFMA_KQ = 4   /* K-quartered dequantize-into-MFMA GEMM (4-bit, m > 96, n >= 4096;
+                              8-bit, m > 64, n >= 16384); a 4-bit codebook that is not
+                              sign-symmetric (never a fitted one) runs the stepped kernel     */
 } logbq_path;
 
 /*

@@ -20,7 +20,7 @@
 //   k_mfma_sk8 the split-K product on 8-bit codes (m <= 16), weights looked up in an LDS table.
 //   k_mfma_kq  the same product for m > 96: each wavefront takes 64 weight rows and one K
 //              quarter of every step for all 128 batch rows of the workgroup; the quarters'
-//              tiles are summed through LDS at the end.
+//              tiles are summed through LDS at the end (k_mfma_kq8: the same on 8-bit codes).
 //   k_encode8, k_dequant8, k_gemv<8, ...>, k_mfma2<8, ...>  the same on 8-bit codes.
 //   k_encode_uniform  codes of the asymmetric linear baseline (Sec. 2), for comparisons.
 //   k_gptq_panel, k_gptq_trail  GPTQ calibration with a fixed codebook (one wavefront per row
@@ -1255,6 +1255,171 @@ __global__ __launch_bounds__(512) void k_mfma_kq(const uint8_t* __restrict__ cod
   }
 }
 
+// ------------------------------------------------------------------ MFMA GEMM, K quarters, 8-bit
+//
+// k_mfma_kq on 8-bit codes: a workgroup of 8 wavefronts owns 128 weight rows x 128 batch rows;
+// wavefront w takes weight rows 64 (w % 2) .. +64 and the K quarter w / 2 of every step of 128 k,
+// for all eight batch tiles, so each weight is looked up once in the LDS table of float16 images
+// and feeds 8 MFMAs. Steps of 128 k (not 256) keep two activation slots (2 x 34 KiB) beside the
+// 64 KiB table. Lane (j, g) holds k = 128 step + 32 kq + 8 g + 0..7 of its rows (natural order,
+// 8 code bytes per row tile). After the last step the table and the slots are reused to sum the
+// four K quarters in a fixed order ((q0 + q2) + (q1 + q3)). Measured on MI355X against the
+// stepped kernel (8-bit, LDS table): 8192 -> 28672 at m = 128 / 256: 213.9 / 419.1 ->
+// 133.4 / 251.3 us; it has only N / 128 workgroups, so narrower layers stay stepped
+// (4096 -> 14336 at m = 128: 51.5 vs 70.5 us), and below m = 65 one stepped column wins
+// (m = 64: 112.9 vs 129.6 us).
+constexpr int kKq8Step = 128;
+constexpr int kKq8Pad = kKq8Step + 8;   // halves per staged activation row
+__global__ __launch_bounds__(512) void k_mfma_kq8(const uint8_t* __restrict__ codes,
+                                                  const uint16_t* __restrict__ x,
+                                                  float* __restrict__ y, int n_rows, int k_cols,
+                                                  int m_rows, float scale, Lut256 lut) {
+  constexpr int XV = 4;                  // 16-byte activation vectors per thread per step
+  constexpr int kTableBytes = kLutWords * 4;
+  constexpr int kSlotBytes = 128 * kKq8Pad * 2;
+  __shared__ __attribute__((aligned(16))) uint8_t s_mem[kTableBytes + 2 * kSlotBytes];
+  uint32_t* s_lut = reinterpret_cast<uint32_t*>(s_mem);
+  auto slot = [&](int u) { return reinterpret_cast<uint16_t*>(s_mem + kTableBytes + u * kSlotBytes); };
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int wave = t >> 6;
+  const int j = lane & 15;
+  const int g = lane >> 4;
+  const int wq = wave & 1;
+  const int kq = wave >> 1;
+  const uint32_t laneoff = (uint32_t)lane << 2;
+  const int nb = blockIdx.x * 128 + 64 * wq;
+  const int mb = blockIdx.y * 128;
+  const int nsteps = (k_cols + kKq8Step - 1) / kKq8Step;
+  GlobalU8 crow[4];
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) {
+    const int r = nb + 16 * rt + j;
+    crow[rt] = (GlobalU8)codes + (int64_t)(r < n_rows ? r : n_rows - 1) * k_cols;
+  }
+  auto load_x = [&](int step, u32x4 (&v)[XV]) {
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int idx = t + 512 * i;
+      const int m = mb + (idx >> 4);
+      const int kk = step * kKq8Step + (idx & 15) * 8;
+      const int mc = m < m_rows ? m : m_rows - 1;
+      const int kc = kk < k_cols ? kk : k_cols - 8;
+      v[i] = *(GlobalU32x4)((const __attribute__((address_space(1))) uint16_t*)x +
+                            (int64_t)mc * k_cols + kc);
+    }
+  };
+  auto store_x = [&](int step, int u, const u32x4 (&v)[XV]) {
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int idx = t + 512 * i;
+      const uint32_t keep = 0u - (uint32_t)((mb + (idx >> 4) < m_rows) &
+                                            (step * kKq8Step + (idx & 15) * 8 < k_cols));
+      u32x4 w = v[i];
+      w.x &= keep; w.y &= keep; w.z &= keep; w.w &= keep;
+      *reinterpret_cast<u32x4*>(slot(u) + (idx >> 4) * kKq8Pad + (idx & 15) * 8) = w;
+    }
+  };
+  // Codes of a step for row tile rt: 8 bytes of row nb + 16 rt + j at k = 128 step + 32 kq + 8 g
+  // (clamped into the row; a clamped piece only meets zero activations).
+  auto load_codes = [&](int step, u32x2 (&q)[4]) {
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      int64_t off = (int64_t)step * kKq8Step + 32 * kq + 8 * g;
+      off = off + 8 <= k_cols ? off : k_cols - 8;
+      q[rt] = *(GlobalU32x2)(crow[rt] + off);
+    }
+  };
+  float4v acc[8][4];
+#pragma unroll
+  for (int bt = 0; bt < 8; ++bt)
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[bt][rt][r] = 0.0f;
+
+  u32x2 q[2][4];
+  u32x4 xr[XV];
+  auto clampstep = [&](int t2) { return t2 < nsteps ? t2 : nsteps - 1; };
+  load_x(0, xr);
+  load_codes(0, q[0]);
+  fill_single_lut<512>(s_lut, lut);
+  store_x(0, 0, xr);
+  load_x(clampstep(1), xr);
+  __syncthreads();
+
+  for (int s0 = 0; s0 < nsteps; s0 += 2) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int step = s0 + u;
+      if (step >= nsteps) break;
+      load_codes(clampstep(step + 1), q[u ^ 1]);
+      half8v b[4];
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        const u32x4 bw{single_pair(s_lut, q[u][rt].x, laneoff, 0),
+                       single_pair(s_lut, q[u][rt].x, laneoff, 1),
+                       single_pair(s_lut, q[u][rt].y, laneoff, 0),
+                       single_pair(s_lut, q[u][rt].y, laneoff, 1)};
+        b[rt] = __builtin_bit_cast(half8v, bw);
+      }
+      const uint16_t* abase = slot(u) + j * kKq8Pad + 32 * kq + 8 * g;
+      half8v a_cur = *reinterpret_cast<const half8v*>(abase);
+#pragma unroll
+      for (int bt = 0; bt < 8; ++bt) {
+        half8v a_nxt = a_cur;
+        if (bt + 1 < 8) a_nxt = *reinterpret_cast<const half8v*>(abase + 16 * (bt + 1) * kKq8Pad);
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+          acc[bt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a_cur, b[rt], acc[bt][rt], 0, 0, 0);
+        a_cur = a_nxt;
+      }
+      store_x(step + 1, u ^ 1, xr);
+      load_x(clampstep(step + 2), xr);
+      __syncthreads();
+    }
+  }
+
+  // Sum the four K quarters through LDS (table and slots are free after the last barrier).
+  float* s_red = reinterpret_cast<float*>(s_mem);
+  static_assert(sizeof(s_mem) >= 4 * 8192 * sizeof(float), "reduction slots fit");
+  auto red_slot = [&](int w_q, int half) { return s_red + (size_t)(w_q * 2 + half) * 8192; };
+  auto put = [&](float* dst) {
+#pragma unroll
+    for (int bt = 0; bt < 8; ++bt)
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+        *reinterpret_cast<float4v*>(dst + ((bt * 4 + rt) * 64 + lane) * 4) = acc[bt][rt];
+  };
+  auto add = [&](const float* src) {
+#pragma unroll
+    for (int bt = 0; bt < 8; ++bt)
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+        acc[bt][rt] += *reinterpret_cast<const float4v*>(src + ((bt * 4 + rt) * 64 + lane) * 4);
+  };
+  if (kq >= 2) put(red_slot(wq, kq - 2));
+  __syncthreads();
+  if (kq < 2) add(red_slot(wq, kq));
+  __syncthreads();
+  if (kq == 1) put(red_slot(wq, 0));
+  __syncthreads();
+  if (kq == 0) {
+    add(red_slot(wq, 0));
+#pragma unroll
+    for (int bt = 0; bt < 8; ++bt)
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        const int row = nb + 16 * rt + j;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb + 16 * bt + 4 * g + r;
+          if (m < m_rows && row < n_rows) y[(int64_t)m * n_rows + row] = acc[bt][rt][r] * scale;
+        }
+      }
+  }
+}
+
 // ------------------------------------------------------------------ split-K MFMA, m <= 16
 //
 // For T batch tiles of 16 rows (T = 1 for m <= 16, T = 2 for m <= 32) and K = 32 W ND KS (W
@@ -2036,6 +2201,19 @@ int32_t launch_sk8(const uint16_t* x, int M, int K, const LinearJob& j, hipStrea
   return launch_status();
 }
 
+// K-quartered MFMA path on 8-bit codes: m > 64 at N >= 16384.
+bool kq8_shape(int M, int64_t N) { return M > 64 && N >= 16384; }
+
+int32_t launch_kq8(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st) {
+  Lut256 lut;
+  float scale;
+  make_lut<8>(j.codebook, &lut, &scale);
+  const int N = (int)j.n;
+  dim3 grid((unsigned)((N + 127) / 128), (unsigned)((M + 127) / 128));
+  hipLaunchKernelGGL(k_mfma_kq8, grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, scale, lut);
+  return launch_status();
+}
+
 // K-quartered MFMA path (4-bit, sign-symmetric codebooks): m > 96 at N >= 4096.
 bool kq_shape(int M, int64_t N) { return M > 96 && N >= 4096; }
 
@@ -2188,6 +2366,7 @@ int choose_path(int M, int K, int64_t N) {
       !(M >= (BITS == 8 ? 5 : 3) && (int64_t)M * N > 65536))
     return LOGBQ_PATH_GEMV;
   if (BITS == 4 && kq_shape(M, N)) return LOGBQ_PATH_MFMA_KQ;
+  if (BITS == 8 && kq8_shape(M, N)) return LOGBQ_PATH_MFMA_KQ;
   return LOGBQ_PATH_MFMA;
 }
 
@@ -2231,7 +2410,7 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
       gl[ng++] = live[a];
       grows += j.n;
     } else if (path == LOGBQ_PATH_MFMA_KQ) {
-      const int32_t r = launch_kq(x, M, K, j, st);
+      const int32_t r = BITS == 8 ? launch_kq8(x, M, K, j, st) : launch_kq(x, M, K, j, st);
       if (r != LOGBQ_OK) return r;
     } else {
       const int32_t r = launch_mfma<BITS>(x, M, K, j, st);
@@ -2700,6 +2879,8 @@ int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const
       const int nbuf = (cpl <= 2 && M <= 2) ? 3 : 2;
       std::snprintf(buf, sizeof(buf), "k_gemv<%d, %d, %d, %s, %d>", bits, M, cpl,
                     wk > 1 ? "true" : "false", nbuf);
+    } else if (path == LOGBQ_PATH_MFMA_KQ && bits == 8) {
+      std::snprintf(buf, sizeof(buf), "k_mfma_kq8");
     } else if (path == LOGBQ_PATH_MFMA_KQ && symmetric) {
       std::snprintf(buf, sizeof(buf), "k_mfma_kq");
     } else {

@@ -254,7 +254,9 @@ def test_linear_path_rule():
     assert lp(4, 96, 8192, 28672) == "mfma"
     # K-quartered MFMA GEMM: 4-bit, m > 96 at N >= 4096
     assert lp(4, 128, 8192, 28672) == "mfma_kq" and lp(4, 97, 1024, 4096) == "mfma_kq"
-    assert lp(4, 128, 1024, 4095) == "mfma" and lp(8, 128, 8192, 28672) == "mfma"
+    assert lp(4, 128, 1024, 4095) == "mfma" and lp(8, 128, 8192, 28672) == "mfma_kq"
+    assert lp(8, 65, 8192, 16384) == "mfma_kq" and lp(8, 64, 8192, 28672) == "mfma"
+    assert lp(8, 128, 4096, 14336) == "mfma"
     # 8-bit codes: split-K for K in {2, 4, 8} Ki at 5 <= m <= 8 (not N <= 1024 at K >= 4096),
     # m = 3, 4 from N = 8192, 9 <= m <= 16 (not N > 16384 at K = 8192); else GEMV unless m >= 5
     # and m * N > 65536, else the stepped MFMA kernel
@@ -289,7 +291,7 @@ def test_linear_kernel_names():
     assert lk(4, 32, 8192, 28672) == "k_mfma2<4, 2, 4, false, true>"
     assert lk(4, 128, 8192, 28672) == "k_mfma_kq"
     assert lk(8, 1, 8192, 28672) == "k_gemv<8, 1, 8, false, 2>"
-    assert lk(8, 128, 8192, 28672) == "k_mfma2<8, 4, 4, true, false>"
+    assert lk(8, 128, 8192, 28672) == "k_mfma_kq8" and lk(8, 128, 4096, 14336) == "k_mfma2<8, 4, 4, true, false>"
     assert lk(8, 8, 8192, 28672) == "k_mfma_sk8<16, 2>" and lk(8, 12, 4096, 4096) == "k_mfma_sk8<8, 1>"
     assert lk(4, 0, 8192, 28672) == "none" and lk(4, 3, 0, 5) == "k_fill_zero"
     # a codebook that is not sign-symmetric takes the LDS table

@@ -339,6 +339,32 @@ def test_linear8_split_k():
     assert L.linear_path(8, 8, 8192, 3001) == "splitk" and L.linear_path(8, 16, 2048, 20001) == "splitk"
 
 
+def test_linear8_k_quartered():
+    """The 8-bit K-quartered kernel (m > 64 at N >= 16384): a partial last 128-row workgroup,
+    K not a multiple of its 128-k step, batch rows past the last full tile and two workgroup
+    rows, a fitted and an arbitrary codebook; y prefilled with NaN, two calls bit-equal."""
+    rng = np.random.default_rng(43)
+    for n, k in ((16400, 1056), (16384, 4096)):
+        w, p, r = prepare(n, k, [18, 43, k % 1000, 0])
+        codes, cb = gpu_encode(w, p)
+        wh = oracle_w_hat(w, r)
+        cb2 = rng.standard_normal(256).astype(np.float32)
+        wh2 = O.dequantize(codes.cpu().numpy(), cb2)
+        for m in ((65, 100, 129) if k == 1056 else (128,)):
+            assert L.linear_path(8, m, k, n) == "mfma_kq"
+            _say(f"linear8 K-quartered n={n} k={k} m={m}")
+            x = inputs.activations(m, k, seed=[18, 43, k % 1000, m])
+            xd = torch.from_numpy(x).to(DEV)
+            for book, ref, bar in ((cb, wh, 2.5e-4), (cb2, wh2, TOL)):
+                y = torch.full((m, n), float("nan"), dtype=torch.float32, device=DEV)
+                L.linear8(xd, codes, book, out=y)
+                y2 = L.linear8(xd, codes, book)
+                torch.cuda.synchronize()
+                assert torch.isfinite(y).all()
+                assert torch.equal(y, y2)
+                assert rel_err(y.cpu().numpy(), x, ref) <= bar, (n, k, m)
+
+
 # ---------------------------------------------------------------- full-size, sampled
 
 def test_full_size_layer8_8192x28672_sampled():
