@@ -112,31 +112,51 @@ def _capture(torch, L, launches, count, offset=0):
 WARM_CHUNK = 1000   # launches per captured warmup graph
 
 
-def time_launches(torch, L, stream, launches, steps, warmup):
-    """Time exactly `steps` logbq_linear launches back to back after `warmup` untimed ones.
-    `launches` is a list of (x, codes, cb, y); launch i uses entry i % len(launches). The
-    launches are captured in HIP graphs so that host launch cost cannot starve the GPU. All
-    graphs are captured first; the warmup graphs are then replayed and the timed graph follows
-    them on the same stream with no host synchronisation in between, so the timed launches run
-    on a GPU that has been busy for the whole warmup (its clocks have ramped up) instead of
-    after an idle gap. Returns ms per launch."""
-    full, rest = divmod(warmup, WARM_CHUNK)
-    warm = _capture(torch, L, launches, WARM_CHUNK) if full else None
-    warm_rest = _capture(torch, L, launches, rest) if rest else None
-    timed = _capture(torch, L, launches, steps, offset=warmup)
+def time_chain(torch, L, stream, rows):
+    """Time several logbq_linear launch sequences back to back on one stream. `rows` is a list
+    of (launches, steps, warmup): `launches` a list of (x, codes, cb, y), launch i of a row
+    using entry i % len(launches); each row takes `warmup` untimed launches and then exactly
+    `steps` timed ones between two events. The launches are captured in HIP graphs so that
+    host launch cost cannot starve the GPU. All graphs are captured first; the rows are then
+    replayed in order with no host synchronisation in between (one synchronisation after the
+    last), so every row's timed launches run on a GPU that has been busy since the first
+    row started, instead of after an idle gap in which its clocks drop. Returns ms per launch
+    for each row."""
+    plans = []
+    for launches, steps, warmup in rows:
+        full, rest = divmod(warmup, WARM_CHUNK)
+        warm = _capture(torch, L, launches, WARM_CHUNK) if full else None
+        warm_rest = _capture(torch, L, launches, rest) if rest else None
+        timed = _capture(torch, L, launches, steps, offset=warmup)
+        plans.append((full, warm, warm_rest, timed, steps))
     torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    events = []
     with torch.cuda.stream(stream):
-        for _ in range(full):
-            warm.replay()
-        if warm_rest is not None:
-            warm_rest.replay()
-        e0.record(stream)
-        timed.replay()
-        e1.record(stream)
+        for full, warm, warm_rest, timed, steps in plans:
+            for _ in range(full):
+                warm.replay()
+            if warm_rest is not None:
+                warm_rest.replay()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            timed.replay()
+            e1.record(stream)
+            events.append((e0, e1, steps))
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / steps
+    return [e0.elapsed_time(e1) / steps for e0, e1, steps in events]
+
+
+def time_launches(torch, L, stream, launches, steps, warmup):
+    """time_chain for one row: ms per launch of exactly `steps` launches after `warmup`."""
+    return time_chain(torch, L, stream, [(launches, steps, warmup)])[0]
+
+
+def aux_counts(steps, warmup):
+    """Timed and warmup launches of a row other than the headline: at least 500 of each
+    whatever --steps / --warmup ask for the headline (64 launches after one warmup launch ran
+    7-17 % slower than the same rows timed over 500)."""
+    return max(500, steps // 4), max(500, warmup // 4)
 
 
 def make_tensor(torch, L, inputs, lin, wl, seed, dev):
@@ -200,21 +220,32 @@ def bench_layer(torch, L, inputs, dev, stream, ms, steps, warmup, with_encode=Tr
                                         "hbm_frac": enc_bytes / enc_ms / 1e6 / HBM_PEAK_GBS,
                                         "bytes": enc_bytes}
     del wd
-    for m in ms:
+    # The other batch sizes first, the headline (ms[0]) last, all back to back on one stream:
+    # the headline's warmup launches start on a GPU that is already at its working clocks.
+    order = list(ms[1:]) + [ms[0]]
+    aux_steps, aux_warm = aux_counts(steps, warmup)
+    plan = []
+    for m in order:
         x = inputs.activations(m, k, seed=[wl["cfg"], 0, 0, 1], device=dev)
         launches = [(x, c, cb, torch.empty((m, n), dtype=torch.float32, device=dev))
                     for c in code_list]
-        timed = steps if m == ms[0] else max(64, steps // 4)
-        t = time_launches(torch, L, stream, launches, timed, warmup if m == ms[0] else warmup // 4)
+        plan.append((launches, steps, warmup) if m == ms[0] else (launches, aux_steps, aux_warm))
+    times = time_chain(torch, L, stream, plan)
+    for m, (_, timed, warm), t in sorted(zip(order, plan, times), key=lambda r: ms.index(r[0])):
         log(f"layer m={m}: {t * 1e3:.2f} us per launch")
         algo = packed + 2 * m * k + 4 * m * n + 64
         flops = 2.0 * m * n * k
         results[f"linear_8192x28672_m{m}"] = {
-            "ms": t, "us": t * 1e3, "launches_timed": timed, "weight_GB_s": packed / t / 1e6,
+            "ms": t, "us": t * 1e3, "launches_timed": timed, "warmup_launches": warm,
+            "weight_GB_s": packed / t / 1e6,
             "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
             "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
             "algo_bytes": algo,
             "path": L.linear_path(4, m, k, n), "kernel": L.linear_kernel(4, m, k, n, cb)}
+        if m == ms[0] and len(ms) > 1:
+            results[f"linear_8192x28672_m{m}"]["preceded_by"] = (
+                "the m = " + ", ".join(str(v) for v in ms[1:]) + " rows on the same stream "
+                "with no host synchronisation in between")
     return results, {"n": n, "k": k, "packed": packed, "copies": copies, "fit_s": fit_s,
                      "params": {"base": p.base, "shift": p.shift, "wmin": p.wmin,
                                 "wmax": p.wmax}}, codes, cb
@@ -260,12 +291,14 @@ def bench_quality(torch, L, inputs, dev, stream, layer_codes, layer_cb, steps, w
             packed = lin.n * lin.k // 2
             copies = max(2, -(-ROTATE_BYTES // packed))
             code_list = [ucodes] + [ucodes.clone() for _ in range(copies - 1)]
+            aux_steps, aux_warm = aux_counts(steps, warmup)
+            plan = []
             for m in (1, 8, 32):
                 xm = inputs.activations(m, lin.k, seed=[wl["cfg"], 0, 0, 1], device=dev)
                 launches = [(xm, c, ucb, torch.empty((m, lin.n), dtype=torch.float32, device=dev))
                             for c in code_list]
-                t = time_launches(torch, L, stream, launches, steps if m == 1 else max(64, steps // 4),
-                                  warmup if m == 1 else warmup // 4)
+                plan.append((launches, aux_steps, aux_warm))
+            for m, t in zip((1, 8, 32), time_chain(torch, L, stream, plan)):
                 row["uniform"][f"linear_m{m}_us"] = t * 1e3
                 row["uniform"][f"linear_m{m}_path"] = L.linear_path(4, m, lin.k, lin.n)
             del code_list
@@ -381,12 +414,16 @@ def bench_layer8(torch, L, inputs, dev, stream, ms, steps, warmup):
                                       "bytes": enc_bytes}}
     copies = max(2, -(-ROTATE_BYTES // nbytes))
     code_list = [codes] + [codes.clone() for _ in range(copies - 1)]
+    aux_steps, aux_warm = aux_counts(steps, warmup)
+    plan = []
     for m in ms:
         x = inputs.activations(m, k, seed=[wl["cfg"], 0, 0, 1], device=dev)
         launches = [(x, c, cb, torch.empty((m, n), dtype=torch.float32, device=dev))
                     for c in code_list]
-        timed = steps if m == ms[0] else max(64, steps // 4)
-        t = time_launches(torch, L, stream, launches, timed, warmup if m == ms[0] else warmup // 4)
+        plan.append((launches, aux_steps, aux_warm))
+    times = time_chain(torch, L, stream, plan)
+    for m, t in zip(ms, times):
+        timed = aux_steps
         log(f"layer8 m={m}: {t * 1e3:.2f} us per launch")
         algo = nbytes + 2 * m * k + 4 * m * n + 1024
         flops = 2.0 * m * n * k

@@ -346,6 +346,36 @@ def test_linear_split_k_two_tiles():
                 assert torch.equal(yg, y1)
 
 
+def test_linear_split_k_14336():
+    """Split-K at K = 14336 on 4099 rows (257 blocks of 16, so a workgroup pair takes two or
+    three blocks and the last block has 3 rows): workgroup pairs of 14 wavefronts add their K
+    halves into y with float atomics after zeroing it, with two batch groups. y is prefilled
+    with NaN (every output must be overwritten), each call is repeated and must give the same
+    bits, and a grouped call (4099 and the first 4096 rows) equals single calls."""
+    n, k = 4099, 14336
+    w, p, r = prepare(n, k, [8, 23, 1, 0])
+    c, cb = gpu_encode(w, p)
+    wh = O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
+    del w
+    c2 = c[:4096]
+    for m in (3, 4, 5, 8):
+        assert L.linear_path(4, m, k, n) == "splitk" and L.linear_path(4, m, k, 4096) == "splitk"
+        _say(f"split-K k={k} m={m} kernel {L.linear_kernel(4, m, k, n)}")
+        x = inputs.activations(m, k, seed=[8, 23, 2, m])
+        xd = torch.from_numpy(x).to(DEV)
+        y = torch.full((m, n), float("nan"), dtype=torch.float32, device=DEV)
+        L.linear(xd, c, cb, out=y)
+        y2 = L.linear(xd, c, cb)
+        torch.cuda.synchronize()
+        assert torch.isfinite(y).all()
+        assert torch.equal(y, y2)
+        assert rel_err(y.cpu().numpy(), x, wh) <= 2.5e-4
+        ys = L.linear_multi(xd, [c, c2], [cb, cb])
+        y3 = L.linear(xd, c2, cb)
+        torch.cuda.synchronize()
+        assert torch.equal(ys[0], y) and torch.equal(ys[1], y3)
+
+
 def test_linear_multi_matches_single_launches():
     """Grouped launch of linears sharing x: every output equals the single-linear call bit for
     bit, and the oracle within tolerance (qkv-like and gate/up-like groups, ragged sizes)."""
