@@ -203,8 +203,8 @@ int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t*
  * activations (the query / key / value projections of a decoder layer, or its gate and up
  * projections), with one launch for the linears that take the GEMV in the same configuration
  * (wavefronts per row and chunks per lane, chosen from m, k and the linear's n) and one for
- * those that take the split-K kernel (when their codebooks are sign-symmetric) (Sec. 3.3
- * lookup + product).
+ * those that take the split-K kernel in the same configuration (chosen from m, k and the
+ * linear's n, when their codebooks are sign-symmetric) (Sec. 3.3 lookup + product).
  *   x_dev, m, k : as logbq_linear; every W_i has k in features.
  *   count       : number of linears, 1..4.
  *   codes_dev   : host array of count device pointers, [n[i]][k/2] packed codes each.

@@ -2236,8 +2236,17 @@ bool sk_shape(int M, int K) {
 
 // Split-K configuration: code dwords per lane and row, wavefronts per workgroup, batch groups,
 // batch tiles and K parts (workgroups per block).
-struct SkConfig { int nd, waves, groups, tiles, kparts; };
-SkConfig sk_config(int M, int K, bool pairs) {
+struct SkConfig {
+  int nd, waves, groups, tiles, kparts;
+  bool operator==(const SkConfig& o) const {
+    return nd == o.nd && waves == o.waves && groups == o.groups && tiles == o.tiles &&
+           kparts == o.kparts;
+  }
+};
+// The configuration of one linear of `blocks` 16-row blocks. It depends only on (m, K, blocks)
+// and the codebook's kind, so a grouped launch only joins linears of equal configuration and
+// each computes as in a call of its own.
+SkConfig sk_config(int M, int K, bool pairs, int blocks) {
   // K = 14336 = 2 x 14 x 512: workgroup pairs of 14 wavefronts, one K half each.
   if (K == 14336) return {16, 14, 2, 1, 2};
   if (M > 16) {   // two batch tiles (register tables only); K = 8192 over workgroup pairs
@@ -2245,14 +2254,24 @@ SkConfig sk_config(int M, int K, bool pairs) {
     const int kparts = K == 8192 ? 2 : 1;
     return {K / (32 * waves * kparts), waves, 1, 2, kparts};
   }
+  // Narrow layers: one workgroup per block leaves CUs idle, and above m = 8 a lane's
+  // activations for all of K take 64 VGPRs; there the K halves go to workgroup pairs
+  // (ND = K / 1024). Measured on MI355X (graph replay, codes streamed from HBM), K = 8192:
+  // N = 2048 at m = 4 / 8 / 16: 7.27 / 8.52 / 12.52 -> 6.79 / 7.23 / 9.17 us; N = 8192 at
+  // m = 12 / 16: 14.32 / 15.80 -> 13.74 / 14.60 us; slower at m <= 8 from N = 3072 on (mixed
+  // to N = 6144) and at N >= 14336. K = 4096 gains only above m = 12 at N <= 2048 (N = 1024 at
+  // m = 16: 7.08 -> 6.41 us).
+  if (!pairs && ((K == 8192 && blocks <= (M <= 8 ? 128 : 512)) ||
+                 (K == 4096 && M > 12 && blocks <= 128)))
+    return {K / 1024, 16, M <= 8 ? 2 : 1, 1, 2};
   const int waves = (!pairs && K >= 4096) ? 16 : 8;
   return {K / (32 * waves), waves, (!pairs && M <= 8) ? 2 : 1, 1, 1};
 }
 
-// Split-K launches for the linears jobs[idx[0..count)] of one call: one grouped launch when
-// every codebook is sign-symmetric (register dequantization), otherwise one launch per linear
-// (above m = 16, and at K = 14336, a codebook that is not sign-symmetric takes the stepped MFMA
-// kernel).
+// Split-K launches for the linears jobs[idx[0..count)] of one call: when every codebook is
+// sign-symmetric (register dequantization), one grouped launch per distinct configuration,
+// otherwise one launch per linear (above m = 16, and at K = 14336, a codebook that is not
+// sign-symmetric takes the stepped MFMA kernel).
 int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const int* idx,
                   int count, hipStream_t st, int cus) {
   SkSegs segs;
@@ -2270,9 +2289,8 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     all_symmetric = make_lut_bytes(j.codebook, &sg.tb, &sg.scale) && all_symmetric;
     total += (int)((j.n + 15) / 16);
   }
-  auto launch = [&](int nseg, const SkSegs& sgs, int nblocks, bool pairs,
-                    const Lut16& l) -> int32_t {
-    const SkConfig c = sk_config(M, K, pairs);
+  auto launch = [&](int nseg, const SkSegs& sgs, int nblocks, bool pairs, const Lut16& l,
+                    const SkConfig& c) -> int32_t {
     // One workgroup per CU (the grid walks the blocks); with two K parts an even grid of
     // workgroup pairs, after zeroing every output the atomic adds will land on.
     int grid = nblocks * c.kparts < cus ? nblocks * c.kparts : cus;
@@ -2298,11 +2316,34 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     LOGBQ_SK(16, 16, 1, 1, 1, false) LOGBQ_SK(16, 16, 2, 1, 1, false)
     LOGBQ_SK(4, 8, 1, 2, 1, false) LOGBQ_SK(4, 16, 1, 2, 1, false)
     LOGBQ_SK(8, 16, 1, 2, 1, false) LOGBQ_SK(8, 16, 1, 2, 2, false)
-    LOGBQ_SK(16, 14, 2, 1, 2, false)
+    LOGBQ_SK(16, 14, 2, 1, 2, false) LOGBQ_SK(8, 16, 2, 1, 2, false)
+    LOGBQ_SK(8, 16, 1, 1, 2, false) LOGBQ_SK(4, 16, 1, 1, 2, false)
 #undef LOGBQ_SK
     return LOGBQ_ERR_UNSUPPORTED;
   };
-  if (all_symmetric) return launch(count, segs, total, false, lut);
+  if (all_symmetric) {
+    SkConfig cfg[kMaxSegs];
+    bool done[kMaxSegs] = {};
+    for (int a = 0; a < count; ++a)
+      cfg[a] = sk_config(M, K, false, (int)((jobs[idx[a]].n + 15) / 16));
+    for (int a0 = 0; a0 < count; ++a0) {
+      if (done[a0]) continue;
+      SkSegs grp;
+      std::memset(&grp, 0, sizeof(grp));
+      int nseg = 0, blocks = 0;
+      for (int a = a0; a < count; ++a)
+        if (!done[a] && cfg[a] == cfg[a0]) {
+          grp.s[nseg] = segs.s[a];
+          grp.s[nseg].blk_begin = blocks;
+          blocks += (int)((jobs[idx[a]].n + 15) / 16);
+          ++nseg;
+          done[a] = true;
+        }
+      const int32_t r = launch(nseg, grp, blocks, false, lut, cfg[a0]);
+      if (r != LOGBQ_OK) return r;
+    }
+    return LOGBQ_OK;
+  }
   for (int a = 0; a < count; ++a) {
     const LinearJob& j = jobs[idx[a]];
     SkSegs one;
@@ -2313,9 +2354,11 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     // table for any other.
     const bool symmetric = make_lut_bytes(j.codebook, &one.s[0].tb, &one.s[0].scale);
     make_lut16(j.codebook, &lut, &one.s[0].scale);
+    const int blocks = (int)((j.n + 15) / 16);
     const int32_t r = ((M > 16 || K == 14336) && !symmetric)
                           ? launch_mfma<4>(x, M, K, j, st)
-                          : launch(1, one, (int)((j.n + 15) / 16), !symmetric, lut);
+                          : launch(1, one, blocks, !symmetric, lut,
+                                   sk_config(M, K, !symmetric, blocks));
     if (r != LOGBQ_OK) return r;
   }
   return LOGBQ_OK;
@@ -2869,7 +2912,7 @@ int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const
     if (path == LOGBQ_PATH_SPLITK && bits == 8) {
       std::snprintf(buf, sizeof(buf), "k_mfma_sk8<%d, %d>", K / 512, M <= 8 ? 2 : 1);
     } else if (path == LOGBQ_PATH_SPLITK && ((M <= 16 && K != 14336) || symmetric)) {
-      const SkConfig c = sk_config(M, K, !symmetric);
+      const SkConfig c = sk_config(M, K, !symmetric, (int)((n + 15) / 16));
       std::snprintf(buf, sizeof(buf), "k_mfma_sk<%d, %d, %d, %d, %d, %s>", c.nd, c.waves,
                     c.groups, c.tiles, c.kparts, symmetric ? "false" : "true");
     } else if (path == LOGBQ_PATH_GEMV) {

@@ -288,6 +288,13 @@ def test_linear_kernel_names():
     assert lk(4, 32, 8192, 2048) == "k_mfma_sk<8, 16, 1, 2, 2, false>"    # K over 2 workgroups
     assert lk(4, 32, 1024, 4096) == "k_mfma_sk<4, 8, 1, 2, 1, false>"
     assert lk(4, 4, 14336, 4096) == "k_mfma_sk<16, 14, 2, 1, 2, false>"   # K over 2 workgroups
+    # narrow layers split K over workgroup pairs (per linear, from its own n)
+    assert lk(4, 4, 8192, 2048) == "k_mfma_sk<8, 16, 2, 1, 2, false>"
+    assert lk(4, 8, 8192, 2049) == "k_mfma_sk<16, 16, 2, 1, 1, false>"
+    assert lk(4, 16, 8192, 8192) == "k_mfma_sk<8, 16, 1, 1, 2, false>"
+    assert lk(4, 16, 8192, 8193) == "k_mfma_sk<16, 16, 1, 1, 1, false>"
+    assert lk(4, 16, 4096, 2048) == "k_mfma_sk<4, 16, 1, 1, 2, false>"
+    assert lk(4, 12, 4096, 2048) == "k_mfma_sk<8, 16, 1, 1, 1, false>"
     assert lk(4, 32, 8192, 28672) == "k_mfma2<4, 2, 4, false, true>"
     assert lk(4, 128, 8192, 28672) == "k_mfma_kq"
     assert lk(8, 1, 8192, 28672) == "k_gemv<8, 1, 8, false, 2>"

@@ -346,6 +346,41 @@ def test_linear_split_k_two_tiles():
                 assert torch.equal(yg, y1)
 
 
+def test_linear_split_k_pairs_narrow():
+    """Narrow layers split K over workgroup pairs (float atomic adds onto a zeroed y), chosen
+    per linear from its own row count: K = 8192 with 2047 rows (128 blocks) at m <= 8 and up
+    to 8192 rows above m = 8, K = 4096 above m = 12 with up to 2048 rows. y is prefilled with
+    NaN, each call is repeated and must give the same bits. A grouped call equals single calls
+    when its linears take different configurations (m = 8: 2047 rows split, 5000 rows not; two
+    launches) and when they share one (m = 12: both split, one launch)."""
+    cases = {8192: (2047, 5000), 4096: (1000,)}
+    for k, ns in cases.items():
+        tensors = [prepare(n, k, [8, 24, k % 1000, j]) for j, n in enumerate(ns)]
+        codes = [gpu_encode(w, p) for w, p, r in tensors]
+        whs = [O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
+               for w, p, r in tensors]
+        del tensors
+        for m in ((4, 5, 8, 9, 12, 16) if k == 8192 else (13, 16)):
+            x = inputs.activations(m, k, seed=[8, 24, k % 1000, m])
+            xd = torch.from_numpy(x).to(DEV)
+            for (c, cb), wh, n in zip(codes, whs, ns):
+                assert L.linear_path(4, m, k, n) == "splitk"
+                _say(f"split-K narrow k={k} n={n} m={m} kernel {L.linear_kernel(4, m, k, n)}")
+                y = torch.full((m, n), float("nan"), dtype=torch.float32, device=DEV)
+                L.linear(xd, c, cb, out=y)
+                y2 = L.linear(xd, c, cb)
+                torch.cuda.synchronize()
+                assert torch.isfinite(y).all()
+                assert torch.equal(y, y2)
+                assert rel_err(y.cpu().numpy(), x, wh) <= 2.5e-4
+            if len(codes) > 1:
+                ys = L.linear_multi(xd, [c for c, _ in codes], [cb for _, cb in codes])
+                for (c, cb), yg in zip(codes, ys):
+                    y1 = L.linear(xd, c, cb)
+                    torch.cuda.synchronize()
+                    assert torch.equal(yg, y1)
+
+
 def test_linear_split_k_14336():
     """Split-K at K = 14336 on 4099 rows (257 blocks of 16, so a workgroup pair takes two or
     three blocks and the last block has 3 rows): workgroup pairs of 14 wavefronts add their K
