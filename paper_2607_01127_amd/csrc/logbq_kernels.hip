@@ -14,9 +14,9 @@
 //              as the A operand; float32 accumulation in the MFMA.
 //   k_mfma_sk  the same product for 2 <= m <= 32 split over K: the 8 or 16 wavefronts of a
 //              workgroup share a block of 16 rows (one K slice each, activations held in
-//              registers) and sum their partial tiles through LDS; at K = 8192 and m > 16, and
-//              at K = 14336, two workgroups share a block (one K half each) and add into a
-//              zeroed y.
+//              registers) and sum their partial tiles through LDS; at K = 8192 and m > 16, on
+//              narrow layers, and at K = 14336, two workgroups share a block (one K half each)
+//              and add into a zeroed y.
 //   k_mfma_sk8 the split-K product on 8-bit codes (m <= 16), weights looked up in an LDS table.
 //   k_mfma_kq  the same product for m > 96: each wavefront takes 64 weight rows and one K
 //              quarter of every step for all 128 batch rows of the workgroup; the quarters'
