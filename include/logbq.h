@@ -186,14 +186,16 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  * k in {1024, 2048, 4096, 8192} (and m <= 8 at k = 14336; there, as above m = 16, only for
  * sign-symmetric codebooks), a split-K dequantize-into-MFMA kernel takes 5 <= m <= 16,
  * m = 4 unless n <= 1024 at k = 8192, m = 3 at n >= 4096, and 17 <= m <= 32 unless m > 20 at
- * k = 8192 and n > 16384 (above m = 16 only for sign-symmetric codebooks; at k = 8192 it first
- * zeroes y and two workgroups add their halves of K into each output); otherwise the
- * wavefront-reduced GEMV runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and
- * shapes whose activations do not fit the GEMV's registers) runs the stepped
- * dequantize-into-MFMA skinny GEMM, except m > 96 at n >= 4096, which runs a K-quartered
- * MFMA GEMM for sign-symmetric codebooks. logbq_linear_path reports the choice. Results are
- * deterministic for every path. k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED
- * (k % 32, alignment), HIP.
+ * k = 8192 and n > 16384 (above m = 16 only for sign-symmetric codebooks; at k = 8192 above
+ * m = 16, and for sign-symmetric codebooks on narrow layers -- k = 8192 with n <= 2048 up to
+ * m = 8 and n <= 8192 above, k = 4096 with n <= 2048 above m = 12 -- it first zeroes y and two
+ * workgroups add their halves of K into each output); otherwise the wavefront-reduced GEMV
+ * runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and shapes whose
+ * activations do not fit the GEMV's registers) runs the stepped dequantize-into-MFMA skinny
+ * GEMM, except m > 96 at n >= 4096, which runs a K-quartered MFMA GEMM for sign-symmetric
+ * codebooks. logbq_linear_path reports the choice. Results are deterministic for every path.
+ * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment, or k >= 2^24 on
+ * the stepped or K-quartered MFMA kernel), HIP.
  */
 int32_t logbq_linear(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,
                      int64_t n, const float* codebook, float* y_dev, void* stream);

@@ -924,8 +924,16 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
   const int mb = blockIdx.y * (MT * 16);
   const int nsteps = (k_cols + kM2Step - 1) / kM2Step;
   const int64_t row_bytes = (int64_t)k_cols * BITS / 8;
+  // One buffer descriptor over the workgroup's 128 rows (rows past n_rows read as zeros and
+  // are not stored). Buffer loads keep the code prefetch where it is issued: plain loads of
+  // the read-only codes were moved by the compiler next to their use.
+  const int band0 = blockIdx.x * 128;
+  const int band_rows = n_rows - band0 < 128 ? n_rows - band0 : 128;
+  const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(codes + (int64_t)band0 * row_bytes), (short)0, (int)(band_rows * row_bytes),
+      kBufferRsrcWord3);
   const int row = n0 + j;
-  const GlobalU8 crow = (GlobalU8)codes + (int64_t)(row < n_rows ? row : n_rows - 1) * row_bytes;
+  const int crow = (wave * 16 + j) * (int)row_bytes;   // this lane's row in the descriptor
 
   // Activation tile of a step: MT*16 rows x 256 halves = MT*512 vectors of 16 bytes, MT per
   // thread. Loads are clamped in bounds; entries past m_rows / k_cols are zeroed when written.
@@ -964,16 +972,15 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
 #pragma unroll
     for (int c = 0; c < CB; ++c) {
       if (COAL) {
-        int r = n0 + RPI * c + lane / (RB / 16);
-        r = r < n_rows ? r : n_rows - 1;
-        int64_t off = (int64_t)step * RB + 16 * (lane % (RB / 16));
-        off = off + 16 <= row_bytes ? off : row_bytes - 16;
-        q[c] = __builtin_nontemporal_load(
-            (GlobalU32x4)((GlobalU8)codes + (int64_t)r * row_bytes + off));
+        const int r = wave * 16 + RPI * c + lane / (RB / 16);
+        int off = step * RB + 16 * (lane % (RB / 16));
+        off = off + 16 <= (int)row_bytes ? off : (int)row_bytes - 16;
+        q[c] = __builtin_amdgcn_raw_buffer_load_b128(crs, r * (int)row_bytes + off, 0,
+                                                     kCachePolicyNT);
       } else {
-        int64_t off = (int64_t)step * RB + (RB / 4) * g + 16 * c;
-        off = off + 16 <= row_bytes ? off : row_bytes - 16;
-        q[c] = __builtin_nontemporal_load((GlobalU32x4)(crow + off));
+        int off = step * RB + (RB / 4) * g + 16 * c;
+        off = off + 16 <= (int)row_bytes ? off : (int)row_bytes - 16;
+        q[c] = __builtin_amdgcn_raw_buffer_load_b128(crs, crow + off, 0, kCachePolicyNT);
       }
     }
   };
@@ -1117,12 +1124,18 @@ __global__ __launch_bounds__(512) void k_mfma_kq(const uint8_t* __restrict__ cod
   const int mb = blockIdx.y * 128;
   const int nsteps = (k_cols + kM2Step - 1) / kM2Step;
   const int64_t row_bytes = (int64_t)k_cols / 2;
-  GlobalU8 crow[4];
+  // One buffer descriptor over the workgroup's 128 rows (rows past n_rows read as zeros; their
+  // results are not stored). Buffer loads keep their place in the program: plain loads of the
+  // read-only codes were moved by the compiler next to their use, past the barrier that ends
+  // the step before, which took away the one-step prefetch.
+  const int band0 = blockIdx.x * 128;
+  const int band_rows = n_rows - band0 < 128 ? n_rows - band0 : 128;
+  const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(codes + (int64_t)band0 * row_bytes), (short)0, (int)(band_rows * row_bytes),
+      kBufferRsrcWord3);
+  int crow[4];
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt) {
-    const int r = nb + 16 * rt + j;
-    crow[rt] = (GlobalU8)codes + (int64_t)(r < n_rows ? r : n_rows - 1) * row_bytes;
-  }
+  for (int rt = 0; rt < 4; ++rt) crow[rt] = (64 * wq + 16 * rt + j) * (int)row_bytes;
   // Activation tile: as k_mfma2 (clamped loads; rows past m_rows and k past k_cols are zeroed
   // when written to LDS).
   auto load_x = [&](int step, u32x4 (&v)[XV]) {
@@ -1155,9 +1168,9 @@ __global__ __launch_bounds__(512) void k_mfma_kq(const uint8_t* __restrict__ cod
   auto load_codes = [&](int step, u32x2 (&q)[4]) {
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
-      int64_t off = (int64_t)step * 128 + 32 * kq + 8 * g;
-      off = off + 8 <= row_bytes ? off : row_bytes - 8;
-      q[rt] = *(GlobalU32x2)(crow[rt] + off);
+      int off = step * 128 + 32 * kq + 8 * g;
+      off = off + 8 <= (int)row_bytes ? off : (int)row_bytes - 8;
+      q[rt] = __builtin_amdgcn_raw_buffer_load_b64(crs, crow[rt] + off, 0, kCachePolicyNT);
     }
   };
   float4v acc[8][4];
@@ -1291,12 +1304,15 @@ __global__ __launch_bounds__(512) void k_mfma_kq8(const uint8_t* __restrict__ co
   const int nb = blockIdx.x * 128 + 64 * wq;
   const int mb = blockIdx.y * 128;
   const int nsteps = (k_cols + kKq8Step - 1) / kKq8Step;
-  GlobalU8 crow[4];
+  // One buffer descriptor over the workgroup's 128 rows, as in k_mfma_kq (buffer loads keep
+  // the one-step code prefetch in place; rows past n_rows read as zeros and are not stored).
+  const int band0 = blockIdx.x * 128;
+  const int band_rows = n_rows - band0 < 128 ? n_rows - band0 : 128;
+  const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(codes + (int64_t)band0 * k_cols), (short)0, band_rows * k_cols, kBufferRsrcWord3);
+  int crow[4];
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt) {
-    const int r = nb + 16 * rt + j;
-    crow[rt] = (GlobalU8)codes + (int64_t)(r < n_rows ? r : n_rows - 1) * k_cols;
-  }
+  for (int rt = 0; rt < 4; ++rt) crow[rt] = (64 * wq + 16 * rt + j) * k_cols;
   auto load_x = [&](int step, u32x4 (&v)[XV]) {
 #pragma unroll
     for (int i = 0; i < XV; ++i) {
@@ -1325,9 +1341,9 @@ __global__ __launch_bounds__(512) void k_mfma_kq8(const uint8_t* __restrict__ co
   auto load_codes = [&](int step, u32x2 (&q)[4]) {
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
-      int64_t off = (int64_t)step * kKq8Step + 32 * kq + 8 * g;
+      int off = step * kKq8Step + 32 * kq + 8 * g;
       off = off + 8 <= k_cols ? off : k_cols - 8;
-      q[rt] = *(GlobalU32x2)(crow[rt] + off);
+      q[rt] = __builtin_amdgcn_raw_buffer_load_b64(crs, crow[rt] + off, 0, kCachePolicyNT);
     }
   };
   float4v acc[8][4];
@@ -1515,12 +1531,25 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
   const int b0 = (int)blockIdx.x / KS;
   const int slice_k0 = part * (k_cols / KS) + w * 32 * ND;
   const int slice_b0 = part * (int)(row_bytes / KS) + w * BR;
-  auto seg_of = [&](int b) {
-    int si = 0;
+  // The fields of the segment that holds block b, selected with static indices: a field read
+  // at a run-time segment index compiles to a vector load from the argument block, and its
+  // wait would also wait for every code load in flight.
+  struct SegView {
+    const uint8_t* codes;
+    float* y;
+    int n_rows, blk_begin;
+    LutBytes tb;
+    float scale;
+  };
+  auto seg_view = [&](int b) {
+    SegView v{segs.s[0].codes, segs.s[0].y, segs.s[0].n_rows, segs.s[0].blk_begin,
+              segs.s[0].tb, segs.s[0].scale};
 #pragma unroll
     for (int i = 1; i < kMaxSegs; ++i)
-      if (i < nseg && b >= segs.s[i].blk_begin) si = i;
-    return si;
+      if (i < nseg && b >= segs.s[i].blk_begin)
+        v = SegView{segs.s[i].codes, segs.s[i].y, segs.s[i].n_rows, segs.s[i].blk_begin,
+                    segs.s[i].tb, segs.s[i].scale};
+    return v;
   };
   // Activations first (they return first): in tile tt, lane row j is batch row
   // 16 tt + j % MB of dword group j / MB; register r holds dword d = G r + j / MB of this
@@ -1547,10 +1576,10 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
     const uint8_t* codes = codes0;
     int n_rows = n_rows0, lb = bb;
     if (nseg > 1) {
-      const int si = seg_of(bb);
-      codes = segs.s[si].codes;
-      n_rows = segs.s[si].n_rows;
-      lb = bb - segs.s[si].blk_begin;
+      const SegView v = seg_view(bb);
+      codes = v.codes;
+      n_rows = v.n_rows;
+      lb = bb - v.blk_begin;
     }
     const int64_t base = (int64_t)lb * 16 * row_bytes;
     const int64_t avail = (int64_t)n_rows * row_bytes - base;
@@ -1580,11 +1609,11 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
       for (int h = 0; h < NRES; ++h) {
         if (h < held) {
           const int b = blast - (held - 1 - h) * gb;
-          const int si = seg_of(b);
-          const int n_rows = segs.s[si].n_rows;
-          const int row = (b - segs.s[si].blk_begin) * 16 + rj;
+          const SegView v = seg_view(b);
+          const int n_rows = v.n_rows;
+          const int row = (b - v.blk_begin) * 16 + rj;
           if (row < n_rows) {
-            float* yp = segs.s[si].y + (int64_t)ri * n_rows + row;
+            float* yp = v.y + (int64_t)ri * n_rows + row;
             if (KS == 2) unsafeAtomicAdd(yp, res[h]);
             else *yp = res[h];
           }
@@ -1596,9 +1625,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_mfma_sk(const uint16_t* __restri
   uint8_t* s_cw = s_ct[w];
   const int my_group = (lane >> 4) * G / 4;   // dword group of this lane's D rows
   auto block = [&](int b, const u32x4 (&qc)[NI]) {
-    const int bsi = seg_of(b);
-    const LutBytes tb = segs.s[bsi].tb;
-    const float scale = segs.s[bsi].scale;
+    const SegView sv = seg_view(b);
+    const LutBytes tb = sv.tb;
+    const float scale = sv.scale;
     // LDS operations of one wavefront complete in order: the reads see the writes.
 #pragma unroll
     for (int c = 0; c < NI; ++c)
@@ -2130,6 +2159,8 @@ constexpr int64_t kMaxBatchRows = 65535LL * 64;
 template <int BITS>
 int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st) {
   const int N = (int)j.n;
+  // The kernel reads a workgroup's 128 rows through one buffer descriptor of at most 2^31 bytes.
+  if ((int64_t)128 * K * BITS / 8 >= ((int64_t)1 << 31)) return LOGBQ_ERR_UNSUPPORTED;
   LutBytes tb = {0, 0, 0, 0};
   typename LutOf<BITS>::type lut;
   float scale;
@@ -2202,7 +2233,8 @@ int32_t launch_sk8(const uint16_t* x, int M, int K, const LinearJob& j, hipStrea
 }
 
 // K-quartered MFMA path on 8-bit codes: m > 64 at N >= 16384.
-bool kq8_shape(int M, int64_t N) { return M > 64 && N >= 16384; }
+// (K < 2^24 keeps the 128-row buffer descriptor below 2^31 bytes.)
+bool kq8_shape(int M, int64_t N, int K) { return M > 64 && N >= 16384 && K < (1 << 24); }
 
 int32_t launch_kq8(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st) {
   Lut256 lut;
@@ -2215,7 +2247,8 @@ int32_t launch_kq8(const uint16_t* x, int M, int K, const LinearJob& j, hipStrea
 }
 
 // K-quartered MFMA path (4-bit, sign-symmetric codebooks): m > 96 at N >= 4096.
-bool kq_shape(int M, int64_t N) { return M > 96 && N >= 4096; }
+// (K < 2^25 keeps the 128-row buffer descriptor below 2^31 bytes.)
+bool kq_shape(int M, int64_t N, int K) { return M > 96 && N >= 4096 && K < (1 << 25); }
 
 int32_t launch_kq(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st) {
   const int N = (int)j.n;
@@ -2408,8 +2441,8 @@ int choose_path(int M, int K, int64_t N) {
   if (M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl) &&
       !(M >= (BITS == 8 ? 5 : 3) && (int64_t)M * N > 65536))
     return LOGBQ_PATH_GEMV;
-  if (BITS == 4 && kq_shape(M, N)) return LOGBQ_PATH_MFMA_KQ;
-  if (BITS == 8 && kq8_shape(M, N)) return LOGBQ_PATH_MFMA_KQ;
+  if (BITS == 4 && kq_shape(M, N, K)) return LOGBQ_PATH_MFMA_KQ;
+  if (BITS == 8 && kq8_shape(M, N, K)) return LOGBQ_PATH_MFMA_KQ;
   return LOGBQ_PATH_MFMA;
 }
 
