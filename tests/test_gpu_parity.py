@@ -346,6 +346,27 @@ def test_linear_split_k_two_tiles():
                 assert torch.equal(yg, y1)
 
 
+def test_linear_long_rows_unsupported():
+    """The stepped MFMA kernel reads a workgroup's 128 rows through one buffer descriptor, so
+    it refuses rows of 2^31 / 128 bytes or more (k >= 2^25 at 4 bits, k >= 2^24 at 8 bits)
+    with UNSUPPORTED before launching anything; the output buffer is left untouched."""
+    m, n = 9, 1
+    for bits, k in ((4, 1 << 25), (8, 1 << 24)):
+        assert L.linear_path(bits, m, k, n) == "mfma"
+        _say(f"long rows bits={bits} k={k}")
+        x = torch.zeros((m, k), dtype=torch.float16, device=DEV)
+        codes = torch.zeros((n, k // 2 if bits == 4 else k), dtype=torch.uint8, device=DEV)
+        cb = np.zeros(16 if bits == 4 else 256, dtype=np.float32)
+        y = torch.full((m, n), 7.0, dtype=torch.float32, device=DEV)
+        fn = L.linear if bits == 4 else L.linear8
+        with pytest.raises(L.LogbqError) as e:
+            fn(x, codes, cb, out=y)
+        assert e.value.status == L.ERR_UNSUPPORTED
+        torch.cuda.synchronize()
+        assert torch.all(y == 7.0).item()
+        del x, codes
+
+
 def test_linear_split_k_pairs_narrow():
     """Narrow layers split K over workgroup pairs (float atomic adds onto a zeroed y), chosen
     per linear from its own row count: K = 8192 with 2047 rows (128 blocks) at m <= 8 and up
