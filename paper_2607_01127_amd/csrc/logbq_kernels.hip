@@ -11,7 +11,8 @@
 //   k_mfma2    y = x . W_hat^T for larger m: a code dword (8 weights of one row) becomes one
 //              lane's B operand of v_mfma_f32_16x16x32_f16, dequantized by pair-table lookups
 //              or by v_perm_b32 byte tables in registers; activations are staged through LDS
-//              as the A operand; float32 accumulation in the MFMA.
+//              as the A operand; float32 accumulation in the MFMA. k_mfma2_narrow: the same
+//              with 64-row workgroups, for layers whose workgroups then all fit on the chip.
 //   k_mfma_sk  the same product for 2 <= m <= 32 split over K: the 8 or 16 wavefronts of a
 //              workgroup share a block of 16 rows (one K slice each, activations held in
 //              registers) and sum their partial tiles through LDS; at K = 8192 and m > 16, on
@@ -898,20 +899,29 @@ __device__ __forceinline__ int x_unit(int r, int u) { return (u + 8 * ((r >> 3) 
 // with that step's codes, STAGES - 1 steps ahead: vector loads complete in issue order, so an
 // activation load issued later than a code load would wait for it. COAL is used for MT <= 2,
 // where it measured 10-20 % faster; larger MT keep the first scheme.
-template <int BITS, int MT, int STAGES, bool PAIRS, bool COAL>
-__global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes,
-                                               const uint16_t* __restrict__ x,
-                                               float* __restrict__ y, int n_rows, int k_cols,
-                                               int m_rows, LutBytes tb,
-                                               typename LutOf<BITS>::type lut, float scale) {
+//
+// W is the number of wavefronts per workgroup (16 W weight rows). k_mfma2 runs W = 8;
+// k_mfma2_narrow runs W = 4 (register tables only) for layers whose 64-row workgroups all fit
+// on the chip at once: there every workgroup has a CU to itself either way, and halving the
+// rows per workgroup halves the K walk each CU does for the layer.
+template <int BITS, int MT, int STAGES, bool PAIRS, bool COAL, int W>
+__device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
+                                           const uint16_t* __restrict__ x,
+                                           float* __restrict__ y, int n_rows, int k_cols,
+                                           int m_rows, LutBytes tb,
+                                           const typename LutOf<BITS>::type& lut, float scale) {
   static_assert(STAGES % 2 == 0, "the loop is unrolled by STAGES and alternates two tiles");
   static_assert(BITS == 4 || PAIRS, "8-bit codes are dequantized through the LDS table");
+  static_assert(W == 8 || (W == 4 && !PAIRS), "the pair table is filled by 512 threads");
+  constexpr int NT = 64 * W;             // threads
+  constexpr int ROWS = 16 * W;           // weight rows per workgroup
+  constexpr int XV = MT * 512 / NT;      // activation vectors per thread per step
   constexpr int RB = 32 * BITS;          // code bytes of one row per step (256 k)
   constexpr int CB = RB / 64;            // 16-byte pieces per lane per step
   constexpr int TP = RB + 16;            // transpose buffer pitch (bytes)
   __shared__ __attribute__((aligned(16))) uint16_t s_x[2][MT * 16][kM2Pad];
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[PAIRS ? kLutWords : 4];
-  __shared__ __attribute__((aligned(16))) uint8_t s_ct[COAL ? 8 * 16 * TP : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t s_ct[COAL ? W * 16 * TP : 16];
   if (PAIRS) fill_lut<BITS, 512>(s_lut, lut);
   const uint32_t laneoff = (uint32_t)(threadIdx.x & 63) << 2;
 
@@ -920,27 +930,27 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
   const int wave = t >> 6;
   const int j = lane & 15;
   const int g = lane >> 4;
-  const int n0 = blockIdx.x * 128 + wave * 16;
+  const int n0 = blockIdx.x * ROWS + wave * 16;
   const int mb = blockIdx.y * (MT * 16);
   const int nsteps = (k_cols + kM2Step - 1) / kM2Step;
   const int64_t row_bytes = (int64_t)k_cols * BITS / 8;
-  // One buffer descriptor over the workgroup's 128 rows (rows past n_rows read as zeros and
-  // are not stored). Buffer loads keep the code prefetch where it is issued: plain loads of
-  // the read-only codes were moved by the compiler next to their use.
-  const int band0 = blockIdx.x * 128;
-  const int band_rows = n_rows - band0 < 128 ? n_rows - band0 : 128;
+  // One buffer descriptor over the workgroup's rows (rows past n_rows read as zeros and are
+  // not stored). Buffer loads keep the code prefetch where it is issued: plain loads of the
+  // read-only codes were moved by the compiler next to their use.
+  const int band0 = blockIdx.x * ROWS;
+  const int band_rows = n_rows - band0 < ROWS ? n_rows - band0 : ROWS;
   const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(codes + (int64_t)band0 * row_bytes), (short)0, (int)(band_rows * row_bytes),
       kBufferRsrcWord3);
   const int row = n0 + j;
   const int crow = (wave * 16 + j) * (int)row_bytes;   // this lane's row in the descriptor
 
-  // Activation tile of a step: MT*16 rows x 256 halves = MT*512 vectors of 16 bytes, MT per
+  // Activation tile of a step: MT*16 rows x 256 halves = MT*512 vectors of 16 bytes, XV per
   // thread. Loads are clamped in bounds; entries past m_rows / k_cols are zeroed when written.
-  auto load_x = [&](int step, u32x4 (&v)[MT]) {
+  auto load_x = [&](int step, u32x4 (&v)[XV]) {
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const int idx = t + 512 * i;
+    for (int i = 0; i < XV; ++i) {
+      const int idx = t + NT * i;
       const int m = mb + (idx >> 5);
       const int kk = step * kM2Step + (idx & 31) * 8;
       const int mc = m < m_rows ? m : m_rows - 1;
@@ -949,10 +959,10 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
                             (int64_t)mc * k_cols + kc);
     }
   };
-  auto store_x = [&](int step, int slot, const u32x4 (&v)[MT]) {
+  auto store_x = [&](int step, int slot, const u32x4 (&v)[XV]) {
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const int idx = t + 512 * i;
+    for (int i = 0; i < XV; ++i) {
+      const int idx = t + NT * i;
       const uint32_t keep = 0u - (uint32_t)((mb + (idx >> 5) < m_rows) &
                                             (step * kM2Step + (idx & 31) * 8 < k_cols));
       u32x4 w = PAIRS ? v[i] : permute_x8(v[i]);
@@ -1015,7 +1025,7 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
   // issued after an older tile.
   constexpr int XR = COAL ? STAGES : 2;
   u32x4 q[STAGES][CB];
-  u32x4 xr[XR][MT];
+  u32x4 xr[XR][XV];
   auto clampstep = [&](int t2) { return t2 < nsteps ? t2 : nsteps - 1; };
   if (COAL) {
 #pragma unroll
@@ -1085,6 +1095,25 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
       const int m = mb + mt * 16 + 4 * g + r;
       if (m < m_rows && row < n_rows) y[(int64_t)m * n_rows + row] = acc[mt][r] * scale;
     }
+}
+
+template <int BITS, int MT, int STAGES, bool PAIRS, bool COAL>
+__global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes,
+                                               const uint16_t* __restrict__ x,
+                                               float* __restrict__ y, int n_rows, int k_cols,
+                                               int m_rows, LutBytes tb,
+                                               typename LutOf<BITS>::type lut, float scale) {
+  mfma2_body<BITS, MT, STAGES, PAIRS, COAL, 8>(codes, x, y, n_rows, k_cols, m_rows, tb, lut,
+                                               scale);
+}
+
+template <int MT, bool COAL>
+__global__ __launch_bounds__(256) void k_mfma2_narrow(const uint8_t* __restrict__ codes,
+                                                      const uint16_t* __restrict__ x,
+                                                      float* __restrict__ y, int n_rows,
+                                                      int k_cols, int m_rows, LutBytes tb,
+                                                      Lut16 lut, float scale) {
+  mfma2_body<4, MT, 4, false, COAL, 4>(codes, x, y, n_rows, k_cols, m_rows, tb, lut, scale);
 }
 
 // ------------------------------------------------------------------ MFMA GEMM, K quarters, m > 96
@@ -2156,6 +2185,20 @@ bool make_lut_bytes(const float* cb, LutBytes* tb, float* scale) {
 // Largest batch: the MFMA grid's y dimension (at most 65535) covers 64 batch rows or more each.
 constexpr int64_t kMaxBatchRows = 65535LL * 64;
 
+// The stepped kernel with 64-row workgroups (k_mfma2_narrow) serves a sign-symmetric codebook
+// when its whole grid fits on the chip at once, one workgroup per CU (gfx950: 256 CUs; a fixed
+// count keeps the path choice a function of m, k and N alone). There each CU walks K for 64
+// rows instead of 128 (or for none, when the 128-row grid leaves it idle). Measured on MI355X
+// (graph replay, codes streamed from HBM), 64-row against 128-row workgroups: 0.73-0.89 of
+// the time for N = 2048 .. 16384, K = 2048 .. 14336, m = 9 .. 96 (e.g. 4096 x 4096 at m = 64:
+// 26.6 -> 20.9 us, 4096 -> 14336 at m = 96: 37.9 -> 29.6 us), bit-identical results (each
+// output is the same K walk); at N = 28672 (448 workgroups) 1.04-1.44 times the time.
+constexpr int64_t kNarrowMaxWorkgroups = 256;
+bool narrow_fits(int M, int64_t N) {
+  const int64_t gy = M > 128 ? (M + 127) / 128 : 1;   // batch tiles of up to 8 x 16 rows
+  return ((N + 63) / 64) * gy <= kNarrowMaxWorkgroups;
+}
+
 template <int BITS>
 int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStream_t st) {
   const int N = (int)j.n;
@@ -2174,12 +2217,27 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
   int mt16 = (M + 15) / 16;
   const int cap = symmetric ? 8 : 4;
   if (mt16 > cap) mt16 = cap;
-  dim3 grid((unsigned)((N + 127) / 128), (unsigned)((M + 16 * mt16 - 1) / (16 * mt16)));
+  const bool narrow = BITS == 4 && symmetric && narrow_fits(M, N);
+  const int rows_wg = narrow ? 64 : 128;
+  dim3 grid((unsigned)((N + rows_wg - 1) / rows_wg),
+            (unsigned)((M + 16 * mt16 - 1) / (16 * mt16)));
 #define LOGBQ_M2(MT, ST, PR) hipLaunchKernelGGL((k_mfma2<BITS, MT, ST, PR, (MT <= 2)>), grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
+#define LOGBQ_M2N(MT) hipLaunchKernelGGL((k_mfma2_narrow<MT, (MT <= 2)>), grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
   if constexpr (BITS == 4) {
     // Register dequantization whenever the codebook allows it: measured 1 to 2.5 us faster than
     // the LDS table at m = 4 .. 32 on the 8192 x 28672 layer, with bit-identical results.
-    if (symmetric) {
+    if (narrow) {
+      switch (mt16) {
+        case 1: LOGBQ_M2N(1); break;
+        case 2: LOGBQ_M2N(2); break;
+        case 3: LOGBQ_M2N(3); break;
+        case 4: LOGBQ_M2N(4); break;
+        case 5: LOGBQ_M2N(5); break;
+        case 6: LOGBQ_M2N(6); break;
+        case 7: LOGBQ_M2N(7); break;
+        default: LOGBQ_M2N(8); break;
+      }
+    } else if (symmetric) {
       switch (mt16) {
         case 1: LOGBQ_M2(1, 4, false); break;
         case 2: LOGBQ_M2(2, 4, false); break;
@@ -2207,6 +2265,7 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
     }
   }
 #undef LOGBQ_M2
+#undef LOGBQ_M2N
   return launch_status();
 }
 
@@ -2409,7 +2468,10 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
 //
 // Above m = 96 at N >= 4096 the K-quartered kernel replaces the stepped one for 4-bit codes with
 // sign-symmetric codebooks (7-11 % faster on the 8192 x 28672 and 4096 x 14336 layers; slower
-// on narrow layers, which have too few 128-row workgroups).
+// on narrow layers, which have too few 128-row workgroups), except where the stepped kernel's
+// 64-row grid fits on the chip: there that one is faster (measured at m = 97 .. 256,
+// N = 4096 .. 16384, K = 2048 .. 14336: 0.76-0.98 of the K-quartered kernel's time, e.g.
+// 4096 x 4096 at m = 128: 37.1 -> 34.3 us, 2048 -> 4096 at m = 128: 23.1 -> 19.3 us).
 //
 // Where the split-K MFMA kernel applies (4-bit codes, 2 <= m <= 32, K = 1, 2, 4 or 8 Ki), it
 // takes 5 <= m <= 16, m = 4 unless N <= 1024 at K = 8192, m = 3 at N >= 4096, and
@@ -2441,7 +2503,7 @@ int choose_path(int M, int K, int64_t N) {
   if (M <= 8 && gemv_config<BITS>(M, K, &wk, &cpl) &&
       !(M >= (BITS == 8 ? 5 : 3) && (int64_t)M * N > 65536))
     return LOGBQ_PATH_GEMV;
-  if (BITS == 4 && kq_shape(M, N, K)) return LOGBQ_PATH_MFMA_KQ;
+  if (BITS == 4 && kq_shape(M, N, K) && !narrow_fits(M, N)) return LOGBQ_PATH_MFMA_KQ;
   if (BITS == 8 && kq8_shape(M, N, K)) return LOGBQ_PATH_MFMA_KQ;
   return LOGBQ_PATH_MFMA;
 }
@@ -2963,8 +3025,12 @@ int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const
       int mt16 = (M + 15) / 16;
       const int cap = symmetric ? 8 : 4;
       if (mt16 > cap) mt16 = cap;
-      std::snprintf(buf, sizeof(buf), "k_mfma2<%d, %d, 4, %s, %s>", bits, mt16,
-                    symmetric ? "false" : "true", mt16 <= 2 ? "true" : "false");
+      if (bits == 4 && symmetric && narrow_fits(M, n))
+        std::snprintf(buf, sizeof(buf), "k_mfma2_narrow<%d, %s>", mt16,
+                      mt16 <= 2 ? "true" : "false");
+      else
+        std::snprintf(buf, sizeof(buf), "k_mfma2<%d, %d, 4, %s, %s>", bits, mt16,
+                      symmetric ? "false" : "true", mt16 <= 2 ? "true" : "false");
     }
   }
   const size_t need = std::strlen(buf) + 1;

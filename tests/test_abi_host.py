@@ -252,8 +252,11 @@ def test_linear_path_rule():
     assert lp(4, 32, 4096, 28672) == "splitk" and lp(4, 33, 4096, 4096) == "mfma"
     assert lp(4, 4, 14336, 4096) == "splitk" and lp(4, 9, 14336, 4096) == "mfma"
     assert lp(4, 96, 8192, 28672) == "mfma"
-    # K-quartered MFMA GEMM: 4-bit, m > 96 at N >= 4096
-    assert lp(4, 128, 8192, 28672) == "mfma_kq" and lp(4, 97, 1024, 4096) == "mfma_kq"
+    # K-quartered MFMA GEMM: 4-bit, m > 96 at N >= 4096, unless the stepped kernel's 64-row
+    # grid fits on the chip (ceil(N / 64) x ceil(m / 128) <= 256 workgroups)
+    assert lp(4, 128, 8192, 28672) == "mfma_kq" and lp(4, 97, 1024, 16448) == "mfma_kq"
+    assert lp(4, 97, 1024, 4096) == "mfma" and lp(4, 128, 1024, 16384) == "mfma"
+    assert lp(4, 129, 1024, 8192) == "mfma" and lp(4, 129, 1024, 8256) == "mfma_kq"
     assert lp(4, 128, 1024, 4095) == "mfma" and lp(8, 128, 8192, 28672) == "mfma_kq"
     assert lp(8, 65, 8192, 16384) == "mfma_kq" and lp(8, 64, 8192, 28672) == "mfma"
     assert lp(8, 128, 4096, 14336) == "mfma"
@@ -297,6 +300,14 @@ def test_linear_kernel_names():
     assert lk(4, 12, 4096, 2048) == "k_mfma_sk<8, 16, 1, 1, 1, false>"
     assert lk(4, 32, 8192, 28672) == "k_mfma2<4, 2, 4, false, true>"
     assert lk(4, 128, 8192, 28672) == "k_mfma_kq"
+    # 64-row workgroups where the whole grid fits on the chip (at most 256 workgroups)
+    assert lk(4, 9, 14336, 4096) == "k_mfma2_narrow<1, true>"
+    assert lk(4, 64, 4096, 4096) == "k_mfma2_narrow<4, false>"
+    assert lk(4, 33, 4096, 16384) == "k_mfma2_narrow<3, false>"
+    assert lk(4, 33, 4096, 16385) == "k_mfma2<4, 3, 4, false, false>"
+    assert lk(4, 128, 4096, 4096) == "k_mfma2_narrow<8, false>"
+    assert lk(4, 129, 1024, 8192) == "k_mfma2_narrow<8, false>"
+    assert lk(4, 129, 1024, 8256) == "k_mfma_kq"
     assert lk(8, 1, 8192, 28672) == "k_gemv<8, 1, 8, false, 2>"
     assert lk(8, 128, 8192, 28672) == "k_mfma_kq8" and lk(8, 128, 4096, 14336) == "k_mfma2<8, 4, 4, true, false>"
     assert lk(8, 8, 8192, 28672) == "k_mfma_sk8<16, 2>" and lk(8, 12, 4096, 4096) == "k_mfma_sk8<8, 1>"
@@ -307,6 +318,7 @@ def test_linear_kernel_names():
     assert lk(4, 32, 4096, 14336, cb) == "k_mfma2<4, 2, 4, true, true>"   # above m = 16
     assert lk(4, 4, 14336, 4096, cb) == "k_mfma2<4, 1, 4, true, true>"    # and at K = 14336
     assert lk(4, 128, 8192, 28672, cb) == "k_mfma2<4, 4, 4, true, false>"
+    assert lk(4, 64, 4096, 4096, cb) == "k_mfma2<4, 4, 4, true, false>"
     sym = np.array([0] + [2.0 ** k for k in range(1, 8)] + [0] + [-(2.0 ** k) for k in range(1, 8)],
                    dtype=np.float32)
     assert lk(4, 128, 8192, 28672, sym) == "k_mfma_kq"

@@ -432,6 +432,55 @@ def test_linear_split_k_14336():
         assert torch.equal(ys[0], y) and torch.equal(ys[1], y3)
 
 
+def test_linear_stepped_narrow():
+    """The stepped MFMA kernel with 64-row workgroups (taken when its whole grid fits on the
+    chip, at most 256 workgroups): ragged row counts, K outside the split-K set (3072) and in
+    it, m from 9 to 200 (one to eight batch tiles, two batch blocks above 128). y is prefilled
+    with NaN, each call is repeated and must give the same bits."""
+    for n, k in ((1000, 3072), (4097, 2048)):
+        w, p, r = prepare(n, k, [8, 25, k % 1000, n])
+        c, cb = gpu_encode(w, p)
+        wh = O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
+        del w
+        for m in (9, 24, 33, 64, 96, 97, 128, 129, 200):
+            if k == 2048 and m <= 32:
+                continue   # split-K territory
+            name = L.linear_kernel(4, m, k, n)
+            _say(f"stepped narrow n={n} k={k} m={m} kernel {name}")
+            assert name.startswith("k_mfma2_narrow<"), name
+            x = inputs.activations(m, k, seed=[8, 25, n, m])
+            xd = torch.from_numpy(x).to(DEV)
+            y = torch.full((m, n), float("nan"), dtype=torch.float32, device=DEV)
+            L.linear(xd, c, cb, out=y)
+            y2 = L.linear(xd, c, cb)
+            torch.cuda.synchronize()
+            assert torch.isfinite(y).all()
+            assert torch.equal(y, y2)
+            assert rel_err(y.cpu().numpy(), x, wh) <= 2.5e-4
+
+
+def test_linear_stepped_narrow_equals_wide():
+    """Both stepped kernels give every output the same K walk, so they agree bit for bit: a
+    16385-row linear (257 workgroups of 64 rows would not fit, so 128-row workgroups) against
+    its first 16384 rows (256 workgroups of 64 rows)."""
+    n, k = 16385, 3072
+    w, p, _ = prepare(64, 256, [8, 26, 0, 0])
+    _, cb = gpu_encode(w, p)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(26)
+    c = torch.randint(0, 256, (n, k // 2), dtype=torch.uint8, device=DEV, generator=gen)
+    for m in (9, 24, 33, 64, 96):
+        wide, narrow = L.linear_kernel(4, m, k, n), L.linear_kernel(4, m, k, n - 1)
+        _say(f"stepped wide {wide} vs narrow {narrow}, k={k} m={m}")
+        assert wide.startswith("k_mfma2<") and narrow.startswith("k_mfma2_narrow<")
+        x = torch.from_numpy(inputs.activations(m, k, seed=[8, 26, 1, m])).to(DEV)
+        y = L.linear(x, c, cb)
+        y1 = L.linear(x, c[: n - 1], cb)
+        torch.cuda.synchronize()
+        assert torch.isfinite(y).all()
+        assert torch.equal(y[:, : n - 1], y1)
+
+
 def test_linear_multi_matches_single_launches():
     """Grouped launch of linears sharing x: every output equals the single-linear call bit for
     bit, and the oracle within tolerance (qkv-like and gate/up-like groups, ragged sizes)."""
