@@ -183,7 +183,7 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  *               a common power-of-two scaling, exact in the result up to float16 rounding.
  *   y_dev     : device, [m][n] float32, written.
  * Accumulation is float32. Four kernels, chosen from (m, k, n) alone: for 2 <= m <= 32 and
- * k in {1024, 2048, 4096, 8192} (and m <= 8 at k = 14336; there, as above m = 16, only for
+ * k in {1024, 2048, 4096, 8192} (and m <= 16 at k = 14336; there, as above m = 16, only for
  * sign-symmetric codebooks), a split-K dequantize-into-MFMA kernel takes 5 <= m <= 16,
  * m = 4 unless n <= 1024 at k = 8192, m = 3 at n >= 4096, and 17 <= m <= 32 unless m > 20 at
  * k = 8192 and n > 16384 (above m = 16 only for sign-symmetric codebooks; at k = 8192 above
@@ -193,7 +193,9 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  * runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and shapes whose
  * activations do not fit the GEMV's registers) runs the stepped dequantize-into-MFMA skinny
  * GEMM, except m > 96 at n >= 4096, which runs a K-quartered MFMA GEMM for sign-symmetric
- * codebooks. logbq_linear_path reports the choice. Results are deterministic for every path.
+ * codebooks unless ceil(n / 64) * ceil(m / 128) <= 256. For sign-symmetric codebooks within
+ * that bound the stepped kernel runs with 64-row workgroups, so that its whole grid is on the
+ * chip at once. logbq_linear_path reports the choice. Results are deterministic for every path.
  * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment, or k >= 2^24 on
  * the stepped or K-quartered MFMA kernel), HIP.
  */

@@ -1504,10 +1504,12 @@ __global__ __launch_bounds__(512) void k_mfma_kq8(const uint8_t* __restrict__ co
 // the same blocks and add their results into y with float atomics after y is zeroed (two terms
 // onto zero: the same sum in either order, so results stay deterministic). The alternative
 // of two launches (the second adding into y) measured 7-8 us slower at 8192 -> 28672.
-// K = 14336 (m <= 8, G = 2) takes the same K split over workgroup pairs of W = 14 wavefronts,
-// ND = 16: 14336 -> 4096 at m = 4 / 8: 14.5 / 26.7 -> 11.5 / 12.6 us against the split-row
-// GEMV and the stepped kernel (one 16-wavefront workgroup per block, ND = 28, measured
-// 14.8 / 17.2 us: 256 blocks leave each workgroup one block, with nothing to overlap).
+// K = 14336 (m <= 16; G = 2 up to m = 8) takes the same K split over workgroup pairs of
+// W = 14 wavefronts, ND = 16: 14336 -> 4096 at m = 4 / 8: 14.5 / 26.7 -> 11.5 / 12.6 us against
+// the split-row GEMV and the stepped kernel (one 16-wavefront workgroup per block, ND = 28,
+// measured 14.8 / 17.2 us: 256 blocks leave each workgroup one block, with nothing to
+// overlap); at m = 9 / 12 / 16: 34.6 / 34.6 / 34.7 -> 13.7-13.9 / 14.7 / 15.8 us against the
+// stepped kernel with 64-row workgroups.
 //
 // Up to kMaxSegs linears that share x, in one launch: their 16-row blocks are numbered one
 // after another (segment s holds blocks [blk_begin, blk_begin + ceil(n_rows / 16))), and every
@@ -2320,10 +2322,10 @@ int32_t launch_kq(const uint16_t* x, int M, int K, const LinearJob& j, hipStream
 }
 
 // Split-K MFMA path: 4-bit codes, 2 <= m <= 32 at K in {1024, 2048, 4096, 8192}, and
-// 2 <= m <= 8 at K = 14336 (the down projection of the 8B-shaped decoder).
+// 2 <= m <= 16 at K = 14336 (the down projection of the 8B-shaped decoder).
 bool sk_shape(int M, int K) {
   return M >= 2 && ((M <= 32 && (K == 1024 || K == 2048 || K == 4096 || K == 8192)) ||
-                    (M <= 8 && K == 14336));
+                    (M <= 16 && K == 14336));
 }
 
 // Split-K configuration: code dwords per lane and row, wavefronts per workgroup, batch groups,
@@ -2340,7 +2342,7 @@ struct SkConfig {
 // each computes as in a call of its own.
 SkConfig sk_config(int M, int K, bool pairs, int blocks) {
   // K = 14336 = 2 x 14 x 512: workgroup pairs of 14 wavefronts, one K half each.
-  if (K == 14336) return {16, 14, 2, 1, 2};
+  if (K == 14336) return {16, 14, M <= 8 ? 2 : 1, 1, 2};
   if (M > 16) {   // two batch tiles (register tables only); K = 8192 over workgroup pairs
     const int waves = K >= 2048 ? 16 : 8;
     const int kparts = K == 8192 ? 2 : 1;
@@ -2408,7 +2410,8 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     LOGBQ_SK(16, 16, 1, 1, 1, false) LOGBQ_SK(16, 16, 2, 1, 1, false)
     LOGBQ_SK(4, 8, 1, 2, 1, false) LOGBQ_SK(4, 16, 1, 2, 1, false)
     LOGBQ_SK(8, 16, 1, 2, 1, false) LOGBQ_SK(8, 16, 1, 2, 2, false)
-    LOGBQ_SK(16, 14, 2, 1, 2, false) LOGBQ_SK(8, 16, 2, 1, 2, false)
+    LOGBQ_SK(16, 14, 2, 1, 2, false) LOGBQ_SK(16, 14, 1, 1, 2, false)
+    LOGBQ_SK(8, 16, 2, 1, 2, false)
     LOGBQ_SK(8, 16, 1, 1, 2, false) LOGBQ_SK(4, 16, 1, 1, 2, false)
 #undef LOGBQ_SK
     return LOGBQ_ERR_UNSUPPORTED;
@@ -2470,7 +2473,7 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
 // sign-symmetric codebooks (7-11 % faster on the 8192 x 28672 and 4096 x 14336 layers; slower
 // on narrow layers, which have too few 128-row workgroups), except where the stepped kernel's
 // 64-row grid fits on the chip: there that one is faster (measured at m = 97 .. 256,
-// N = 4096 .. 16384, K = 2048 .. 14336: 0.76-0.98 of the K-quartered kernel's time, e.g.
+// N = 4096 .. 16384, K = 2048 .. 14336: 0.77-1.00 of the K-quartered kernel's time, e.g.
 // 4096 x 4096 at m = 128: 37.1 -> 34.3 us, 2048 -> 4096 at m = 128: 23.1 -> 19.3 us).
 //
 // Where the split-K MFMA kernel applies (4-bit codes, 2 <= m <= 32, K = 1, 2, 4 or 8 Ki), it
