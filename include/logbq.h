@@ -183,8 +183,9 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  *               a common power-of-two scaling, exact in the result up to float16 rounding.
  *   y_dev     : device, [m][n] float32, written.
  * Accumulation is float32. Four kernels, chosen from (m, k, n) alone: for 2 <= m <= 32 and
- * k in {1024, 2048, 4096, 8192} (and m <= 16 at k = 14336; there, as above m = 16, only for
- * sign-symmetric codebooks), a split-K dequantize-into-MFMA kernel takes 5 <= m <= 16,
+ * k in {1024, 2048, 4096, 8192} (and m <= 48 at k = 14336, run as launches of at most 16
+ * batch rows; there, as above m = 16, only for sign-symmetric codebooks), a split-K
+ * dequantize-into-MFMA kernel takes 5 <= m <= 16,
  * m = 4 unless n <= 1024 at k = 8192, m = 3 at n >= 4096, and 17 <= m <= 32 unless m > 20 at
  * k = 8192 and n > 16384 (above m = 16 only for sign-symmetric codebooks; at k = 8192 above
  * m = 16, and for sign-symmetric codebooks on narrow layers -- k = 8192 with n <= 2048 up to
@@ -346,8 +347,9 @@ int32_t logbq_linear_path(int32_t bits, int64_t m, int64_t k, int64_t n, int32_t
  * logbq_linear_kernel -- name of the kernel instance (with its template arguments, as a
  * profiler lists it) that reads the codes in a logbq_linear / logbq_linear8 call of shape
  * (m, k, n), e.g. "k_gemv<4, 1, 4, false, 2>" (Sec. 3.3 product; the choice is this
- * library's); a split-K call over workgroup pairs launches k_fill_zero before it. Host only:
- * needs no device and touches none.
+ * library's); a split-K call over workgroup pairs launches k_fill_zero before it, and one
+ * that runs its batch in 16-row launches (k = 14336 above m = 16) is named by its first.
+ * Host only: needs no device and touches none.
  *   bits, m, k, n : as logbq_linear_path; n fits in int32.
  *   codebook      : host, 2^bits floats, or NULL for a fitted (sign-symmetric) codebook; the
  *                   4-bit MFMA kernels dequantize in registers only for sign-symmetric ones.

@@ -1504,12 +1504,12 @@ __global__ __launch_bounds__(512) void k_mfma_kq8(const uint8_t* __restrict__ co
 // the same blocks and add their results into y with float atomics after y is zeroed (two terms
 // onto zero: the same sum in either order, so results stay deterministic). The alternative
 // of two launches (the second adding into y) measured 7-8 us slower at 8192 -> 28672.
-// K = 14336 (m <= 16; G = 2 up to m = 8) takes the same K split over workgroup pairs of
-// W = 14 wavefronts, ND = 16: 14336 -> 4096 at m = 4 / 8: 14.5 / 26.7 -> 11.5 / 12.6 us against
-// the split-row GEMV and the stepped kernel (one 16-wavefront workgroup per block, ND = 28,
-// measured 14.8 / 17.2 us: 256 blocks leave each workgroup one block, with nothing to
-// overlap); at m = 9 / 12 / 16: 34.6 / 34.6 / 34.7 -> 13.7-13.9 / 14.7 / 15.8 us against the
-// stepped kernel with 64-row workgroups.
+// K = 14336 (at most 16 batch rows per launch; G = 2 up to m = 8) takes the same K split over
+// workgroup pairs of W = 14 wavefronts, ND = 16: 14336 -> 4096 at m = 4 / 8: 14.5 / 26.7 ->
+// 11.5 / 12.6 us against the split-row GEMV and the stepped kernel (one 16-wavefront workgroup
+// per block, ND = 28, measured 14.8 / 17.2 us: 256 blocks leave each workgroup one block, with
+// nothing to overlap); at m = 9 / 12 / 16: 34.6 / 34.6 / 34.7 -> 13.7-13.9 / 14.7 / 15.8 us
+// against the stepped kernel with 64-row workgroups.
 //
 // Up to kMaxSegs linears that share x, in one launch: their 16-row blocks are numbered one
 // after another (segment s holds blocks [blk_begin, blk_begin + ceil(n_rows / 16))), and every
@@ -2322,10 +2322,11 @@ int32_t launch_kq(const uint16_t* x, int M, int K, const LinearJob& j, hipStream
 }
 
 // Split-K MFMA path: 4-bit codes, 2 <= m <= 32 at K in {1024, 2048, 4096, 8192}, and
-// 2 <= m <= 16 at K = 14336 (the down projection of the 8B-shaped decoder).
+// 2 <= m <= 48 at K = 14336 (the down projection of the 8B-shaped decoder; above m = 16 as
+// launches of at most 16 batch rows).
 bool sk_shape(int M, int K) {
   return M >= 2 && ((M <= 32 && (K == 1024 || K == 2048 || K == 4096 || K == 8192)) ||
-                    (M <= 16 && K == 14336));
+                    (M <= 48 && K == 14336));
 }
 
 // Split-K configuration: code dwords per lane and row, wavefronts per workgroup, batch groups,
@@ -2382,6 +2383,28 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     sg.blk_begin = total;
     all_symmetric = make_lut_bytes(j.codebook, &sg.tb, &sg.scale) && all_symmetric;
     total += (int)((j.n + 15) / 16);
+  }
+  if (all_symmetric && K == 14336 && M > 16) {
+    // Two batch tiles at this K would need 128 activation registers per lane, so the batch
+    // runs as launches of at most 16 rows (x and y rows are contiguous; chunk sizes differ by
+    // at most one). Measured on MI355X, 14336 -> 4096 at m = 17 / 24 / 32 / 48: 46.5 / 46.7 /
+    // 46.6 / 54.7 -> 27.1 / 29.6 / 32.2 / 48.9 us against the stepped kernel with 64-row
+    // workgroups (2048 rows at m = 24 / 32: 46.4 / 46.5 -> 24.2 / 26.6 us).
+    const int nchunk = (M + 15) / 16;
+    LinearJob part[kMaxSegs];
+    int pidx[kMaxSegs];
+    for (int c = 0, m0 = 0; c < nchunk; ++c) {
+      const int mc = M / nchunk + (c < M % nchunk ? 1 : 0);
+      for (int a = 0; a < count; ++a) {
+        part[a] = jobs[idx[a]];
+        part[a].y = jobs[idx[a]].y + (int64_t)m0 * jobs[idx[a]].n;
+        pidx[a] = a;
+      }
+      const int32_t r = launch_sk(x + (int64_t)m0 * K, mc, K, part, pidx, count, st, cus);
+      if (r != LOGBQ_OK) return r;
+      m0 += mc;
+    }
+    return LOGBQ_OK;
   }
   auto launch = [&](int nseg, const SkSegs& sgs, int nblocks, bool pairs, const Lut16& l,
                     const SkConfig& c) -> int32_t {

@@ -406,7 +406,7 @@ def test_linear_split_k_14336():
     """Split-K at K = 14336 on 4099 rows (257 blocks of 16, so a workgroup pair takes two or
     three blocks and the last block has 3 rows): workgroup pairs of 14 wavefronts add their K
     halves into y with float atomics after zeroing it, with two batch groups up to m = 8 and
-    one above. y is prefilled
+    one above; above m = 16 the batch runs as launches of at most 16 rows. y is prefilled
     with NaN (every output must be overwritten), each call is repeated and must give the same
     bits, and a grouped call (4099 and the first 4096 rows) equals single calls."""
     n, k = 4099, 14336
@@ -415,7 +415,7 @@ def test_linear_split_k_14336():
     wh = O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
     del w
     c2 = c[:4096]
-    for m in (3, 4, 5, 8, 9, 12, 16):
+    for m in (3, 4, 5, 8, 9, 12, 16, 17, 33, 48):
         assert L.linear_path(4, m, k, n) == "splitk" and L.linear_path(4, m, k, 4096) == "splitk"
         _say(f"split-K k={k} m={m} kernel {L.linear_kernel(4, m, k, n)}")
         x = inputs.activations(m, k, seed=[8, 23, 2, m])
