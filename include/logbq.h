@@ -194,9 +194,10 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  * runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and shapes whose
  * activations do not fit the GEMV's registers) runs the stepped dequantize-into-MFMA skinny
  * GEMM, except m > 96 at n >= 4096, which runs a K-quartered MFMA GEMM for sign-symmetric
- * codebooks unless ceil(n / 64) * ceil(m / 128) <= 256. For sign-symmetric codebooks within
- * that bound the stepped kernel runs with 64-row workgroups, so that its whole grid is on the
- * chip at once. logbq_linear_path reports the choice. Results are deterministic for every path.
+ * codebooks unless ceil(n / 64) * ceil(m / 128) <= 256. The stepped kernel runs with 64-row
+ * workgroups wherever its whole grid is then on the chip at once (ceil(n / 64) times its
+ * batch blocks of 128 rows, 64 for 8-bit codes and codebooks that are not sign-symmetric, at
+ * most 256). logbq_linear_path reports the choice. Results are deterministic for every path.
  * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment, or k >= 2^24 on
  * the stepped or K-quartered MFMA kernel), HIP.
  */

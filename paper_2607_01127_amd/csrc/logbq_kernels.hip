@@ -901,9 +901,9 @@ __device__ __forceinline__ int x_unit(int r, int u) { return (u + 8 * ((r >> 3) 
 // where it measured 10-20 % faster; larger MT keep the first scheme.
 //
 // W is the number of wavefronts per workgroup (16 W weight rows). k_mfma2 runs W = 8;
-// k_mfma2_narrow runs W = 4 (register tables only) for layers whose 64-row workgroups all fit
-// on the chip at once: there every workgroup has a CU to itself either way, and halving the
-// rows per workgroup halves the K walk each CU does for the layer.
+// k_mfma2_narrow runs W = 4 for layers whose 64-row workgroups all fit on the chip at once:
+// there every workgroup has a CU to itself either way, and halving the rows per workgroup
+// halves the K walk each CU does for the layer.
 template <int BITS, int MT, int STAGES, bool PAIRS, bool COAL, int W>
 __device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
                                            const uint16_t* __restrict__ x,
@@ -912,7 +912,7 @@ __device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
                                            const typename LutOf<BITS>::type& lut, float scale) {
   static_assert(STAGES % 2 == 0, "the loop is unrolled by STAGES and alternates two tiles");
   static_assert(BITS == 4 || PAIRS, "8-bit codes are dequantized through the LDS table");
-  static_assert(W == 8 || (W == 4 && !PAIRS), "the pair table is filled by 512 threads");
+  static_assert(W == 8 || W == 4, "8 or 4 wavefronts");
   constexpr int NT = 64 * W;             // threads
   constexpr int ROWS = 16 * W;           // weight rows per workgroup
   constexpr int XV = MT * 512 / NT;      // activation vectors per thread per step
@@ -922,7 +922,7 @@ __device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
   __shared__ __attribute__((aligned(16))) uint16_t s_x[2][MT * 16][kM2Pad];
   __shared__ __attribute__((aligned(16))) uint32_t s_lut[PAIRS ? kLutWords : 4];
   __shared__ __attribute__((aligned(16))) uint8_t s_ct[COAL ? W * 16 * TP : 16];
-  if (PAIRS) fill_lut<BITS, 512>(s_lut, lut);
+  if (PAIRS) fill_lut<BITS, NT>(s_lut, lut);
   const uint32_t laneoff = (uint32_t)(threadIdx.x & 63) << 2;
 
   const int t = threadIdx.x;
@@ -1107,13 +1107,14 @@ __global__ __launch_bounds__(512) void k_mfma2(const uint8_t* __restrict__ codes
                                                scale);
 }
 
-template <int MT, bool COAL>
+template <int BITS, int MT, bool PAIRS, bool COAL>
 __global__ __launch_bounds__(256) void k_mfma2_narrow(const uint8_t* __restrict__ codes,
                                                       const uint16_t* __restrict__ x,
                                                       float* __restrict__ y, int n_rows,
                                                       int k_cols, int m_rows, LutBytes tb,
-                                                      Lut16 lut, float scale) {
-  mfma2_body<4, MT, 4, false, COAL, 4>(codes, x, y, n_rows, k_cols, m_rows, tb, lut, scale);
+                                                      typename LutOf<BITS>::type lut,
+                                                      float scale) {
+  mfma2_body<BITS, MT, 4, PAIRS, COAL, 4>(codes, x, y, n_rows, k_cols, m_rows, tb, lut, scale);
 }
 
 // ------------------------------------------------------------------ MFMA GEMM, K quarters, m > 96
@@ -2187,17 +2188,21 @@ bool make_lut_bytes(const float* cb, LutBytes* tb, float* scale) {
 // Largest batch: the MFMA grid's y dimension (at most 65535) covers 64 batch rows or more each.
 constexpr int64_t kMaxBatchRows = 65535LL * 64;
 
-// The stepped kernel with 64-row workgroups (k_mfma2_narrow) serves a sign-symmetric codebook
-// when its whole grid fits on the chip at once, one workgroup per CU (gfx950: 256 CUs; a fixed
-// count keeps the path choice a function of m, k and N alone). There each CU walks K for 64
-// rows instead of 128 (or for none, when the 128-row grid leaves it idle). Measured on MI355X
-// (graph replay, codes streamed from HBM), 64-row against 128-row workgroups: 0.73-0.89 of
-// the time for N = 2048 .. 16384, K = 2048 .. 14336, m = 9 .. 96 (e.g. 4096 x 4096 at m = 64:
-// 26.6 -> 20.9 us, 4096 -> 14336 at m = 96: 37.9 -> 29.6 us), bit-identical results (each
-// output is the same K walk); at N = 28672 (448 workgroups) 1.04-1.44 times the time.
+// The stepped kernel with 64-row workgroups (k_mfma2_narrow) runs when its whole grid fits on
+// the chip at once, one workgroup per CU (gfx950: 256 CUs; a fixed count keeps the path choice
+// a function of m, k and N alone). There each CU walks K for 64 rows instead of 128 (or for
+// none, when the 128-row grid leaves it idle). Measured on MI355X (graph replay, codes
+// streamed from HBM), 64-row against 128-row workgroups, bit-identical results (each output is
+// the same K walk): register tables 0.73-0.89 of the time for N = 2048 .. 16384,
+// K = 2048 .. 14336, m = 9 .. 96 (e.g. 4096 x 4096 at m = 64: 26.6 -> 20.9 us, 4096 -> 14336 at
+// m = 96: 37.9 -> 29.6 us); the LDS tables (8-bit codes, other codebooks) 0.66-0.81 (8-bit
+// 4096 x 4096 at m = 48: 40.9 -> 27.0 us, 8192 x 8192 at m = 64: 86.0 -> 59.1 us; 4-bit
+// 4096 x 4096 at m = 64: 30.1 -> 21.0 us); at N = 28672 (448 workgroups) 1.04-1.44 times the
+// time. `cap` is the kernel's batch tiles per workgroup column (8 with register tables, 4 with
+// the LDS table).
 constexpr int64_t kNarrowMaxWorkgroups = 256;
-bool narrow_fits(int M, int64_t N) {
-  const int64_t gy = M > 128 ? (M + 127) / 128 : 1;   // batch tiles of up to 8 x 16 rows
+bool narrow_fits(int M, int64_t N, int cap = 8) {
+  const int64_t gy = M > 16 * cap ? (M + 16 * cap - 1) / (16 * cap) : 1;
   return ((N + 63) / 64) * gy <= kNarrowMaxWorkgroups;
 }
 
@@ -2219,25 +2224,32 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
   int mt16 = (M + 15) / 16;
   const int cap = symmetric ? 8 : 4;
   if (mt16 > cap) mt16 = cap;
-  const bool narrow = BITS == 4 && symmetric && narrow_fits(M, N);
+  const bool narrow = narrow_fits(M, N, cap);
   const int rows_wg = narrow ? 64 : 128;
   dim3 grid((unsigned)((N + rows_wg - 1) / rows_wg),
             (unsigned)((M + 16 * mt16 - 1) / (16 * mt16)));
 #define LOGBQ_M2(MT, ST, PR) hipLaunchKernelGGL((k_mfma2<BITS, MT, ST, PR, (MT <= 2)>), grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
-#define LOGBQ_M2N(MT) hipLaunchKernelGGL((k_mfma2_narrow<MT, (MT <= 2)>), grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
+#define LOGBQ_M2N(MT, PR) hipLaunchKernelGGL((k_mfma2_narrow<BITS, MT, PR, (MT <= 2)>), grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
   if constexpr (BITS == 4) {
     // Register dequantization whenever the codebook allows it: measured 1 to 2.5 us faster than
     // the LDS table at m = 4 .. 32 on the 8192 x 28672 layer, with bit-identical results.
-    if (narrow) {
+    if (narrow && symmetric) {
       switch (mt16) {
-        case 1: LOGBQ_M2N(1); break;
-        case 2: LOGBQ_M2N(2); break;
-        case 3: LOGBQ_M2N(3); break;
-        case 4: LOGBQ_M2N(4); break;
-        case 5: LOGBQ_M2N(5); break;
-        case 6: LOGBQ_M2N(6); break;
-        case 7: LOGBQ_M2N(7); break;
-        default: LOGBQ_M2N(8); break;
+        case 1: LOGBQ_M2N(1, false); break;
+        case 2: LOGBQ_M2N(2, false); break;
+        case 3: LOGBQ_M2N(3, false); break;
+        case 4: LOGBQ_M2N(4, false); break;
+        case 5: LOGBQ_M2N(5, false); break;
+        case 6: LOGBQ_M2N(6, false); break;
+        case 7: LOGBQ_M2N(7, false); break;
+        default: LOGBQ_M2N(8, false); break;
+      }
+    } else if (narrow) {
+      switch (mt16) {
+        case 1: LOGBQ_M2N(1, true); break;
+        case 2: LOGBQ_M2N(2, true); break;
+        case 3: LOGBQ_M2N(3, true); break;
+        default: LOGBQ_M2N(4, true); break;
       }
     } else if (symmetric) {
       switch (mt16) {
@@ -2257,6 +2269,13 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
         case 3: LOGBQ_M2(3, 4, true); break;
         default: LOGBQ_M2(4, 4, true); break;
       }
+    }
+  } else if (narrow) {
+    switch (mt16) {
+      case 1: LOGBQ_M2N(1, true); break;
+      case 2: LOGBQ_M2N(2, true); break;
+      case 3: LOGBQ_M2N(3, true); break;
+      default: LOGBQ_M2N(4, true); break;
     }
   } else {
     switch (mt16) {
@@ -3051,9 +3070,9 @@ int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const
       int mt16 = (M + 15) / 16;
       const int cap = symmetric ? 8 : 4;
       if (mt16 > cap) mt16 = cap;
-      if (bits == 4 && symmetric && narrow_fits(M, n))
-        std::snprintf(buf, sizeof(buf), "k_mfma2_narrow<%d, %s>", mt16,
-                      mt16 <= 2 ? "true" : "false");
+      if (narrow_fits(M, n, cap))
+        std::snprintf(buf, sizeof(buf), "k_mfma2_narrow<%d, %d, %s, %s>", bits, mt16,
+                      symmetric ? "false" : "true", mt16 <= 2 ? "true" : "false");
       else
         std::snprintf(buf, sizeof(buf), "k_mfma2<%d, %d, 4, %s, %s>", bits, mt16,
                       symmetric ? "false" : "true", mt16 <= 2 ? "true" : "false");

@@ -304,24 +304,28 @@ def test_linear_kernel_names():
     # 64-row workgroups where the whole grid fits on the chip (at most 256 workgroups)
     assert lk(4, 9, 14336, 4096) == "k_mfma_sk<16, 14, 1, 1, 2, false>"
     assert lk(4, 17, 14336, 4096) == "k_mfma_sk<16, 14, 1, 1, 2, false>"   # first of 2 launches
-    assert lk(4, 49, 14336, 4096) == "k_mfma2_narrow<4, false>"
-    assert lk(4, 64, 4096, 4096) == "k_mfma2_narrow<4, false>"
-    assert lk(4, 33, 4096, 16384) == "k_mfma2_narrow<3, false>"
+    assert lk(4, 49, 14336, 4096) == "k_mfma2_narrow<4, 4, false, false>"
+    assert lk(4, 64, 4096, 4096) == "k_mfma2_narrow<4, 4, false, false>"
+    assert lk(4, 33, 4096, 16384) == "k_mfma2_narrow<4, 3, false, false>"
     assert lk(4, 33, 4096, 16385) == "k_mfma2<4, 3, 4, false, false>"
-    assert lk(4, 128, 4096, 4096) == "k_mfma2_narrow<8, false>"
-    assert lk(4, 129, 1024, 8192) == "k_mfma2_narrow<8, false>"
+    assert lk(4, 128, 4096, 4096) == "k_mfma2_narrow<4, 8, false, false>"
+    assert lk(4, 129, 1024, 8192) == "k_mfma2_narrow<4, 8, false, false>"
     assert lk(4, 129, 1024, 8256) == "k_mfma_kq"
     assert lk(8, 1, 8192, 28672) == "k_gemv<8, 1, 8, false, 2>"
     assert lk(8, 128, 8192, 28672) == "k_mfma_kq8" and lk(8, 128, 4096, 14336) == "k_mfma2<8, 4, 4, true, false>"
+    assert lk(8, 64, 4096, 14336) == "k_mfma2_narrow<8, 4, true, false>"
+    assert lk(8, 32, 8192, 28672) == "k_mfma2<8, 2, 4, true, true>"
     assert lk(8, 8, 8192, 28672) == "k_mfma_sk8<16, 2>" and lk(8, 12, 4096, 4096) == "k_mfma_sk8<8, 1>"
     assert lk(4, 0, 8192, 28672) == "none" and lk(4, 3, 0, 5) == "k_fill_zero"
     # a codebook that is not sign-symmetric takes the LDS table
     cb = np.arange(16, dtype=np.float32)
     assert lk(4, 8, 8192, 28672, cb) == "k_mfma_sk<32, 8, 1, 1, 1, true>"
-    assert lk(4, 32, 4096, 14336, cb) == "k_mfma2<4, 2, 4, true, true>"   # above m = 16
-    assert lk(4, 4, 14336, 4096, cb) == "k_mfma2<4, 1, 4, true, true>"    # and at K = 14336
+    assert lk(4, 32, 4096, 14336, cb) == "k_mfma2_narrow<4, 2, true, true>"   # above m = 16
+    assert lk(4, 4, 14336, 4096, cb) == "k_mfma2_narrow<4, 1, true, true>"    # and at K = 14336
     assert lk(4, 128, 8192, 28672, cb) == "k_mfma2<4, 4, 4, true, false>"
-    assert lk(4, 64, 4096, 4096, cb) == "k_mfma2<4, 4, 4, true, false>"
+    assert lk(4, 64, 4096, 4096, cb) == "k_mfma2_narrow<4, 4, true, false>"
+    assert lk(4, 65, 4096, 16384, cb) == "k_mfma2<4, 4, 4, true, false>"   # two 64-row blocks
+    assert lk(4, 64, 4096, 16384, cb) == "k_mfma2_narrow<4, 4, true, false>"
     sym = np.array([0] + [2.0 ** k for k in range(1, 8)] + [0] + [-(2.0 ** k) for k in range(1, 8)],
                    dtype=np.float32)
     assert lk(4, 128, 8192, 28672, sym) == "k_mfma_kq"

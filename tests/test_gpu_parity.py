@@ -460,23 +460,34 @@ def test_linear_stepped_narrow():
             assert rel_err(y.cpu().numpy(), x, wh) <= 2.5e-4
 
 
-def test_linear_stepped_narrow_equals_wide():
+@pytest.mark.parametrize("kind", ["fitted4", "table4", "fitted8"])
+def test_linear_stepped_narrow_equals_wide(kind):
     """Both stepped kernels give every output the same K walk, so they agree bit for bit: a
     16385-row linear (257 workgroups of 64 rows would not fit, so 128-row workgroups) against
-    its first 16384 rows (256 workgroups of 64 rows)."""
+    its first 16384 rows (256 workgroups of 64 rows), with register tables (a fitted 4-bit
+    codebook) and with the LDS table (a 4-bit codebook that is not sign-symmetric, and 8-bit
+    codes)."""
     n, k = 16385, 3072
-    w, p, _ = prepare(64, 256, [8, 26, 0, 0])
-    _, cb = gpu_encode(w, p)
+    bits = 8 if kind == "fitted8" else 4
+    w, _, _ = prepare(64, 256, [8, 26, 0, 0])
+    if kind == "table4":
+        cb = torch.linspace(-0.07, 0.08, 16, dtype=torch.float32)
+    else:
+        p = L.fit(w, 8, 1e-6) if bits == 8 else L.fit(w)
+        _, cb = gpu_encode(w, p)
+    lin = L.linear8 if bits == 8 else L.linear
     gen = torch.Generator(device=DEV)
     gen.manual_seed(26)
-    c = torch.randint(0, 256, (n, k // 2), dtype=torch.uint8, device=DEV, generator=gen)
-    for m in (9, 24, 33, 64, 96):
-        wide, narrow = L.linear_kernel(4, m, k, n), L.linear_kernel(4, m, k, n - 1)
-        _say(f"stepped wide {wide} vs narrow {narrow}, k={k} m={m}")
+    c = torch.randint(0, 256, (n, k * bits // 8), dtype=torch.uint8, device=DEV, generator=gen)
+    cbh = None if kind == "fitted4" else np.asarray(cb, dtype=np.float32)
+    for m in ((9, 24, 33, 64, 96) if kind == "fitted4" else (9, 24, 33, 64)):
+        wide = L.linear_kernel(bits, m, k, n, cbh)
+        narrow = L.linear_kernel(bits, m, k, n - 1, cbh)
+        _say(f"stepped {kind} wide {wide} vs narrow {narrow}, k={k} m={m}")
         assert wide.startswith("k_mfma2<") and narrow.startswith("k_mfma2_narrow<")
         x = torch.from_numpy(inputs.activations(m, k, seed=[8, 26, 1, m])).to(DEV)
-        y = L.linear(x, c, cb)
-        y1 = L.linear(x, c[: n - 1], cb)
+        y = lin(x, c, cb)
+        y1 = lin(x, c[: n - 1], cb)
         torch.cuda.synchronize()
         assert torch.isfinite(y).all()
         assert torch.equal(y[:, : n - 1], y1)
