@@ -461,6 +461,44 @@ def read_ceiling(torch, stream, nbytes=1 << 32, steps=20, warmup=10):
             "kernel": "k_read (libhbmread.so), 4 KiB per wavefront unit, 2 units in flight"}
 
 
+def bench_batched(torch, L, inputs, dev, stream, ms, steps, warmup):
+    """The distinct linear shapes of the 8B-shaped decoder layer (o: 4096 x 4096, gate/up:
+    4096 -> 14336, down: 14336 -> 4096) run one at a time at batch sizes above decode (the
+    split-K kernel, the stepped kernel with 64-row workgroups or the K-quartered kernel,
+    whichever the path rule takes), codes rotated over copies larger than the last-level
+    cache, all rows chained on one stream."""
+    wl = inputs.WORKLOADS["decode_8b_32x7"]
+    shapes = [lin for lin in wl["layers"] if lin.name in ("o", "gate", "down")]
+    plan, keys = [], []
+    for lin in shapes:
+        log(f"batched {lin.name} {lin.k}->{lin.n}: generate / fit / encode")
+        codes, cb = make_tensor(torch, L, inputs, lin, wl, [wl["cfg"], 1, inputs.PROJ[lin.name], 0],
+                                dev)
+        packed = lin.n * lin.k // 2
+        copies = max(2, -(-ROTATE_BYTES // packed))
+        code_list = [codes] + [codes.clone() for _ in range(copies - 1)]
+        for m in ms:
+            x = inputs.activations(m, lin.k, seed=[wl["cfg"], 1, inputs.PROJ[lin.name], m],
+                                   device=dev)
+            launches = [(x, c, cb, torch.empty((m, lin.n), dtype=torch.float32, device=dev))
+                        for c in code_list]
+            plan.append((launches, steps, warmup))
+            keys.append((lin, m, packed, cb))
+    times = time_chain(torch, L, stream, plan)
+    out = {}
+    for (lin, m, packed, cb), (_, timed, warm), t in zip(keys, plan, times):
+        algo = packed + 2 * m * lin.k + 4 * m * lin.n + 64
+        flops = 2.0 * m * lin.n * lin.k
+        log(f"batched {lin.name} m={m}: {t * 1e3:.2f} us per launch")
+        out[f"{lin.name}_{lin.k}x{lin.n}_m{m}"] = {
+            "us": t * 1e3, "launches_timed": timed, "warmup_launches": warm,
+            "algo_GB_s": algo / t / 1e6, "hbm_frac": algo / t / 1e6 / HBM_PEAK_GBS,
+            "TFLOP_s": flops / t / 1e9, "mfma_frac": flops / t / 1e9 / MFMA_F16_PEAK_TFLOPS,
+            "path": L.linear_path(4, m, lin.k, lin.n),
+            "kernel": L.linear_kernel(4, m, lin.k, lin.n, cb)}
+    return out
+
+
 def bench_small(torch, L, inputs, dev, stream, name, steps, warmup):
     wl = inputs.WORKLOADS[name]
     lin = wl["layers"][0]
@@ -720,10 +758,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=10000,
                     help="untimed launches before the timed ones (about 0.2 s of GPU work at M = 1)")
     ap.add_argument("--quick", action="store_true", help="main layer only, no extra rows")
-    ap.add_argument("--rows", default="layer,layer8,small,decode1b,decode8b,quality,gptq",
+    ap.add_argument("--rows", default="layer,layer8,small,decode1b,decode8b,batched,quality,gptq",
                     help="comma list of extra rows: layer (M sweep + encode), layer8 (the same "
-                         "layer at 8 bits), small, decode1b, decode8b, quality (LogbQuant "
-                         "against the asymmetric linear baseline), gptq (calibration)")
+                         "layer at 8 bits), small, decode1b, decode8b, batched (the 8B-shaped "
+                         "layer's linears at m = 16 .. 128), quality (LogbQuant against the "
+                         "asymmetric linear baseline), gptq (calibration)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=0,
                     help="timed (and warmup) passes of each decode row (default 200 for the "
@@ -799,6 +838,11 @@ def main():
         n8 = args.decode_steps or 100
         rows["decode_8b_32x7"] = bench_decode(torch, L, inputs, dev, stream, "decode_8b_32x7",
                                               [1, 4], n8, n8)
+        torch.cuda.empty_cache()
+    if "batched" in want:
+        bs, bw = aux_counts(args.steps, args.warmup)
+        rows["batched_8b_linears"] = bench_batched(torch, L, inputs, dev, stream,
+                                                   [16, 32, 64, 128], bs, bw)
         torch.cuda.empty_cache()
 
     cpu = None
