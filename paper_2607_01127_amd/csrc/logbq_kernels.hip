@@ -1960,12 +1960,28 @@ __global__ __launch_bounds__(kFitThreads) void k_fit_hist(const float* __restric
   const int64_t begin = (int64_t)blockIdx.x * C;   // C <= fit_chunk_max(PASS), a multiple of 4
   const int64_t end = n - begin < C ? n : begin + C;
   const int64_t vend = begin + ((end - begin) & ~int64_t(3));
-  for (int64_t i = begin + 4 * t; i < vend; i += 4 * kFitThreads) {
-    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(w + i));
-    add(v.x);
-    add(v.y);
-    add(v.z);
-    add(v.w);
+  // Passes 1 and 2 take U = 4 vectors per thread per iteration, all requested before any is
+  // binned (pass 1 waits on its LDS atomics, and with two workgroups per CU one vector in
+  // flight per thread left HBM idle: 263 -> 244 us and 196 -> 182 us per pass on the
+  // 8192 x 28672 tensor, MI355X); pass 3 bins almost nothing and streams best with U = 1.
+  constexpr int U = PASS == 3 ? 1 : 4;
+  for (int64_t i0 = begin + 4 * t; i0 < vend; i0 += 4 * kFitThreads * U) {
+    u32x4 v[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int64_t i = i0 + (int64_t)j * 4 * kFitThreads;
+      v[j] = i < vend ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(w + i))
+                      : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      if (i0 + (int64_t)j * 4 * kFitThreads < vend) {
+        add(v[j].x);
+        add(v[j].y);
+        add(v[j].z);
+        add(v[j].w);
+      }
+    }
   }
   if (vend + t < end) add(__float_as_uint(w[vend + t]));
   if (PASS == 1) {
