@@ -275,7 +275,8 @@ def test_linear_deterministic_and_empty():
 
 def test_linear_arbitrary_codebook():
     """Any 16 finite floats work as a codebook (the table-lookup kernels); a fitted codebook is
-    sign-symmetric and takes the register-dequant MFMA path, any other takes the pair table."""
+    sign-symmetric and takes the register-dequant MFMA path, any other takes the pair table
+    (at K = 14336 above m = 16 the stepped kernel in one launch, not 16-row split-K launches)."""
     rng = np.random.default_rng(12)
     n = 300
     for k in (1024, 2048, 4096, 8192, 14336):
@@ -284,7 +285,7 @@ def test_linear_arbitrary_codebook():
         for trial in range(2):
             cb = rng.standard_normal(16).astype(np.float32) * np.float32(10.0 ** (3 * trial - 2))
             wh = O.dequantize(codes_np, cb)
-            for m in ((1, 5, 16, 33, 128) if k == 1024 else (5, 16)):
+            for m in ((1, 5, 16, 33, 128) if k == 1024 else (5, 16, 24) if k == 14336 else (5, 16)):
                 _say(f"arbitrary codebook k={k} trial {trial} m={m}")
                 x = inputs.activations(m, k, seed=[8, 9, trial, m + k])
                 y = L.linear(torch.from_numpy(x).to(DEV), codes, cb)
