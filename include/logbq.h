@@ -194,10 +194,14 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  * runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and shapes whose
  * activations do not fit the GEMV's registers) runs the stepped dequantize-into-MFMA skinny
  * GEMM, except m > 96 at n >= 4096, which runs a K-quartered MFMA GEMM for sign-symmetric
- * codebooks unless ceil(n / 64) * ceil(m / 128) <= 256. The stepped kernel runs with 64-row
- * workgroups wherever its whole grid is then on the chip at once (ceil(n / 64) times its
- * batch blocks of 128 rows, 64 for 8-bit codes and codebooks that are not sign-symmetric, at
- * most 256). logbq_linear_path reports the choice. Results are deterministic for every path.
+ * codebooks unless ceil(n / 64) * ceil(m / 128) <= 256. For 8-bit codes and codebooks that
+ * are not sign-symmetric the stepped kernel runs with 64-row workgroups wherever its whole
+ * grid is then on the chip at once (ceil(n / 64) times its batch blocks of 64 rows, at most
+ * 256), else 128-row ones. For sign-symmetric codebooks it runs in the launch shape a cost
+ * model rates cheapest among those whose grid is on the chip at once: 64- or 128-row
+ * workgroups, batch blocks of 16 to 128 rows, and K in one part or (from k = 4096) in two,
+ * where y is zeroed first and each part adds into it. logbq_linear_path reports the path, and
+ * logbq_linear_kernel the kernel. Results are deterministic for every path.
  * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment, or k >= 2^24 on
  * the stepped or K-quartered MFMA kernel), HIP.
  */

@@ -913,6 +913,15 @@ __device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
   static_assert(STAGES % 2 == 0, "the loop is unrolled by STAGES and alternates two tiles");
   static_assert(BITS == 4 || PAIRS, "8-bit codes are dequantized through the LDS table");
   static_assert(W == 8 || W == 4, "8 or 4 wavefronts");
+  // K parts: workgroup z of gridDim.z takes the steps [z per_z, +per_z) (the last part may be
+  // shorter) and adds its partial products into y, which the host has zeroed. The host splits
+  // K in at most two parts, so every output receives exactly two adds and 0 + a + b rounds the
+  // same in either order.
+  const int nsteps_all = (k_cols + kM2Step - 1) / kM2Step;
+  const int per_z = (nsteps_all + (int)gridDim.z - 1) / (int)gridDim.z;
+  const int s_lo = (int)blockIdx.z * per_z;
+  const int nsteps = per_z < nsteps_all - s_lo ? per_z : nsteps_all - s_lo;
+  if (nsteps <= 0) return;
   constexpr int NT = 64 * W;             // threads
   constexpr int ROWS = 16 * W;           // weight rows per workgroup
   constexpr int XV = MT * 512 / NT;      // activation vectors per thread per step
@@ -932,7 +941,6 @@ __device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
   const int g = lane >> 4;
   const int n0 = blockIdx.x * ROWS + wave * 16;
   const int mb = blockIdx.y * (MT * 16);
-  const int nsteps = (k_cols + kM2Step - 1) / kM2Step;
   const int64_t row_bytes = (int64_t)k_cols * BITS / 8;
   // One buffer descriptor over the workgroup's rows (rows past n_rows read as zeros and are
   // not stored). Buffer loads keep the code prefetch where it is issued: plain loads of the
@@ -945,6 +953,7 @@ __device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
   const int row = n0 + j;
   const int crow = (wave * 16 + j) * (int)row_bytes;   // this lane's row in the descriptor
 
+  // Steps below are counted within the workgroup's K part (global step s_lo + step).
   // Activation tile of a step: MT*16 rows x 256 halves = MT*512 vectors of 16 bytes, XV per
   // thread. Loads are clamped in bounds; entries past m_rows / k_cols are zeroed when written.
   auto load_x = [&](int step, u32x4 (&v)[XV]) {
@@ -952,7 +961,7 @@ __device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
     for (int i = 0; i < XV; ++i) {
       const int idx = t + NT * i;
       const int m = mb + (idx >> 5);
-      const int kk = step * kM2Step + (idx & 31) * 8;
+      const int kk = (s_lo + step) * kM2Step + (idx & 31) * 8;
       const int mc = m < m_rows ? m : m_rows - 1;
       const int kc = kk < k_cols ? kk : k_cols - 8;
       v[i] = *(GlobalU32x4)((const __attribute__((address_space(1))) uint16_t*)x +
@@ -964,7 +973,7 @@ __device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
     for (int i = 0; i < XV; ++i) {
       const int idx = t + NT * i;
       const uint32_t keep = 0u - (uint32_t)((mb + (idx >> 5) < m_rows) &
-                                            (step * kM2Step + (idx & 31) * 8 < k_cols));
+                                            ((s_lo + step) * kM2Step + (idx & 31) * 8 < k_cols));
       u32x4 w = PAIRS ? v[i] : permute_x8(v[i]);
       w.x &= keep; w.y &= keep; w.z &= keep; w.w &= keep;
       const int r = idx >> 5;
@@ -983,12 +992,12 @@ __device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
     for (int c = 0; c < CB; ++c) {
       if (COAL) {
         const int r = wave * 16 + RPI * c + lane / (RB / 16);
-        int off = step * RB + 16 * (lane % (RB / 16));
+        int off = (s_lo + step) * RB + 16 * (lane % (RB / 16));
         off = off + 16 <= (int)row_bytes ? off : (int)row_bytes - 16;
         q[c] = __builtin_amdgcn_raw_buffer_load_b128(crs, r * (int)row_bytes + off, 0,
                                                      kCachePolicyNT);
       } else {
-        int off = step * RB + (RB / 4) * g + 16 * c;
+        int off = (s_lo + step) * RB + (RB / 4) * g + 16 * c;
         off = off + 16 <= (int)row_bytes ? off : (int)row_bytes - 16;
         q[c] = __builtin_amdgcn_raw_buffer_load_b128(crs, crow + off, 0, kCachePolicyNT);
       }
@@ -1093,7 +1102,10 @@ __device__ __forceinline__ void mfma2_body(const uint8_t* __restrict__ codes,
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int m = mb + mt * 16 + 4 * g + r;
-      if (m < m_rows && row < n_rows) y[(int64_t)m * n_rows + row] = acc[mt][r] * scale;
+      if (m < m_rows && row < n_rows) {
+        if (gridDim.z > 1) unsafeAtomicAdd(&y[(int64_t)m * n_rows + row], acc[mt][r] * scale);
+        else y[(int64_t)m * n_rows + row] = acc[mt][r] * scale;
+      }
     }
 }
 
@@ -2215,11 +2227,66 @@ constexpr int64_t kMaxBatchRows = 65535LL * 64;
 // 4096 x 4096 at m = 48: 40.9 -> 27.0 us, 8192 x 8192 at m = 64: 86.0 -> 59.1 us; 4-bit
 // 4096 x 4096 at m = 64: 30.1 -> 21.0 us); at N = 28672 (448 workgroups) 1.04-1.44 times the
 // time. `cap` is the kernel's batch tiles per workgroup column (8 with register tables, 4 with
-// the LDS table).
+// the LDS table). With register tables this rule now only decides between the stepped and the
+// K-quartered kernel; step_config below picks the stepped kernel's shape.
 constexpr int64_t kNarrowMaxWorkgroups = 256;
 bool narrow_fits(int M, int64_t N, int cap = 8) {
   const int64_t gy = M > 16 * cap ? (M + 16 * cap - 1) / (16 * cap) : 1;
   return ((N + 63) / 64) * gy <= kNarrowMaxWorkgroups;
+}
+
+// Launch shape of the stepped kernel: 64-row (narrow) or 128-row workgroups, batch tiles of 16
+// rows per workgroup column, and K in one or two parts (two: the output is zeroed first and each
+// part adds into it).
+struct StepCfg {
+  bool narrow;
+  int mt16;
+  int ks;
+};
+// Codebooks that take the LDS table keep the rule above: batch tiles up to the cap, 64-row
+// workgroups when their grid fits on the chip, one K part. With register tables (sign-symmetric
+// 4-bit codebooks) the shape is the cheapest, by a cost model, of every shape whose grid fits
+// on the chip at once (at most one workgroup per CU): 64 or 128 rows, t = t0, t0 / 2, ... 1
+// batch tiles (halving rounds up; t0 = min(ceil(m / 16), 8)), one K part, or two when K has at
+// least 16 steps of 256. A workgroup's time is its steps times a per-step time that grows with
+// t (activation staging, MFMAs and LDS reads) on top of a fixed part (code loads and
+// dequantization); two K parts add a fixed cost (the zeroing launch, the atomic adds, a shorter
+// pipeline). The constants are fitted to MI355X measurements (graph replay, codes streamed from
+// HBM) of 64- and 128-row workgroups at t = 1 .. 8 on 14336 x 4096, 4096 x 14336, 4096 x 4096,
+// 2048 x 8192 and 1024 x 4096. Against 64-row workgroups with all t0 tiles and one K part,
+// e.g.: 4096 x 14336 at m = 128 (128 rows, t = 2, two parts) 109.9 -> 35.9 us, at m = 64
+// (64 rows, t = 2, two parts) 65.1 -> 27.8 us; 4096 x 4096 at m = 256 (128 rows, t = 2)
+// 34.8 -> 20.1 us; 14336 x 4096 at m = 128 (128 rows, t = 4) 37.2 -> 30.3 us; 2048 x 8192 at
+// m = 64 (64 rows, t = 1, two parts) 38.3 -> 13.7 us. Where no shape fits (N = 28672) the rule
+// above stands.
+constexpr double kStepFixed128 = 0.500, kStepTile128 = 0.300;   // us per step of 256
+constexpr double kStepFixed64 = 0.376, kStepTile64 = 0.184;
+constexpr double kTwoPartsCost = 5.0;                            // us
+StepCfg step_config(int M, int64_t N, int K, bool symmetric) {
+  const int cap = symmetric ? 8 : 4;
+  int t0 = (M + 15) / 16;
+  if (t0 > cap) t0 = cap;
+  StepCfg best{narrow_fits(M, N, cap), t0, 1};
+  if (!symmetric) return best;
+  const int64_t nsteps = ((int64_t)K + kM2Step - 1) / kM2Step;
+  double best_cost = -1.0;
+  for (int rows = 128; rows >= 64; rows /= 2)
+    for (int mt = t0;; mt = (mt + 1) / 2) {
+      for (int ks = 1; ks <= (nsteps >= 16 ? 2 : 1); ++ks) {
+        const int64_t wgs = ((N + rows - 1) / rows) * ((M + 16 * mt - 1) / (16 * mt)) * ks;
+        if (wgs > kNarrowMaxWorkgroups) continue;
+        const double per_step = rows == 128 ? kStepFixed128 + mt * kStepTile128
+                                            : kStepFixed64 + mt * kStepTile64;
+        const double cost = (double)((nsteps + ks - 1) / ks) * per_step +
+                            (ks == 2 ? kTwoPartsCost : 0.0);
+        if (best_cost < 0.0 || cost < best_cost) {
+          best_cost = cost;
+          best = {rows == 64, mt, ks};
+        }
+      }
+      if (mt == 1) break;
+    }
+  return best;
 }
 
 template <int BITS>
@@ -2237,13 +2304,19 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
   make_lut<BITS>(j.codebook, &lut, &scale);
   // Batch tiles of 16 rows: up to 8 per workgroup column (128 rows). Up to 4 tiles use the
   // LDS table; more tiles leave LDS to the activation ring and dequantize in registers.
-  int mt16 = (M + 15) / 16;
-  const int cap = symmetric ? 8 : 4;
-  if (mt16 > cap) mt16 = cap;
-  const bool narrow = narrow_fits(M, N, cap);
+  const StepCfg cfg = step_config(M, N, K, symmetric);
+  const int mt16 = cfg.mt16;
+  const bool narrow = cfg.narrow;
   const int rows_wg = narrow ? 64 : 128;
   dim3 grid((unsigned)((N + rows_wg - 1) / rows_wg),
-            (unsigned)((M + 16 * mt16 - 1) / (16 * mt16)));
+            (unsigned)((M + 16 * mt16 - 1) / (16 * mt16)), (unsigned)cfg.ks);
+  if (cfg.ks > 1) {
+    const int cus = device_cus();
+    if (cus <= 0) return LOGBQ_ERR_HIP;
+    const int64_t cnt = (int64_t)M * N;
+    hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)grid_for(cnt, 256, (int64_t)cus * 16)),
+                       dim3(256), 0, st, j.y, cnt);
+  }
 #define LOGBQ_M2(MT, ST, PR) hipLaunchKernelGGL((k_mfma2<BITS, MT, ST, PR, (MT <= 2)>), grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
 #define LOGBQ_M2N(MT, PR) hipLaunchKernelGGL((k_mfma2_narrow<BITS, MT, PR, (MT <= 2)>), grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
   if constexpr (BITS == 4) {
@@ -3083,10 +3156,9 @@ int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const
     } else if (path == LOGBQ_PATH_MFMA_KQ && symmetric) {
       std::snprintf(buf, sizeof(buf), "k_mfma_kq");
     } else {
-      int mt16 = (M + 15) / 16;
-      const int cap = symmetric ? 8 : 4;
-      if (mt16 > cap) mt16 = cap;
-      if (narrow_fits(M, n, cap))
+      const StepCfg cfg = step_config(M, n, K, symmetric);
+      const int mt16 = cfg.mt16;
+      if (cfg.narrow)
         std::snprintf(buf, sizeof(buf), "k_mfma2_narrow<%d, %d, %s, %s>", bits, mt16,
                       symmetric ? "false" : "true", mt16 <= 2 ? "true" : "false");
       else

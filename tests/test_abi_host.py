@@ -11,6 +11,7 @@ import pytest
 from oracle import logbq_oracle as O
 from paper_2607_01127_amd import inputs
 from paper_2607_01127_amd import logbq as L
+from stepped_rule import stepped_name, stepped_shape
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "logbq.h")
 
@@ -278,6 +279,24 @@ def test_linear_path_rule():
             lp(*bad)
 
 
+def test_stepped_shape_rule():
+    """The library's stepped-kernel launch shapes agree with the rule stated above on every
+    shape of a grid (ragged n, k from 1 to 56 steps, m from 3 to 256) that takes that kernel,
+    and every chosen grid fits on the chip when one can."""
+    seen = set()
+    for k in (1024, 2048, 3072, 4096, 8192, 14336):
+        for n in (64, 1000, 2048, 4097, 8192, 14336, 16385, 28672):
+            for m in (3, 9, 17, 33, 48, 64, 65, 96, 97, 128, 129, 200, 256):
+                if L.linear_path(4, m, k, n) != "mfma":
+                    continue
+                assert L.linear_kernel(4, m, k, n) == stepped_name(m, k, n), (m, k, n)
+                narrow, t, parts = stepped_shape(m, k, n)
+                wgs = -(-n // (64 if narrow else 128)) * -(-m // (16 * t)) * parts
+                assert wgs <= 256 or (-(-n // 128)) * -(-m // 128) > 256 or not narrow
+                seen.add((narrow, parts))
+    assert seen == {(True, 1), (True, 2), (False, 1), (False, 2)}
+
+
 def test_linear_kernel_names():
     """The kernel instance a call runs, named as the profiler lists it (host logic)."""
     lk = L.linear_kernel
@@ -301,16 +320,22 @@ def test_linear_kernel_names():
     assert lk(4, 12, 4096, 2048) == "k_mfma_sk<8, 16, 1, 1, 1, false>"
     assert lk(4, 32, 8192, 28672) == "k_mfma2<4, 2, 4, false, true>"
     assert lk(4, 128, 8192, 28672) == "k_mfma_kq"
-    # 64-row workgroups where the whole grid fits on the chip (at most 256 workgroups)
     assert lk(4, 9, 14336, 4096) == "k_mfma_sk<16, 14, 1, 1, 2, false>"
     assert lk(4, 17, 14336, 4096) == "k_mfma_sk<16, 14, 1, 1, 2, false>"   # first of 2 launches
-    assert lk(4, 49, 14336, 4096) == "k_mfma2_narrow<4, 4, false, false>"
-    assert lk(4, 64, 4096, 4096) == "k_mfma2_narrow<4, 4, false, false>"
+    # register tables: the cheapest launch shape whose grid fits on the chip (cost model)
+    assert lk(4, 49, 14336, 4096) == "k_mfma2_narrow<4, 2, false, true>"
+    assert lk(4, 64, 4096, 4096) == "k_mfma2_narrow<4, 1, false, true>"
+    assert lk(4, 128, 4096, 4096) == "k_mfma2_narrow<4, 2, false, true>"
+    assert lk(4, 128, 14336, 4096) == "k_mfma2<4, 2, 4, false, true>"
+    assert lk(4, 256, 4096, 4096) == "k_mfma2<4, 2, 4, false, true>"
+    assert lk(4, 64, 4096, 14336) == "k_mfma2<4, 2, 4, false, true>"
+    assert lk(4, 128, 4096, 14336) == "k_mfma2<4, 4, 4, false, false>"
     assert lk(4, 33, 4096, 16384) == "k_mfma2_narrow<4, 3, false, false>"
     assert lk(4, 33, 4096, 16385) == "k_mfma2<4, 3, 4, false, false>"
-    assert lk(4, 128, 4096, 4096) == "k_mfma2_narrow<4, 8, false, false>"
-    assert lk(4, 129, 1024, 8192) == "k_mfma2_narrow<4, 8, false, false>"
+    assert lk(4, 129, 1024, 8192) == "k_mfma2<4, 4, 4, false, false>"
     assert lk(4, 129, 1024, 8256) == "k_mfma_kq"
+    for m, k, n in ((64, 8192, 28672), (96, 8192, 28672), (48, 8192, 16385), (200, 2048, 1000)):
+        assert lk(4, m, k, n) == stepped_name(m, k, n), (m, k, n)
     assert lk(8, 1, 8192, 28672) == "k_gemv<8, 1, 8, false, 2>"
     assert lk(8, 128, 8192, 28672) == "k_mfma_kq8" and lk(8, 128, 4096, 14336) == "k_mfma2<8, 4, 4, true, false>"
     assert lk(8, 64, 4096, 14336) == "k_mfma2_narrow<8, 4, true, false>"

@@ -13,6 +13,7 @@ import pytest
 from oracle import logbq_oracle as O
 from paper_2607_01127_amd import inputs
 from paper_2607_01127_amd import logbq as L
+from stepped_rule import stepped_name, stepped_shape
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -434,22 +435,27 @@ def test_linear_split_k_14336():
         assert torch.equal(ys[0], y) and torch.equal(ys[1], y3)
 
 
-def test_linear_stepped_narrow():
-    """The stepped MFMA kernel with 64-row workgroups (taken when its whole grid fits on the
-    chip, at most 256 workgroups): ragged row counts, K outside the split-K set (3072) and in
-    it, m from 9 to 200 (one to eight batch tiles, two batch blocks above 128). y is prefilled
-    with NaN, each call is repeated and must give the same bits."""
-    for n, k in ((1000, 3072), (4097, 2048)):
+def test_linear_stepped_shapes():
+    """The stepped MFMA kernel in the launch shapes its cost model picks: 64- and 128-row
+    workgroups, one to eight batch tiles, K in one part or in two (outputs zeroed, then two
+    atomic adds each), ragged row counts (1000, 2049, 4097), K outside the split-K set (3072)
+    and in it, m from 9 to 200 (two batch blocks above 128). y is prefilled with NaN, each call
+    is repeated and must give the same bits, and every output is within tolerance of the
+    oracle."""
+    parts_seen = set()
+    for n, k in ((1000, 3072), (4097, 2048), (1000, 8192), (2049, 8192)):
         w, p, r = prepare(n, k, [8, 25, k % 1000, n])
         c, cb = gpu_encode(w, p)
         wh = O.dequantize(O.encode(w, r.base, r.shift), O.codebook(r.base, r.shift))
         del w
         for m in (9, 24, 33, 64, 96, 97, 128, 129, 200):
-            if k == 2048 and m <= 32:
+            if L.linear_path(4, m, k, n) != "mfma":
                 continue   # split-K territory
             name = L.linear_kernel(4, m, k, n)
-            _say(f"stepped narrow n={n} k={k} m={m} kernel {name}")
-            assert name.startswith("k_mfma2_narrow<"), name
+            narrow, tiles, parts = stepped_shape(m, k, n)
+            _say(f"stepped n={n} k={k} m={m} kernel {name} K parts {parts}")
+            assert name == stepped_name(m, k, n), name
+            parts_seen.add((narrow, parts))
             x = inputs.activations(m, k, seed=[8, 25, n, m])
             xd = torch.from_numpy(x).to(DEV)
             y = torch.full((m, n), float("nan"), dtype=torch.float32, device=DEV)
@@ -459,15 +465,17 @@ def test_linear_stepped_narrow():
             assert torch.isfinite(y).all()
             assert torch.equal(y, y2)
             assert rel_err(y.cpu().numpy(), x, wh) <= 2.5e-4
+    assert parts_seen == {(True, 1), (True, 2), (False, 1), (False, 2)}
 
 
 @pytest.mark.parametrize("kind", ["fitted4", "table4", "fitted8"])
 def test_linear_stepped_narrow_equals_wide(kind):
-    """Both stepped kernels give every output the same K walk, so they agree bit for bit: a
-    16385-row linear (257 workgroups of 64 rows would not fit, so 128-row workgroups) against
-    its first 16384 rows (256 workgroups of 64 rows), with register tables (a fitted 4-bit
-    codebook) and with the LDS table (a 4-bit codebook that is not sign-symmetric, and 8-bit
-    codes)."""
+    """With K in one part every launch shape gives every output the same K walk, so shapes
+    agree bit for bit: a 16385-row linear (257 workgroups of 64 rows would not fit, so 128-row
+    workgroups) against its first 16384 rows (256 workgroups of 64 rows, or, from m = 64 with a
+    fitted codebook, 128-row workgroups with half the batch tiles), with register tables (a
+    fitted 4-bit codebook) and with the LDS table (a 4-bit codebook that is not sign-symmetric,
+    and 8-bit codes)."""
     n, k = 16385, 3072
     bits = 8 if kind == "fitted8" else 4
     w, _, _ = prepare(64, 256, [8, 26, 0, 0])
@@ -485,7 +493,9 @@ def test_linear_stepped_narrow_equals_wide(kind):
         wide = L.linear_kernel(bits, m, k, n, cbh)
         narrow = L.linear_kernel(bits, m, k, n - 1, cbh)
         _say(f"stepped {kind} wide {wide} vs narrow {narrow}, k={k} m={m}")
-        assert wide.startswith("k_mfma2<") and narrow.startswith("k_mfma2_narrow<")
+        assert wide.startswith("k_mfma2<") and narrow != wide
+        # 12 steps of 256: one K part in both shapes
+        assert kind != "fitted4" or m >= 64 or narrow.startswith("k_mfma2_narrow<")
         x = torch.from_numpy(inputs.activations(m, k, seed=[8, 26, 1, m])).to(DEV)
         y = lin(x, c, cb)
         y1 = lin(x, c[: n - 1], cb)
