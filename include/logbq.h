@@ -183,8 +183,8 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  *               a common power-of-two scaling, exact in the result up to float16 rounding.
  *   y_dev     : device, [m][n] float32, written.
  * Accumulation is float32. Four kernels, chosen from (m, k, n) alone: for 2 <= m <= 32 and
- * k in {1024, 2048, 4096, 8192} (and m <= 48 at k = 14336, run as launches of at most 16
- * batch rows; there, as above m = 16, only for sign-symmetric codebooks), a split-K
+ * k in {1024, 2048, 4096, 8192} (and m <= 16 at k = 14336; there, as above m = 16, only for
+ * sign-symmetric codebooks), a split-K
  * dequantize-into-MFMA kernel takes 5 <= m <= 16,
  * m = 4 unless n <= 1024 at k = 8192, m = 3 at n >= 4096, and 17 <= m <= 32 unless m > 20 at
  * k = 8192 and n > 16384 (above m = 16 only for sign-symmetric codebooks; at k = 8192 above

@@ -1517,7 +1517,7 @@ __global__ __launch_bounds__(512) void k_mfma_kq8(const uint8_t* __restrict__ co
 // the same blocks and add their results into y with float atomics after y is zeroed (two terms
 // onto zero: the same sum in either order, so results stay deterministic). The alternative
 // of two launches (the second adding into y) measured 7-8 us slower at 8192 -> 28672.
-// K = 14336 (at most 16 batch rows per launch; G = 2 up to m = 8) takes the same K split over
+// K = 14336 (m <= 16; G = 2 up to m = 8) takes the same K split over
 // workgroup pairs of W = 14 wavefronts, ND = 16: 14336 -> 4096 at m = 4 / 8: 14.5 / 26.7 ->
 // 11.5 / 12.6 us against the split-row GEMV and the stepped kernel (one 16-wavefront workgroup
 // per block, ND = 28, measured 14.8 / 17.2 us: 256 blocks leave each workgroup one block, with
@@ -2430,11 +2430,14 @@ int32_t launch_kq(const uint16_t* x, int M, int K, const LinearJob& j, hipStream
 }
 
 // Split-K MFMA path: 4-bit codes, 2 <= m <= 32 at K in {1024, 2048, 4096, 8192}, and
-// 2 <= m <= 48 at K = 14336 (the down projection of the 8B-shaped decoder; above m = 16 as
-// launches of at most 16 batch rows).
+// 2 <= m <= 16 at K = 14336 (the down projection of the 8B-shaped decoder). Above m = 16 at
+// K = 14336 the stepped kernel in its cost-model shape is faster than split-K launches of at
+// most 16 batch rows each (4096 rows at m = 17 / 24 / 32 / 48: 26.4 / 28.7 / 31.4 / 46.6 ->
+// 21.0 / 21.0 / 21.0 / 27.2 us on MI355X); at the other K, split-K stays ahead to m = 24 and
+// even at m = 32 (e.g. 4096 x 4096 at m = 17: 9.0 vs 11.3 us).
 bool sk_shape(int M, int K) {
   return M >= 2 && ((M <= 32 && (K == 1024 || K == 2048 || K == 4096 || K == 8192)) ||
-                    (M <= 48 && K == 14336));
+                    (M <= 16 && K == 14336));
 }
 
 // Split-K configuration: code dwords per lane and row, wavefronts per workgroup, batch groups,
@@ -2474,7 +2477,7 @@ SkConfig sk_config(int M, int K, bool pairs, int blocks) {
 // Split-K launches for the linears jobs[idx[0..count)] of one call: when every codebook is
 // sign-symmetric (register dequantization), one grouped launch per distinct configuration,
 // otherwise one launch per linear (above m = 16, and at K = 14336, a codebook that is not
-// sign-symmetric takes the stepped MFMA kernel).
+// sign-symmetric takes the stepped MFMA kernel). At K = 14336, m <= 16.
 int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const int* idx,
                   int count, hipStream_t st, int cus) {
   SkSegs segs;
@@ -2491,28 +2494,6 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     sg.blk_begin = total;
     all_symmetric = make_lut_bytes(j.codebook, &sg.tb, &sg.scale) && all_symmetric;
     total += (int)((j.n + 15) / 16);
-  }
-  if (all_symmetric && K == 14336 && M > 16) {
-    // Two batch tiles at this K would need 128 activation registers per lane, so the batch
-    // runs as launches of at most 16 rows (x and y rows are contiguous; chunk sizes differ by
-    // at most one). Measured on MI355X, 14336 -> 4096 at m = 17 / 24 / 32 / 48: 46.5 / 46.7 /
-    // 46.6 / 54.7 -> 27.1 / 29.6 / 32.2 / 48.9 us against the stepped kernel with 64-row
-    // workgroups (2048 rows at m = 24 / 32: 46.4 / 46.5 -> 24.2 / 26.6 us).
-    const int nchunk = (M + 15) / 16;
-    LinearJob part[kMaxSegs];
-    int pidx[kMaxSegs];
-    for (int c = 0, m0 = 0; c < nchunk; ++c) {
-      const int mc = M / nchunk + (c < M % nchunk ? 1 : 0);
-      for (int a = 0; a < count; ++a) {
-        part[a] = jobs[idx[a]];
-        part[a].y = jobs[idx[a]].y + (int64_t)m0 * jobs[idx[a]].n;
-        pidx[a] = a;
-      }
-      const int32_t r = launch_sk(x + (int64_t)m0 * K, mc, K, part, pidx, count, st, cus);
-      if (r != LOGBQ_OK) return r;
-      m0 += mc;
-    }
-    return LOGBQ_OK;
   }
   auto launch = [&](int nseg, const SkSegs& sgs, int nblocks, bool pairs, const Lut16& l,
                     const SkConfig& c) -> int32_t {

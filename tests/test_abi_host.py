@@ -251,8 +251,8 @@ def test_linear_path_rule():
     assert lp(4, 17, 8192, 2048) == "splitk" and lp(4, 32, 8192, 16384) == "splitk"
     assert lp(4, 20, 8192, 28672) == "splitk" and lp(4, 21, 8192, 28672) == "mfma"
     assert lp(4, 32, 4096, 28672) == "splitk" and lp(4, 33, 4096, 4096) == "mfma"
-    assert lp(4, 4, 14336, 4096) == "splitk" and lp(4, 48, 14336, 4096) == "splitk"
-    assert lp(4, 49, 14336, 4096) == "mfma"
+    assert lp(4, 4, 14336, 4096) == "splitk" and lp(4, 16, 14336, 4096) == "splitk"
+    assert lp(4, 17, 14336, 4096) == "mfma" and lp(4, 48, 14336, 4096) == "mfma"
     assert lp(4, 96, 8192, 28672) == "mfma"
     # K-quartered MFMA GEMM: 4-bit, m > 96 at N >= 4096, unless the stepped kernel's 64-row
     # grid fits on the chip (ceil(N / 64) x ceil(m / 128) <= 256 workgroups)
@@ -321,7 +321,8 @@ def test_linear_kernel_names():
     assert lk(4, 32, 8192, 28672) == "k_mfma2<4, 2, 4, false, true>"
     assert lk(4, 128, 8192, 28672) == "k_mfma_kq"
     assert lk(4, 9, 14336, 4096) == "k_mfma_sk<16, 14, 1, 1, 2, false>"
-    assert lk(4, 17, 14336, 4096) == "k_mfma_sk<16, 14, 1, 1, 2, false>"   # first of 2 launches
+    assert lk(4, 16, 14336, 4096) == "k_mfma_sk<16, 14, 1, 1, 2, false>"
+    assert lk(4, 17, 14336, 4096) == "k_mfma2_narrow<4, 1, false, true>"
     # register tables: the cheapest launch shape whose grid fits on the chip (cost model)
     assert lk(4, 49, 14336, 4096) == "k_mfma2_narrow<4, 2, false, true>"
     assert lk(4, 64, 4096, 4096) == "k_mfma2_narrow<4, 1, false, true>"

@@ -277,7 +277,7 @@ def test_linear_deterministic_and_empty():
 def test_linear_arbitrary_codebook():
     """Any 16 finite floats work as a codebook (the table-lookup kernels); a fitted codebook is
     sign-symmetric and takes the register-dequant MFMA path, any other takes the pair table
-    (at K = 14336 above m = 16 the stepped kernel in one launch, not 16-row split-K launches)."""
+    (at K = 14336 above m = 16 the stepped kernel, as for fitted codebooks)."""
     rng = np.random.default_rng(12)
     n = 300
     for k in (1024, 2048, 4096, 8192, 14336):
@@ -408,9 +408,9 @@ def test_linear_split_k_14336():
     """Split-K at K = 14336 on 4099 rows (257 blocks of 16, so a workgroup pair takes two or
     three blocks and the last block has 3 rows): workgroup pairs of 14 wavefronts add their K
     halves into y with float atomics after zeroing it, with two batch groups up to m = 8 and
-    one above; above m = 16 the batch runs as launches of at most 16 rows. y is prefilled
-    with NaN (every output must be overwritten), each call is repeated and must give the same
-    bits, and a grouped call (4099 and the first 4096 rows) equals single calls."""
+    one above; above m = 16 the stepped kernel runs (64-row workgroups, K in two parts). y is
+    prefilled with NaN (every output must be overwritten), each call is repeated and must give
+    the same bits, and a grouped call (4099 and the first 4096 rows) equals single calls."""
     n, k = 4099, 14336
     w, p, r = prepare(n, k, [8, 23, 1, 0])
     c, cb = gpu_encode(w, p)
@@ -418,7 +418,8 @@ def test_linear_split_k_14336():
     del w
     c2 = c[:4096]
     for m in (3, 4, 5, 8, 9, 12, 16, 17, 33, 48):
-        assert L.linear_path(4, m, k, n) == "splitk" and L.linear_path(4, m, k, 4096) == "splitk"
+        path = "splitk" if m <= 16 else "mfma"
+        assert L.linear_path(4, m, k, n) == path and L.linear_path(4, m, k, 4096) == path
         _say(f"split-K k={k} m={m} kernel {L.linear_kernel(4, m, k, n)}")
         x = inputs.activations(m, k, seed=[8, 23, 2, m])
         xd = torch.from_numpy(x).to(DEV)
