@@ -194,14 +194,13 @@ int32_t logbq_encode(const float* w_dev, int64_t n, int64_t k, const logbq_param
  * runs for m <= 8 unless m >= 3 and m * n > 65536; everything else (and shapes whose
  * activations do not fit the GEMV's registers) runs the stepped dequantize-into-MFMA skinny
  * GEMM, except m > 96 at n >= 4096, which runs a K-quartered MFMA GEMM for sign-symmetric
- * codebooks unless ceil(n / 64) * ceil(m / 128) <= 256. For 8-bit codes and codebooks that
- * are not sign-symmetric the stepped kernel runs with 64-row workgroups wherever its whole
- * grid is then on the chip at once (ceil(n / 64) times its batch blocks of 64 rows, at most
- * 256), else 128-row ones. For sign-symmetric codebooks it runs in the launch shape a cost
- * model rates cheapest among those whose grid is on the chip at once: 64- or 128-row
- * workgroups, batch blocks of 16 to 128 rows, and K in one part or (from k = 4096) in two,
- * where y is zeroed first and each part adds into it. logbq_linear_path reports the path, and
- * logbq_linear_kernel the kernel. Results are deterministic for every path.
+ * codebooks unless ceil(n / 64) * ceil(m / 128) <= 256. The stepped kernel runs in the launch
+ * shape a cost model rates cheapest among those whose grid is on the chip at once (at most 256
+ * workgroups): 64- or 128-row workgroups, batch blocks of 16 to 128 rows (to 64 for 8-bit codes
+ * and codebooks that are not sign-symmetric), and K in one part or (from k = 4096) in two,
+ * where y is zeroed first and each part adds into it; with none that fits, 128-row workgroups
+ * with the largest batch blocks. logbq_linear_path reports the path, and logbq_linear_kernel
+ * the kernel. Results are deterministic for every path.
  * k == 0 writes zeros. Errors: INVALID_ARG, UNSUPPORTED (k % 32, alignment, or k >= 2^24 on
  * the stepped or K-quartered MFMA kernel), HIP.
  */
@@ -249,7 +248,8 @@ int32_t logbq_dequantize(const uint8_t* codes_dev, int64_t n, int64_t k, const f
  * takes 5 <= m <= 8 unless n <= 1024 at k >= 4096, m = 3, 4 at n >= 8192, and 9 <= m <= 16
  * unless n > 16384 at k = 8192; otherwise the GEMV runs for m <= 8 unless m >= 5 and
  * m * n > 65536, a K-quartered MFMA GEMM for m > 64 at n >= 16384, and the stepped
- * dequantize-into-MFMA skinny GEMM for the rest.
+ * dequantize-into-MFMA skinny GEMM for the rest, in its cost-model launch shape (as for
+ * logbq_linear; with K in two parts y is zeroed first). Results are deterministic.
  * Errors: as logbq_linear.
  */
 int32_t logbq_linear8(const uint16_t* x_dev, int64_t m, int64_t k, const uint8_t* codes_dev,

@@ -251,10 +251,15 @@ __global__ __launch_bounds__(256) void k_dequant8(const uint32_t* __restrict__ c
   }
 }
 
+// y[0 .. count) = 0 with 16-byte stores (y is 16-byte aligned); the count % 4 floats of the
+// tail are written by the first threads.
 __global__ __launch_bounds__(256) void k_fill_zero(float* __restrict__ y, int64_t count) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
-    y[i] = 0.0f;
+  const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n4 = count >> 2;
+  f32x4* y4 = reinterpret_cast<f32x4*>(y);
+  for (int64_t i = t0; i < n4; i += stride) y4[i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  if (t0 < (count & 3)) y[(n4 << 2) + t0] = 0.0f;
 }
 
 // ------------------------------------------------------------------ shared device helpers
@@ -2105,6 +2110,12 @@ int64_t grid_for(int64_t items, int64_t per_block, int64_t cap) {
   return g;
 }
 
+// Zeroes y[0 .. count) on the stream (one 16-byte store per thread and pass).
+void fill_zero(float* y, int64_t count, int cus, hipStream_t st) {
+  hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)grid_for((count + 3) / 4, 256, (int64_t)cus * 4)),
+                     dim3(256), 0, st, y, count);
+}
+
 template <int BITS, int M, int CPL>
 void launch_gemv(int grid, hipStream_t st, const uint16_t* x, int k, int wk, int stage_x,
                  const GemvSegs<BITS>& segs) {
@@ -2227,8 +2238,8 @@ constexpr int64_t kMaxBatchRows = 65535LL * 64;
 // 4096 x 4096 at m = 48: 40.9 -> 27.0 us, 8192 x 8192 at m = 64: 86.0 -> 59.1 us; 4-bit
 // 4096 x 4096 at m = 64: 30.1 -> 21.0 us); at N = 28672 (448 workgroups) 1.04-1.44 times the
 // time. `cap` is the kernel's batch tiles per workgroup column (8 with register tables, 4 with
-// the LDS table). With register tables this rule now only decides between the stepped and the
-// K-quartered kernel; step_config below picks the stepped kernel's shape.
+// the LDS table). This rule now decides between the stepped and the K-quartered kernel, and is
+// what step_config below falls back to where no launch shape fits on the chip.
 constexpr int64_t kNarrowMaxWorkgroups = 256;
 bool narrow_fits(int M, int64_t N, int cap = 8) {
   const int64_t gy = M > 16 * cap ? (M + 16 * cap - 1) / (16 * cap) : 1;
@@ -2243,31 +2254,34 @@ struct StepCfg {
   int mt16;
   int ks;
 };
-// Codebooks that take the LDS table keep the rule above: batch tiles up to the cap, 64-row
-// workgroups when their grid fits on the chip, one K part. With register tables (sign-symmetric
-// 4-bit codebooks) the shape is the cheapest, by a cost model, of every shape whose grid fits
-// on the chip at once (at most one workgroup per CU): 64 or 128 rows, t = t0, t0 / 2, ... 1
-// batch tiles (halving rounds up; t0 = min(ceil(m / 16), 8)), one K part, or two when K has at
-// least 16 steps of 256. A workgroup's time is its steps times a per-step time that grows with
-// t (activation staging, MFMAs and LDS reads) on top of a fixed part (code loads and
-// dequantization); two K parts add a fixed cost (the zeroing launch, the atomic adds, a shorter
-// pipeline). The constants are fitted to MI355X measurements (graph replay, codes streamed from
-// HBM) of 64- and 128-row workgroups at t = 1 .. 8 on 14336 x 4096, 4096 x 14336, 4096 x 4096,
-// 2048 x 8192 and 1024 x 4096. Against 64-row workgroups with all t0 tiles and one K part,
-// e.g.: 4096 x 14336 at m = 128 (128 rows, t = 2, two parts) 109.9 -> 35.9 us, at m = 64
-// (64 rows, t = 2, two parts) 65.1 -> 27.8 us; 4096 x 4096 at m = 256 (128 rows, t = 2)
-// 34.8 -> 20.1 us; 14336 x 4096 at m = 128 (128 rows, t = 4) 37.2 -> 30.3 us; 2048 x 8192 at
-// m = 64 (64 rows, t = 1, two parts) 38.3 -> 13.7 us. Where no shape fits (N = 28672) the rule
-// above stands.
-constexpr double kStepFixed128 = 0.500, kStepTile128 = 0.300;   // us per step of 256
-constexpr double kStepFixed64 = 0.376, kStepTile64 = 0.184;
-constexpr double kTwoPartsCost = 5.0;                            // us
-StepCfg step_config(int M, int64_t N, int K, bool symmetric) {
-  const int cap = symmetric ? 8 : 4;
+// The shape is the cheapest, by a cost model, of every shape whose grid fits on the chip at
+// once (at most one workgroup per CU): 64 or 128 rows, t = t0, t0 / 2, ... 1 batch tiles
+// (halving rounds up; t0 = ceil(m / 16) up to the cap: 8 with register tables, 4 with the LDS
+// table), one K part, or two when K has at least 16 steps of 256. A workgroup's time is its
+// steps times a per-step time that grows with t (activation staging, MFMAs and LDS reads) on
+// top of a fixed part (code loads and dequantization); two K parts add a fixed cost (the
+// zeroing launch, the atomic adds, a shorter pipeline). The constants are least-squares fits to
+// MI355X measurements (graph replay, codes streamed from HBM) of 64- and 128-row workgroups at
+// every t on 4096 x 14336, 4096 x 4096, 14336 x 4096 and 2048 x 8192 (plus 1024 x 4096 for
+// register tables), one set per kind of dequantization. Against 64-row workgroups with all t0
+// tiles and one K part (the rule above), e.g.: 4096 x 14336 at m = 128, register tables
+// (128 rows, t = 2, two parts) 109.9 -> 35.9 us; at m = 64, 8-bit codes (64 rows, t = 2, two
+// parts) 93.1 -> 34.4 us; 2048 x 8192 at m = 64, a 4-bit LDS table (64 rows, t = 1, two parts)
+// 38.4 -> 13.5 us; 14336 x 4096 at m = 128, register tables (128 rows, t = 4, one part)
+// 37.2 -> 30.3 us. Where no shape fits (N = 28672) the rule above stands.
+struct StepCosts {
+  double fixed64, tile64, fixed128, tile128, two_parts;   // us per step of 256; us
+};
+constexpr StepCosts kCostsRegister = {0.376, 0.184, 0.500, 0.300, 5.0};
+constexpr StepCosts kCostsTable4 = {0.283, 0.198, 0.205, 0.374, 3.1};
+constexpr StepCosts kCostsTable8 = {0.422, 0.279, 0.156, 0.600, 3.0};
+StepCfg step_config(int M, int64_t N, int K, int bits, bool symmetric) {
+  const bool reg = bits == 4 && symmetric;
+  const int cap = reg ? 8 : 4;
   int t0 = (M + 15) / 16;
   if (t0 > cap) t0 = cap;
   StepCfg best{narrow_fits(M, N, cap), t0, 1};
-  if (!symmetric) return best;
+  const StepCosts& cc = reg ? kCostsRegister : bits == 4 ? kCostsTable4 : kCostsTable8;
   const int64_t nsteps = ((int64_t)K + kM2Step - 1) / kM2Step;
   double best_cost = -1.0;
   for (int rows = 128; rows >= 64; rows /= 2)
@@ -2275,10 +2289,10 @@ StepCfg step_config(int M, int64_t N, int K, bool symmetric) {
       for (int ks = 1; ks <= (nsteps >= 16 ? 2 : 1); ++ks) {
         const int64_t wgs = ((N + rows - 1) / rows) * ((M + 16 * mt - 1) / (16 * mt)) * ks;
         if (wgs > kNarrowMaxWorkgroups) continue;
-        const double per_step = rows == 128 ? kStepFixed128 + mt * kStepTile128
-                                            : kStepFixed64 + mt * kStepTile64;
+        const double per_step = rows == 128 ? cc.fixed128 + mt * cc.tile128
+                                            : cc.fixed64 + mt * cc.tile64;
         const double cost = (double)((nsteps + ks - 1) / ks) * per_step +
-                            (ks == 2 ? kTwoPartsCost : 0.0);
+                            (ks == 2 ? cc.two_parts : 0.0);
         if (best_cost < 0.0 || cost < best_cost) {
           best_cost = cost;
           best = {rows == 64, mt, ks};
@@ -2304,7 +2318,7 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
   make_lut<BITS>(j.codebook, &lut, &scale);
   // Batch tiles of 16 rows: up to 8 per workgroup column (128 rows). Up to 4 tiles use the
   // LDS table; more tiles leave LDS to the activation ring and dequantize in registers.
-  const StepCfg cfg = step_config(M, N, K, symmetric);
+  const StepCfg cfg = step_config(M, N, K, BITS, symmetric);
   const int mt16 = cfg.mt16;
   const bool narrow = cfg.narrow;
   const int rows_wg = narrow ? 64 : 128;
@@ -2313,9 +2327,7 @@ int32_t launch_mfma(const uint16_t* x, int M, int K, const LinearJob& j, hipStre
   if (cfg.ks > 1) {
     const int cus = device_cus();
     if (cus <= 0) return LOGBQ_ERR_HIP;
-    const int64_t cnt = (int64_t)M * N;
-    hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)grid_for(cnt, 256, (int64_t)cus * 16)),
-                       dim3(256), 0, st, j.y, cnt);
+    fill_zero(j.y, (int64_t)M * N, cus, st);
   }
 #define LOGBQ_M2(MT, ST, PR) hipLaunchKernelGGL((k_mfma2<BITS, MT, ST, PR, (MT <= 2)>), grid, dim3(512), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
 #define LOGBQ_M2N(MT, PR) hipLaunchKernelGGL((k_mfma2_narrow<BITS, MT, PR, (MT <= 2)>), grid, dim3(256), 0, st, j.codes, x, j.y, N, K, M, tb, lut, scale)
@@ -2502,11 +2514,7 @@ int32_t launch_sk(const uint16_t* x, int M, int K, const LinearJob* jobs, const 
     int grid = nblocks * c.kparts < cus ? nblocks * c.kparts : cus;
     grid -= grid % c.kparts;
     if (c.kparts == 2)
-      for (int a = 0; a < nseg; ++a) {
-        const int64_t cnt = (int64_t)M * sgs.s[a].n_rows;
-        hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)grid_for(cnt, 256, (int64_t)cus * 16)),
-                           dim3(256), 0, st, sgs.s[a].y, cnt);
-      }
+      for (int a = 0; a < nseg; ++a) fill_zero(sgs.s[a].y, (int64_t)M * sgs.s[a].n_rows, cus, st);
 #define LOGBQ_SK(ND, W, GG, TT, KP, PR)                                                          \
   if (c.nd == ND && c.waves == W && c.groups == GG && c.tiles == TT && c.kparts == KP &&         \
       pairs == PR) {                                                                             \
@@ -2637,9 +2645,7 @@ int32_t run_linears(const uint16_t* x, int64_t m, int64_t k, const LinearJob* jo
   if (k == 0) {
     for (int a = 0; a < nlive; ++a) {
       const LinearJob& j = jobs[live[a]];
-      const int64_t cnt = m * j.n;
-      hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)grid_for(cnt, 256, (int64_t)cus * 16)),
-                         dim3(256), 0, st, j.y, cnt);
+      fill_zero(j.y, m * j.n, cus, st);
       if (launch_status() != LOGBQ_OK) return LOGBQ_ERR_HIP;
     }
     return LOGBQ_OK;
@@ -3137,7 +3143,7 @@ int32_t logbq_linear_kernel(int32_t bits, int64_t m, int64_t k, int64_t n, const
     } else if (path == LOGBQ_PATH_MFMA_KQ && symmetric) {
       std::snprintf(buf, sizeof(buf), "k_mfma_kq");
     } else {
-      const StepCfg cfg = step_config(M, n, K, symmetric);
+      const StepCfg cfg = step_config(M, n, K, bits, symmetric);
       const int mt16 = cfg.mt16;
       if (cfg.narrow)
         std::snprintf(buf, sizeof(buf), "k_mfma2_narrow<%d, %d, %s, %s>", bits, mt16,

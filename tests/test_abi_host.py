@@ -280,21 +280,27 @@ def test_linear_path_rule():
 
 
 def test_stepped_shape_rule():
-    """The library's stepped-kernel launch shapes agree with the rule stated above on every
-    shape of a grid (ragged n, k from 1 to 56 steps, m from 3 to 256) that takes that kernel,
-    and every chosen grid fits on the chip when one can."""
-    seen = set()
-    for k in (1024, 2048, 3072, 4096, 8192, 14336):
-        for n in (64, 1000, 2048, 4097, 8192, 14336, 16385, 28672):
-            for m in (3, 9, 17, 33, 48, 64, 65, 96, 97, 128, 129, 200, 256):
-                if L.linear_path(4, m, k, n) != "mfma":
-                    continue
-                assert L.linear_kernel(4, m, k, n) == stepped_name(m, k, n), (m, k, n)
-                narrow, t, parts = stepped_shape(m, k, n)
-                wgs = -(-n // (64 if narrow else 128)) * -(-m // (16 * t)) * parts
-                assert wgs <= 256 or (-(-n // 128)) * -(-m // 128) > 256 or not narrow
-                seen.add((narrow, parts))
-    assert seen == {(True, 1), (True, 2), (False, 1), (False, 2)}
+    """The library's stepped-kernel launch shapes agree with the rule stated in stepped_rule on
+    every shape of a grid (ragged n, k from 1 to 56 steps, m from 3 to 256) that takes that
+    kernel, for register tables, the 4-bit LDS table and 8-bit codes, and each rule reaches
+    every kind of shape (64- and 128-row workgroups, one and two K parts)."""
+    table = np.linspace(-0.07, 0.08, 16, dtype=np.float32)     # not sign-symmetric
+    for kind in ("register", "table4", "bits8"):
+        bits = 8 if kind == "bits8" else 4
+        cb = table if kind == "table4" else None
+        seen = set()
+        for k in (1024, 2048, 3072, 4096, 8192, 14336):
+            for n in (64, 1000, 2048, 4097, 8192, 14336, 16385, 28672):
+                for m in (3, 9, 17, 33, 48, 64, 65, 96, 97, 128, 129, 200, 256):
+                    if L.linear_path(bits, m, k, n) not in ("mfma", "mfma_kq"):
+                        continue
+                    name = L.linear_kernel(bits, m, k, n, cb)
+                    if name.startswith("k_mfma_kq") or name.startswith("k_mfma_sk"):
+                        continue
+                    assert name == stepped_name(m, k, n, kind), (kind, m, k, n)
+                    narrow, t, parts = stepped_shape(m, k, n, kind)
+                    seen.add((narrow, parts))
+        assert seen == {(True, 1), (True, 2), (False, 1), (False, 2)}, kind
 
 
 def test_linear_kernel_names():
@@ -339,19 +345,19 @@ def test_linear_kernel_names():
         assert lk(4, m, k, n) == stepped_name(m, k, n), (m, k, n)
     assert lk(8, 1, 8192, 28672) == "k_gemv<8, 1, 8, false, 2>"
     assert lk(8, 128, 8192, 28672) == "k_mfma_kq8" and lk(8, 128, 4096, 14336) == "k_mfma2<8, 4, 4, true, false>"
-    assert lk(8, 64, 4096, 14336) == "k_mfma2_narrow<8, 4, true, false>"
+    assert lk(8, 64, 4096, 14336) == "k_mfma2<8, 2, 4, true, true>"
     assert lk(8, 32, 8192, 28672) == "k_mfma2<8, 2, 4, true, true>"
     assert lk(8, 8, 8192, 28672) == "k_mfma_sk8<16, 2>" and lk(8, 12, 4096, 4096) == "k_mfma_sk8<8, 1>"
     assert lk(4, 0, 8192, 28672) == "none" and lk(4, 3, 0, 5) == "k_fill_zero"
     # a codebook that is not sign-symmetric takes the LDS table
     cb = np.arange(16, dtype=np.float32)
     assert lk(4, 8, 8192, 28672, cb) == "k_mfma_sk<32, 8, 1, 1, 1, true>"
-    assert lk(4, 32, 4096, 14336, cb) == "k_mfma2_narrow<4, 2, true, true>"   # above m = 16
+    assert lk(4, 32, 4096, 14336, cb) == "k_mfma2<4, 1, 4, true, true>"   # above m = 16
     assert lk(4, 4, 14336, 4096, cb) == "k_mfma2_narrow<4, 1, true, true>"    # and at K = 14336
     assert lk(4, 128, 8192, 28672, cb) == "k_mfma2<4, 4, 4, true, false>"
-    assert lk(4, 64, 4096, 4096, cb) == "k_mfma2_narrow<4, 4, true, false>"
+    assert lk(4, 64, 4096, 4096, cb) == "k_mfma2_narrow<4, 1, true, true>"
     assert lk(4, 65, 4096, 16384, cb) == "k_mfma2<4, 4, 4, true, false>"   # two 64-row blocks
-    assert lk(4, 64, 4096, 16384, cb) == "k_mfma2_narrow<4, 4, true, false>"
+    assert lk(4, 64, 4096, 16384, cb) == "k_mfma2<4, 2, 4, true, true>"
     sym = np.array([0] + [2.0 ** k for k in range(1, 8)] + [0] + [-(2.0 ** k) for k in range(1, 8)],
                    dtype=np.float32)
     assert lk(4, 128, 8192, 28672, sym) == "k_mfma_kq"

@@ -469,6 +469,45 @@ def test_linear_stepped_shapes():
     assert parts_seen == {(True, 1), (True, 2), (False, 1), (False, 2)}
 
 
+@pytest.mark.parametrize("kind", ["table4", "bits8"])
+def test_linear_stepped_shapes_lds_table(kind):
+    """The stepped kernel with the LDS table (a 4-bit codebook that is not sign-symmetric, and
+    8-bit codes) in the launch shapes its cost model picks, 64- and 128-row workgroups and K in
+    one or two parts, on ragged row counts: each call is repeated and must give the same bits,
+    and every output is within tolerance of the oracle's product with the dequantized codes."""
+    rng = np.random.default_rng(31)
+    bits = 8 if kind == "bits8" else 4
+    seen = set()
+    for n, k in ((1000, 3072), (1000, 8192), (2049, 8192)):
+        codes_np = rng.integers(0, 1 << bits, size=(n, k), dtype=np.uint8)
+        if bits == 8:
+            cb = (rng.standard_normal(256) * 0.01).astype(np.float32)
+            codes = torch.from_numpy(codes_np).to(DEV)
+        else:
+            cb = (rng.standard_normal(16) * 0.01).astype(np.float32)
+            codes = torch.from_numpy(O.pack(codes_np)).to(DEV)
+        wh = O.dequantize(codes_np, cb)
+        lin = L.linear8 if bits == 8 else L.linear
+        for m in (33, 64, 97, 128, 200):
+            if L.linear_path(bits, m, k, n) != "mfma":
+                continue
+            name = L.linear_kernel(bits, m, k, n, cb)
+            narrow, tiles, parts = stepped_shape(m, k, n, kind)
+            _say(f"stepped {kind} n={n} k={k} m={m} kernel {name} K parts {parts}")
+            assert name == stepped_name(m, k, n, kind), name
+            seen.add((narrow, parts))
+            x = inputs.activations(m, k, seed=[8, 31, n, m])
+            xd = torch.from_numpy(x).to(DEV)
+            y = torch.full((m, n), float("nan"), dtype=torch.float32, device=DEV)
+            lin(xd, codes, cb, out=y)
+            y2 = lin(xd, codes, cb)
+            torch.cuda.synchronize()
+            assert torch.isfinite(y).all()
+            assert torch.equal(y, y2)
+            assert rel_err(y.cpu().numpy(), x, wh) <= TOL
+    assert (True, 2) in seen and (False, 2) in seen and (True, 1) in seen
+
+
 @pytest.mark.parametrize("kind", ["fitted4", "table4", "fitted8"])
 def test_linear_stepped_narrow_equals_wide(kind):
     """With K in one part every launch shape gives every output the same K walk, so shapes
