@@ -2286,7 +2286,11 @@ StepCfg step_config(int M, int64_t N, int K, int bits, bool symmetric) {
   double best_cost = -1.0;
   for (int rows = 128; rows >= 64; rows /= 2)
     for (int mt = t0;; mt = (mt + 1) / 2) {
-      for (int ks = 1; ks <= (nsteps >= 16 ? 2 : 1); ++ks) {
+      // 8-bit codes in 128-row workgroups with one batch tile take far longer than the linear
+      // fit says (4096 -> 14336 at m = 128: 73.4 us, against 48.7 with two tiles and two K
+      // parts); those shapes are left out.
+      for (int ks = 1; ks <= (nsteps >= 16 ? 2 : 1) && !(bits == 8 && rows == 128 && mt == 1);
+           ++ks) {
         const int64_t wgs = ((N + rows - 1) / rows) * ((M + 16 * mt - 1) / (16 * mt)) * ks;
         if (wgs > kNarrowMaxWorkgroups) continue;
         const double per_step = rows == 128 ? cc.fixed128 + mt * cc.tile128

@@ -16,8 +16,9 @@ def stepped_shape(m, k, n, kind="register"):
     """(64-row workgroups, batch tiles per workgroup column, K parts). Every shape whose grid
     has at most 256 workgroups competes on (steps per workgroup) x (per-step time), plus the
     cost of two K parts (allowed from 16 steps of 256); t runs t0, ceil(t0 / 2), ... 1 with
-    t0 = min(ceil(m / 16), cap), cap 8 for register tables and 4 otherwise. With no shape that
-    fits: 128-row workgroups with t0 tiles, unless 64-row ones fit."""
+    t0 = min(ceil(m / 16), cap), cap 8 for register tables and 4 otherwise; 8-bit codes never
+    take 128-row workgroups with one tile. With no shape that fits: 128-row workgroups with t0
+    tiles, unless 64-row ones fit."""
     f64, t64, f128, t128, two = COSTS[kind]
     cap = 8 if kind == "register" else 4
     t0 = min(-(-m // 16), cap)
@@ -28,6 +29,8 @@ def stepped_shape(m, k, n, kind="register"):
         t = t0
         while True:
             for parts in ((1, 2) if steps >= 16 else (1,)):
+                if kind == "bits8" and rows == 128 and t == 1:
+                    continue     # left out for 8-bit codes
                 if -(-n // rows) * -(-m // (16 * t)) * parts > 256:
                     continue
                 per = f128 + t128 * t if rows == 128 else f64 + t64 * t
